@@ -1,0 +1,90 @@
+"""The five chunk workloads and the per-layer parameter naming.
+
+Shapes follow the paper's setting of a decoder split into chunks of
+consecutive layers (Sec. II.A, Eq. (1)); the concrete widths are the
+GPT-2-small, Llama-1B and Llama-3-8B shapes plus a tiny parity model.
+"""
+from dataclasses import dataclass, replace
+
+
+@dataclass(frozen=True)
+class ChunkShape:
+    name: str
+    arch: str            # "llama" (RMSNorm, RoPE, SwiGLU) or "gpt2" (LayerNorm, GELU, biases)
+    n_layers: int        # layers in the chunk
+    d_model: int
+    n_heads: int
+    n_kv_heads: int
+    head_dim: int
+    d_ff: int
+    vocab: int
+    batch: int
+    seq: int
+    dtype: str           # "f32" or "bf16" (bf16 compute, fp32 master/grad/state)
+    rope_theta: float
+    n_chunks: int        # chunks the whole model is split into
+    norm_eps: float = 1e-5
+
+    @property
+    def tokens(self):
+        return self.batch * self.seq
+
+    def with_(self, **kw):
+        return replace(self, **kw)
+
+
+CONFIGS = {
+    "tiny": ChunkShape("tiny", "llama", 2, 64, 4, 4, 16, 256, 256, 4, 32, "f32", 1e4, 2),
+    "gpt2": ChunkShape("gpt2", "gpt2", 3, 768, 12, 12, 64, 3072, 50257, 8, 512, "bf16", 0.0, 4),
+    "1b": ChunkShape("1b", "llama", 4, 2048, 32, 8, 64, 8192, 128256, 4, 2048, "bf16", 5e5, 4),
+    "1b-long": ChunkShape("1b-long", "llama", 4, 2048, 32, 8, 64, 8192, 128256, 1, 8192, "bf16", 5e5, 4),
+    "8b": ChunkShape("8b", "llama", 8, 4096, 32, 8, 128, 14336, 128256, 4, 4096, "bf16", 5e5, 4),
+}
+
+
+def get_config(name, **overrides):
+    cfg = CONFIGS[name]
+    return cfg.with_(**overrides) if overrides else cfg
+
+
+def param_specs(cfg):
+    """Trainable tensors of one chunk, in order: list of (key, shape, kind).
+
+    key is "L{layer}.{name}"; kind is one of "norm_w", "norm_b", "weight",
+    "bias".  Linear weights are [out, in] (y = x W^T, as in Eq. (2)).
+    """
+    d, hd = cfg.d_model, cfg.head_dim
+    dq, dkv, ff = cfg.n_heads * hd, cfg.n_kv_heads * hd, cfg.d_ff
+    out = []
+    for l in range(cfg.n_layers):
+        p = f"L{l}."
+        if cfg.arch == "llama":
+            out += [
+                (p + "ln1_w", (d,), "norm_w"),
+                (p + "wq", (dq, d), "weight"),
+                (p + "wk", (dkv, d), "weight"),
+                (p + "wv", (dkv, d), "weight"),
+                (p + "wo", (d, dq), "weight"),
+                (p + "ln2_w", (d,), "norm_w"),
+                (p + "wg", (ff, d), "weight"),
+                (p + "wu", (ff, d), "weight"),
+                (p + "wd", (d, ff), "weight"),
+            ]
+        elif cfg.arch == "gpt2":
+            out += [
+                (p + "ln1_w", (d,), "norm_w"),
+                (p + "ln1_b", (d,), "norm_b"),
+                (p + "wqkv", (dq + 2 * dkv, d), "weight"),
+                (p + "bqkv", (dq + 2 * dkv,), "bias"),
+                (p + "wo", (d, dq), "weight"),
+                (p + "bo", (d,), "bias"),
+                (p + "ln2_w", (d,), "norm_w"),
+                (p + "ln2_b", (d,), "norm_b"),
+                (p + "wfc", (ff, d), "weight"),
+                (p + "bfc", (ff,), "bias"),
+                (p + "wproj", (d, ff), "weight"),
+                (p + "bproj", (d,), "bias"),
+            ]
+        else:
+            raise ValueError(cfg.arch)
+    return out
