@@ -1,0 +1,222 @@
+"""Benchmark: chunk-local update tokens/s on one MI355X, and MFMA utilisation.
+
+One step = one whole zl_chunk_update (forward, local objective on the frozen
+head, chunk-local backward, AdamW step) over one synthetic micro-batch whose
+inputs are already resident in HBM.  Default workload: the Llama-3-8B-shaped
+chunk (8 layers, d 4096, 32/8 heads x 128, MLP 14336, vocab 128256),
+B = 4, S = 4096, bf16 with fp32 master weights, alpha = 0.5.
+
+Prints one JSON line.  `roofline` covers the kernel with the largest share
+of the step time (timed with HIP events on the launch stream inside the
+timed steps); `cpu_baseline` times the fp64 oracle on a bounded slice of the
+same workload on the host.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "chunk-local update tokens/sec on 1 MI355X; MFMA util % of bf16 peak"
+PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16: 256 CU x 2.4 GHz x 4096 FLOP/clk/CU
+PEAK_HBM_GBS = 8000.0
+
+
+def algorithmic_flops(shp, T, S, alpha):
+    """FLOPs the method must compute per update (no recompute counted):
+    6 * P_lin * T for the chunk linears (forward, dgrad, wgrad); causal
+    attention 2 * d_q * (S + 1) per token forward and twice that backward;
+    head: readout of h_out, readout of h_in (alpha < 1), and the dgrad into
+    h_out, 2 * d * V per token each (the head is frozen: no wgrad)."""
+    d, hd, ff = shp.d_model, shp.head_dim, shp.d_ff
+    dq, dkv = shp.n_heads * hd, shp.n_kv_heads * hd
+    if shp.arch == "llama":
+        p_lin = d * (dq + 2 * dkv) + dq * d + 3 * d * ff
+    else:
+        p_lin = d * (dq + 2 * dkv) + dq * d + 2 * d * ff
+    lin = 6.0 * p_lin * T * shp.n_layers
+    attn = 3.0 * 2.0 * dq * (S + 1) * T * shp.n_layers
+    head = (3.0 if alpha < 1.0 else 2.0) * 2.0 * d * shp.vocab * T
+    return lin + attn + head, dict(linear=lin, attention=attn, head=head)
+
+
+def cpu_baseline(shp, alpha, seconds_hint=30.0):
+    """The oracle, as it stands, on one layer of the chunk at full width with
+    the full head, B = 1, S = 256; scaled to the whole chunk as
+    t_head + n_layers * (t_slice - t_head)."""
+    import numpy as np
+    import oracle
+    import workload
+    from oracle.chunk import init_opt_state
+    from oracle.objective import local_objective_ref
+    S = 256
+    sl = shp.with_(n_layers=1, batch=1, seq=S)
+    params = workload.init_params(workload.param_specs(sl), seed=0)
+    batch = workload.make_batch(sl)
+    cfg = oracle.OracleConfig.from_shape(sl, alpha=alpha)
+    mb = dict(h_in=batch["h_in"], labels=batch["labels"])
+    t0 = time.perf_counter()
+    r = oracle.chunk_update_ref(cfg, params, init_opt_state(), [mb], batch["head_w"],
+                                batch["head_norm_w"], batch["head_norm_b"])
+    t_slice = time.perf_counter() - t0
+    h = r["runs"][0]["h_out"].reshape(S, -1)
+    t0 = time.perf_counter()
+    local_objective_ref(h, batch["h_in"].reshape(S, -1), batch["labels"].reshape(-1),
+                        oracle.bf16_round(batch["head_w"]), sl.arch, batch["head_norm_w"],
+                        batch["head_norm_b"], sl.norm_eps, alpha, "reverse")
+    t_head = time.perf_counter() - t0
+    t_layer = max(t_slice - t_head, 1e-9)
+    t_full = t_head + shp.n_layers * t_layer
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cores = os.cpu_count()
+    threads = int(os.environ.get("OMP_NUM_THREADS", cores) or cores)
+    return {"value": S / t_full, "unit": "tokens/s", "cores": min(cores, threads), "kind": "oracle",
+            "sample": (f"fp64 NumPy oracle, one update of 1 of {shp.n_layers} layers at full "
+                       f"width with the full head and AdamW, B=1 S={S} ({t_slice:.1f} s, head "
+                       f"{t_head:.1f} s); scaled to the {shp.n_layers}-layer chunk as "
+                       f"t_head + L*t_layer = {t_full:.1f} s per {S} tokens")}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="8b")
+    ap.add_argument("--alpha", type=float, default=0.5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-json", default=None, help="write the per-kernel profile here")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py: this build runs one chunk on one GPU; --gpus {args.gpus} "
+              f"(WORLD_SIZE={world}) is not supported. A K-GPU pipeline would run one "
+              "chunk per GPU and exchange only hidden states.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import workload
+    from paper_2608_07974_amd import zl
+    from paper_2608_07974_amd.chunk import TorchChunk, config_from_shape, current_stream
+
+    shp = workload.get_config(args.config)
+    B, S = shp.batch, shp.seq
+    T = B * S
+    dev = torch.device("cuda:0")
+    torch.manual_seed(0)
+    cfg = config_from_shape(shp, alpha=args.alpha)
+    ch = TorchChunk(cfg, device=dev)
+    # random-init weights of the architecture, on device: N(0, 0.02) linears,
+    # norm weights 1, biases 0; frozen head N(0, 0.02), head norm 1 / 0
+    ch.master.normal_(0.0, 0.02)
+    for t in ch.layout:
+        v = ch.view(ch.master, f"L{t['layer']}.{t['name']}")
+        if t["name"].startswith("ln") and t["name"].endswith("_w"):
+            v.fill_(1.0)
+        elif len(t["shape"]) == 1:
+            v.zero_()
+    ch.head_w.normal_(0.0, 0.02)
+    zl.zl_refresh_shadow(ch.handle, current_stream())
+    tokens = workload.zipf_tokens(B, S, shp.vocab, seed=1) if shp.vocab > 256 else \
+        workload.uniform_tokens(B, S, shp.vocab, seed=1)
+    labels = torch.tensor(workload.labels_from_tokens(tokens), device=dev)
+    table = torch.empty(shp.vocab, shp.d_model, dtype=ch.dtype, device=dev).normal_(0.0, 0.02)
+    h_in = table[torch.tensor(tokens, device=dev, dtype=torch.long)].contiguous()
+    if shp.arch == "gpt2":
+        pos = torch.empty(S, shp.d_model, dtype=ch.dtype, device=dev).normal_(0.0, 0.02)
+        h_in = (h_in + pos[None]).contiguous()
+    del table
+    h_out = torch.empty_like(h_in)
+    torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        ch.update(h_in, labels, h_out=h_out)
+    torch.cuda.synchronize()
+    loss_warm = float(ch.loss.item())
+
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    zl.zl_profile_begin(ch.handle, 1024 * max(1, args.steps))
+    torch.cuda.synchronize()
+    ev[0].record(stream)
+    for i in range(args.steps):
+        ch.update(h_in, labels, h_out=h_out)
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    prof = zl.zl_profile_end(ch.handle, 512)
+    step_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
+    total_ms = ev[0].elapsed_time(ev[-1])
+    loss = float(ch.loss.item())
+    med = float(np.median(step_ms))
+
+    flops, parts = algorithmic_flops(shp, T, S, args.alpha)
+    tokens_s = T / (med / 1e3)
+    mfma_pct = 100.0 * flops / (med / 1e3) / (PEAK_BF16_TFLOPS * 1e12)
+
+    # dominant kernel by summed time over the timed steps
+    prof.sort(key=lambda e: -e["total_ms"])
+    dom = prof[0]
+    per_launch_ms = dom["total_ms"] / dom["launches"]
+    if dom["flops"] > 0:
+        achieved = dom["flops"] / (dom["total_ms"] / 1e3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None}
+    else:
+        achieved = dom["bytes"] / (dom["total_ms"] / 1e3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None}
+    roof["kernel"] = dom["name"]
+    roof["launches_per_step"] = dom["launches"] / args.steps
+    roof["avg_launch_ms"] = round(per_launch_ms, 4)
+    roof["share_of_step"] = round(dom["total_ms"] / total_ms, 4)
+
+    kernels = []
+    for e in prof:
+        k = {"name": e["name"], "ms_per_step": round(e["total_ms"] / args.steps, 3),
+             "launches_per_step": e["launches"] / args.steps}
+        if e["flops"] > 0:
+            k["tflops"] = round(e["flops"] / (e["total_ms"] / 1e3) / 1e12, 1)
+        if e["bytes"] > 0:
+            k["gbs"] = round(e["bytes"] / (e["total_ms"] / 1e3) / 1e9, 1)
+        kernels.append(k)
+    if args.profile_json:
+        with open(args.profile_json, "w") as f:
+            json.dump(dict(kernels=kernels, step_ms=step_ms), f, indent=1)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(shp, args.alpha)
+
+    out = {
+        "metric": METRIC, "value": round(tokens_s, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(med, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (Zipf(1.1) token ids, random-init N(0,0.02) weights)",
+        "config": {"workload": f"{shp.name}: llama-3-8B-shaped chunk of {shp.n_layers} layers, "
+                               f"d={shp.d_model}, heads {shp.n_heads}/{shp.n_kv_heads}x"
+                               f"{shp.head_dim}, ff={shp.d_ff}, vocab={shp.vocab}"
+                               if shp.name == "8b" else shp.name,
+                   "global_batch": B, "seq_len": S, "tokens_per_step": T,
+                   "alpha": args.alpha, "optimizer": "adamw", "parallelism": "none (1 GPU)"},
+        "mfma_util_pct": round(mfma_pct, 2),
+        "algorithmic_tflop_per_step": round(flops / 1e12, 2),
+        "flop_split": {k: round(v / flops, 4) for k, v in parts.items()},
+        "ms_per_step_min": round(min(step_ms), 3),
+        "loss_first_warmup_to_last": [round(loss_warm, 4), round(loss, 4)],
+        "roofline": roof,
+        "kernels": kernels[:16],
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out))
+    ch.close()
+
+
+if __name__ == "__main__":
+    main()

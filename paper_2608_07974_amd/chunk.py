@@ -1,0 +1,149 @@
+"""A chunk whose buffers live in torch device tensors.
+
+torch provides device memory and the current HIP stream; every step of the
+update runs in libzl's kernels through the C ABI (zl.py).  Parameter keys
+are "L{layer}.{name}" with the names of zl_param_layout.
+"""
+import numpy as np
+import torch
+
+from . import zl
+
+_TORCH_DT = {zl.ZL_F32: torch.float32, zl.ZL_BF16: torch.bfloat16}
+
+
+def _ptr(t):
+    return 0 if t is None else t.data_ptr()
+
+
+def current_stream():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def config_from_shape(shp, alpha=0.5, consis="reverse", optimizer="adamw", lr=1e-4, wd=0.01,
+                      max_batch=None, max_seq=None):
+    """zl_config for a workload shape (arch, widths, dtype) and objective."""
+    return zl.make_config(
+        zl.ZL_ARCH_LLAMA if shp.arch == "llama" else zl.ZL_ARCH_GPT2, shp.n_layers, shp.d_model,
+        shp.n_heads, shp.n_kv_heads, shp.head_dim, shp.d_ff, shp.vocab, norm_eps=shp.norm_eps,
+        rope_theta=max(shp.rope_theta, 2.0),
+        dtype=zl.ZL_BF16 if shp.dtype == "bf16" else zl.ZL_F32, alpha=alpha,
+        consis=zl.ZL_KL_REVERSE if consis == "reverse" else zl.ZL_KL_FORWARD,
+        optimizer=zl.ZL_ADAMW if optimizer == "adamw" else zl.ZL_SGD, lr=lr, beta1=0.9,
+        beta2=0.999, eps=1e-8, weight_decay=wd, max_batch=max_batch or shp.batch,
+        max_seq=max_seq or shp.seq)
+
+
+class TorchChunk:
+    def __init__(self, cfg, device="cuda"):
+        zl.load()
+        self.cfg = cfg
+        self.device = torch.device(device)
+        self.dtype = _TORCH_DT[cfg.dtype]
+        self.n_params, self.layout = zl.zl_param_layout(cfg)
+        dev = self.device
+        n = self.n_params
+        self.master = torch.zeros(n, dtype=torch.float32, device=dev)
+        self.shadow = torch.zeros(n, dtype=torch.bfloat16, device=dev) if cfg.dtype == zl.ZL_BF16 else None
+        self.grad = torch.zeros(n, dtype=torch.float32, device=dev)
+        adam = cfg.optimizer == zl.ZL_ADAMW
+        self.adam_m = torch.zeros(n, dtype=torch.float32, device=dev) if adam else None
+        self.adam_v = torch.zeros(n, dtype=torch.float32, device=dev) if adam else None
+        d, V = cfg.d_model, cfg.vocab
+        self.head_w = torch.zeros(V, d, dtype=self.dtype, device=dev)
+        self.head_norm_w = torch.ones(d, dtype=torch.float32, device=dev)
+        self.head_norm_b = torch.zeros(d, dtype=torch.float32, device=dev) if cfg.arch == zl.ZL_ARCH_GPT2 else None
+        self.ws_bytes = zl.zl_workspace_size(cfg)
+        self._ws = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=dev)
+        self.ws_ptr = (self._ws.data_ptr() + 255) // 256 * 256
+        self.loss = torch.zeros(1, dtype=torch.float32, device=dev)
+        bufs = zl.zl_buffers(_ptr(self.master), _ptr(self.shadow), _ptr(self.grad),
+                             _ptr(self.adam_m), _ptr(self.adam_v), _ptr(self.head_w),
+                             _ptr(self.head_norm_w), _ptr(self.head_norm_b))
+        self.handle = zl.zl_chunk_create(cfg, bufs, self.ws_ptr, self.ws_bytes)
+        self.by_key = {f"L{t['layer']}.{t['name']}": t for t in self.layout}
+
+    def close(self):
+        if self.handle:
+            zl.zl_chunk_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # ------------------------------------------------------------ params
+    def view(self, buf, key):
+        t = self.by_key[key]
+        return buf[t["offset"]: t["offset"] + t["numel"]].view(*t["shape"])
+
+    def load_params(self, params):
+        for key, val in params.items():
+            self.view(self.master, key).copy_(torch.as_tensor(np.asarray(val, np.float32)))
+        zl.zl_refresh_shadow(self.handle, current_stream())
+
+    def load_head(self, head_w, head_norm_w, head_norm_b=None):
+        self.head_w.copy_(torch.as_tensor(np.asarray(head_w, np.float32)).to(self.dtype))
+        self.head_norm_w.copy_(torch.as_tensor(np.asarray(head_norm_w, np.float32)))
+        if self.head_norm_b is not None and head_norm_b is not None:
+            self.head_norm_b.copy_(torch.as_tensor(np.asarray(head_norm_b, np.float32)))
+
+    def tensors(self, buf):
+        torch.cuda.synchronize(self.device)
+        return {k: self.view(buf, k).detach().cpu().double().numpy() for k in self.by_key}
+
+    # ------------------------------------------------------------ update
+    def _check_inputs(self, h_in, seq_lens=None, pos_ids=None, labels=None, h_out=None):
+        if h_in.dtype != self.dtype or not h_in.is_contiguous() or h_in.dim() != 3:
+            raise TypeError(f"h_in must be a contiguous [B, S, d] {self.dtype} tensor")
+        for name, t in (("seq_lens", seq_lens), ("pos_ids", pos_ids), ("labels", labels)):
+            if t is not None and (t.dtype != torch.int32 or not t.is_contiguous()):
+                raise TypeError(f"{name} must be a contiguous int32 tensor")
+        if h_out is not None and (h_out.dtype != self.dtype or h_out.shape != h_in.shape):
+            raise TypeError("h_out must match h_in in shape and dtype")
+
+    def forward(self, h_in, seq_lens=None, pos_ids=None, h_out=None):
+        self._check_inputs(h_in, seq_lens, pos_ids, None, h_out)
+        B, S, _ = h_in.shape
+        if h_out is None:
+            h_out = torch.empty_like(h_in)
+        zl.zl_chunk_forward(self.handle, _ptr(h_in), _ptr(seq_lens), _ptr(pos_ids), B, S,
+                            _ptr(h_out), current_stream())
+        return h_out
+
+    def objective(self, labels):
+        if labels.dtype != torch.int32 or not labels.is_contiguous():
+            raise TypeError("labels must be a contiguous int32 tensor")
+        zl.zl_local_objective(self.handle, _ptr(labels), _ptr(self.loss), current_stream())
+        return self.loss
+
+    def backward(self, grad_scale=1.0, accumulate=0):
+        zl.zl_chunk_backward(self.handle, grad_scale, accumulate, current_stream())
+
+    def step(self):
+        zl.zl_optimizer_step(self.handle, current_stream())
+
+    def update(self, h_in, labels, seq_lens=None, pos_ids=None, h_out=None):
+        self._check_inputs(h_in, seq_lens, pos_ids, labels, h_out)
+        B, S, _ = h_in.shape
+        if h_out is None:
+            h_out = torch.empty_like(h_in)
+        zl.zl_chunk_update(self.handle, _ptr(h_in), _ptr(seq_lens), _ptr(pos_ids), _ptr(labels),
+                           B, S, _ptr(h_out), _ptr(self.loss), current_stream())
+        return h_out
+
+    def inspect(self, name, layer=0):
+        """Copy of a workspace view as a float64 numpy array."""
+        v = zl.zl_inspect(self.handle, name, layer)
+        torch.cuda.synchronize(self.device)
+        dt = torch.bfloat16 if v["dtype"] == zl.ZL_BF16 else torch.float32
+        esz = 2 if dt == torch.bfloat16 else 4
+        n = v["rows"] * v["ld"]
+        raw = torch.empty(n, dtype=dt, device=self.device)
+        # view the workspace bytes at v["ptr"] through the owning tensor
+        off = v["ptr"] - self._ws.data_ptr()
+        src = self._ws[off: off + n * esz].view(dt)
+        raw.copy_(src)
+        return raw.view(v["rows"], v["ld"])[:, : v["cols"]].double().cpu().numpy()

@@ -1,0 +1,169 @@
+// Local objective of Eq. (3)-(5) on the frozen readout of Eq. (2).
+//
+// The head GEMM writes fp32 logits of a row block: rows of z (readout of
+// h_out) interleaved with rows of z' (readout of h_in, the stop-gradient
+// consistency target) when alpha < 1.  One workgroup per token row then
+//   pass 1: online max / sum-exp of z and z', plus the KL statistic
+//           E = sum_v p_v (z_v - z'_v)   (reverse)   or
+//           F = sum_v q_v (z'_v - z_v)   (forward),
+//   pass 2: dL/dz_v = (1/|Omega|) [alpha (p_v - [v = y]) + (1 - alpha) g_v]
+//           with g = p (z - z' - E) (reverse, the softmax Jacobian applied to
+//           log p - log q) or g = p - q (forward),
+// and writes the row's loss alpha CE + (1 - alpha) KL (0 outside Omega),
+// CE = lse - z_y, KL_rev = E - lse + lse', KL_fwd = F - lse' + lse.
+#include "common.h"
+
+namespace zl {
+
+constexpr int OT = 256;
+
+__device__ inline bool label_ok(int y, int V) { return y >= 0 && y < V; }
+
+__global__ void count_omega_kernel(const int32_t* __restrict__ labels, int T, int V,
+                                   float* __restrict__ out) {
+  __shared__ int red[OT / 64];
+  int c = 0;
+  for (int i = threadIdx.x; i < T; i += OT) c += label_ok(labels[i], V) ? 1 : 0;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o, 64);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int t = 0;
+    for (int i = 0; i < OT / 64; ++i) t += red[i];
+    out[0] = (float)t;
+  }
+}
+
+hipError_t launch_count_omega(const int32_t* labels, int T, int V, float* n_omega,
+                              hipStream_t s) {
+  hipLaunchKernelGGL(count_omega_kernel, dim3(1), dim3(OT), 0, s, labels, T, V, n_omega);
+  return hipGetLastError();
+}
+
+struct Soft {  // running (max, sum exp(x - max), sum exp(x - max) * w)
+  float m, s, e;
+};
+
+__device__ inline Soft soft_merge(Soft a, Soft b) {
+  const float m = fmaxf(a.m, b.m);
+  if (m == -INFINITY) return a;
+  const float fa = __expf(a.m - m), fb = __expf(b.m - m);
+  return {m, a.s * fa + b.s * fb, a.e * fa + b.e * fb};
+}
+
+__device__ inline Soft soft_add(Soft a, float x, float w) {
+  if (x > a.m) {
+    const float f = __expf(a.m - x);
+    return {x, a.s * f + 1.f, a.e * f + w};
+  }
+  const float p = __expf(x - a.m);
+  return {a.m, a.s + p, a.e + p * w};
+}
+
+__device__ inline Soft block_soft(Soft v, Soft* red) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    Soft t = {__shfl_xor(v.m, o, 64), __shfl_xor(v.s, o, 64), __shfl_xor(v.e, o, 64)};
+    v = soft_merge(v, t);
+  }
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  Soft r = red[0];
+  for (int i = 1; i < OT / 64; ++i) r = soft_merge(r, red[i]);
+  return r;
+}
+
+__global__ void __launch_bounds__(OT) objective_rows_kernel(ObjDesc o) {
+  __shared__ Soft red[OT / 64];
+  const int i = blockIdx.x;
+  const float* z = o.zc + (int64_t)i * o.stacked * o.ldz;
+  const float* zp = o.stacked == 2 ? z + o.ldz : nullptr;
+  const int y = o.labels[i];
+  const bool in_omega = label_ok(y, o.V);
+  const float nomega = o.n_omega[0];
+  const float inv = nomega > 0.f ? 1.f / nomega : 0.f;
+  const bool rev = o.consis == 0;
+  const int64_t orow = (int64_t)i * o.lddz;
+
+  if (!in_omega) {
+    for (int v = threadIdx.x; v < o.Vpad; v += OT) {
+      if (o.dz_dtype == BF16) ((bf16_t*)o.dz)[orow + v] = 0;
+      else ((float*)o.dz)[orow + v] = 0.f;
+    }
+    if (threadIdx.x == 0) o.row_loss[i] = 0.f;
+    return;
+  }
+
+  Soft sp = {-INFINITY, 0.f, 0.f}, sq = {-INFINITY, 0.f, 0.f};
+  for (int v = threadIdx.x; v < o.V; v += OT) {
+    const float a = z[v];
+    const float b = zp ? zp[v] : 0.f;
+    sp = soft_add(sp, a, a - b);   // e accumulates sum p (z - z') unnormalised
+    if (zp) sq = soft_add(sq, b, b - a);
+  }
+  sp = block_soft(sp, red);
+  const float lse = sp.m + __logf(sp.s);
+  float lse2 = 0.f, E = 0.f, F = 0.f;
+  E = sp.e / sp.s;
+  if (zp) {
+    sq = block_soft(sq, red);
+    lse2 = sq.m + __logf(sq.s);
+    F = sq.e / sq.s;
+  }
+  const float zy = z[y];
+  const float ce = lse - zy;
+  float kl = 0.f;
+  if (zp) kl = rev ? (E - lse + lse2) : (F - lse2 + lse);
+  const float a = o.alpha;
+  if (threadIdx.x == 0) o.row_loss[i] = a * ce + (zp ? (1.f - a) * kl : 0.f);
+
+  for (int v = threadIdx.x; v < o.Vpad; v += OT) {
+    float g = 0.f;
+    if (v < o.V) {
+      const float zv = z[v];
+      const float p = __expf(zv - lse);
+      g = a * (p - (v == y ? 1.f : 0.f));
+      if (zp) {
+        const float zpv = zp[v];
+        if (rev) g += (1.f - a) * p * (zv - zpv - E);
+        else g += (1.f - a) * (p - __expf(zpv - lse2));
+      }
+      g *= inv;
+    }
+    if (o.dz_dtype == BF16) ((bf16_t*)o.dz)[orow + v] = f32_to_bf16(g);
+    else ((float*)o.dz)[orow + v] = g;
+  }
+}
+
+hipError_t launch_objective_rows(const ObjDesc& o, hipStream_t s) {
+  if (o.rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(objective_rows_kernel, dim3(o.rows), dim3(OT), 0, s, o);
+  return hipGetLastError();
+}
+
+__global__ void loss_reduce_kernel(const float* __restrict__ row_loss, int T,
+                                   const float* __restrict__ n_omega, float* __restrict__ loss) {
+  __shared__ float red[OT / 64];
+  float s = 0.f;
+  for (int i = threadIdx.x; i < T; i += OT) s += row_loss[i];
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float t = 0.f;
+    for (int i = 0; i < OT / 64; ++i) t += red[i];
+    const float n = n_omega[0];
+    loss[0] = n > 0.f ? t / n : 0.f;
+  }
+}
+
+hipError_t launch_loss_reduce(const float* row_loss, int T, const float* n_omega, float* loss,
+                              hipStream_t s) {
+  hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(OT), 0, s, row_loss, T, n_omega, loss);
+  return hipGetLastError();
+}
+
+}  // namespace zl

@@ -1,0 +1,418 @@
+// Row-wise and elementwise kernels of the chunk map (Eq. (1)) and of the
+// frozen head's norm (Eq. (2)): RMSNorm / LayerNorm forward and backward,
+// rotary embedding, SwiGLU, casts, deterministic two-stage reductions.
+// All HBM-bound: one pass over each operand, coalesced along the row.
+#include "common.h"
+
+namespace zl {
+
+constexpr int RT = 256;            // threads per row block
+
+__device__ inline float ldf(const void* p, int dt, size_t i) {
+  return dt == BF16 ? bf16_to_f32(((const bf16_t*)p)[i]) : ((const float*)p)[i];
+}
+__device__ inline void stf(void* p, int dt, size_t i, float v) {
+  if (dt == BF16) ((bf16_t*)p)[i] = f32_to_bf16(v);
+  else ((float*)p)[i] = v;
+}
+
+// ----------------------------------------------------------- norm forward
+// One wave per output row; float4 loads; the row is read three times (sum,
+// centred sum of squares, output) and stays in L1/L2 between the passes.
+// Output row r reads source row: xb ? (r even: xa[row0 + r/2], odd:
+// xb[row0 + r/2]) : xa[row0 + r].
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+__global__ void __launch_bounds__(RT)
+norm_fwd_kernel(int layernorm, const float* __restrict__ xa, const float* __restrict__ xb,
+                int64_t ldx, int row0, const float* __restrict__ w, const float* __restrict__ b,
+                void* __restrict__ y, int64_t ldy, int ydt, float* __restrict__ mean,
+                float* __restrict__ rstd, int rows, int d, float eps) {
+  const int r = blockIdx.x * (RT / 64) + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= rows) return;
+  const float* x;
+  if (xb) x = ((r & 1) ? xb : xa) + (int64_t)(row0 + (r >> 1)) * ldx;
+  else x = xa + (int64_t)(row0 + r) * ldx;
+  float mu = 0.f;
+  if (layernorm) {
+    float s = 0.f;
+    for (int c = lane * 4; c < d; c += 256) {
+      const float4 v = *reinterpret_cast<const float4*>(x + c);
+      s += (v.x + v.y) + (v.z + v.w);
+    }
+    mu = wave_sum(s) / d;
+  }
+  float q = 0.f;
+  for (int c = lane * 4; c < d; c += 256) {
+    const float4 v = *reinterpret_cast<const float4*>(x + c);
+    const float a0 = v.x - mu, a1 = v.y - mu, a2 = v.z - mu, a3 = v.w - mu;
+    q += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
+  }
+  const float rs = rsqrtf(wave_sum(q) / d + eps);
+  if (lane == 0) {
+    rstd[r] = rs;
+    if (layernorm && mean) mean[r] = mu;
+  }
+  for (int c = lane * 4; c < d; c += 256) {
+    const float4 v = *reinterpret_cast<const float4*>(x + c);
+    const float4 g = *reinterpret_cast<const float4*>(w + c);
+    float o0 = (v.x - mu) * rs * g.x, o1 = (v.y - mu) * rs * g.y;
+    float o2 = (v.z - mu) * rs * g.z, o3 = (v.w - mu) * rs * g.w;
+    if (layernorm) {
+      const float4 bb = *reinterpret_cast<const float4*>(b + c);
+      o0 += bb.x; o1 += bb.y; o2 += bb.z; o3 += bb.w;
+    }
+    const int64_t o = (int64_t)r * ldy + c;
+    if (ydt == BF16) {
+      *reinterpret_cast<ushort4*>((bf16_t*)y + o) =
+          make_ushort4(f32_to_bf16(o0), f32_to_bf16(o1), f32_to_bf16(o2), f32_to_bf16(o3));
+    } else {
+      *reinterpret_cast<float4*>((float*)y + o) = make_float4(o0, o1, o2, o3);
+    }
+  }
+}
+
+hipError_t launch_norm_fwd(bool layernorm, const float* x, int64_t ldx, const float* w,
+                           const float* b, void* y, int64_t ldy, int ydtype, float* mean,
+                           float* rstd, int T, int d, float eps, hipStream_t s) {
+  if (T <= 0) return hipSuccess;
+  hipLaunchKernelGGL(norm_fwd_kernel, dim3((T + 3) / 4), dim3(RT), 0, s, (int)layernorm, x,
+                     (const float*)nullptr, ldx, 0, w, b, y, ldy, ydtype, mean, rstd, T, d, eps);
+  return hipGetLastError();
+}
+
+hipError_t launch_head_norm(bool layernorm, const float* xa, const float* xb, int64_t ldx,
+                            int row0, int rows, const float* w, const float* b, void* y,
+                            int ydtype, float* mean, float* rstd, int d, float eps,
+                            hipStream_t s) {
+  const int out_rows = xb ? 2 * rows : rows;
+  if (out_rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(norm_fwd_kernel, dim3((out_rows + 3) / 4), dim3(RT), 0, s, (int)layernorm,
+                     xa, xb, ldx, row0, w, b, y, (int64_t)d, ydtype, mean, rstd, out_rows, d, eps);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------- norm backward
+// One wave per row, each wave owning a contiguous run of rows.  Per row:
+// g = dy * w, xhat = (x - mean) * rstd,
+//   rms: dx = rstd * (g - xhat * mean(g * xhat))
+//   ln:  dx = rstd * (g - mean(g) - xhat * mean(g * xhat))
+// The weight-gradient partials sum(dy * xhat) (and sum(dy)) over the wave's
+// rows accumulate in a wave-private LDS slice and are written as one row of
+// part_w / part_b per wave: deterministic, no atomics.
+constexpr int NB_WAVES = 1024;  // waves (partial rows) of a norm backward launch
+
+int norm_bwd_blocks(int T) {
+  const int waves = T < NB_WAVES ? (T > 0 ? T : 1) : NB_WAVES;
+  return waves;  // number of partial rows
+}
+
+__global__ void __launch_bounds__(RT)
+norm_bwd_kernel(int layernorm, const float* __restrict__ dy, int64_t lddy,
+                const float* __restrict__ x, const float* __restrict__ w,
+                const float* __restrict__ mean, const float* __restrict__ rstd, int rstride,
+                const float* dres, float* dx, void* dx_act, int adt,
+                float* __restrict__ part_w, float* __restrict__ part_b, int T, int d, int rpw,
+                int nwaves, int row_out0) {
+  extern __shared__ float accs[];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int gw = blockIdx.x * (RT / 64) + wave;
+  const bool want_part = part_w != nullptr;
+  float* aw = accs + (size_t)wave * (layernorm ? 2 : 1) * d;
+  float* ab = aw + d;
+  if (want_part)
+    for (int c = lane * 4; c < d; c += 256) {
+      *reinterpret_cast<float4*>(aw + c) = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (layernorm) *reinterpret_cast<float4*>(ab + c) = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  const int r0 = gw * rpw, r1 = min(T, r0 + rpw);
+  for (int r = (gw < nwaves ? r0 : T); r < r1; ++r) {
+    const float rs = rstd[(int64_t)r * rstride];
+    const float mu = layernorm ? mean[(int64_t)r * rstride] : 0.f;
+    const int ro = row_out0 + r;
+    const float* dyr = dy + (int64_t)r * lddy;
+    const float* xr = x + (int64_t)ro * d;
+    float sg = 0.f, sgx = 0.f;
+    for (int c = lane * 4; c < d; c += 256) {
+      const float4 a = *reinterpret_cast<const float4*>(dyr + c);
+      const float4 v = *reinterpret_cast<const float4*>(xr + c);
+      const float4 g = *reinterpret_cast<const float4*>(w + c);
+      const float h0 = (v.x - mu) * rs, h1 = (v.y - mu) * rs, h2 = (v.z - mu) * rs, h3 = (v.w - mu) * rs;
+      const float g0 = a.x * g.x, g1 = a.y * g.y, g2 = a.z * g.z, g3 = a.w * g.w;
+      sg += (g0 + g1) + (g2 + g3);
+      sgx += (g0 * h0 + g1 * h1) + (g2 * h2 + g3 * h3);
+      if (want_part) {
+        float4 t = *reinterpret_cast<float4*>(aw + c);
+        t.x += a.x * h0; t.y += a.y * h1; t.z += a.z * h2; t.w += a.w * h3;
+        *reinterpret_cast<float4*>(aw + c) = t;
+        if (layernorm) {
+          float4 u = *reinterpret_cast<float4*>(ab + c);
+          u.x += a.x; u.y += a.y; u.z += a.z; u.w += a.w;
+          *reinterpret_cast<float4*>(ab + c) = u;
+        }
+      }
+    }
+    if (!dx) continue;
+    const float mg = layernorm ? wave_sum(sg) / d : 0.f;
+    const float mgx = wave_sum(sgx) / d;
+    for (int c = lane * 4; c < d; c += 256) {
+      const float4 a = *reinterpret_cast<const float4*>(dyr + c);
+      const float4 v = *reinterpret_cast<const float4*>(xr + c);
+      const float4 g = *reinterpret_cast<const float4*>(w + c);
+      float o[4];
+      const float av[4] = {a.x, a.y, a.z, a.w}, vv[4] = {v.x, v.y, v.z, v.w}, gv[4] = {g.x, g.y, g.z, g.w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const float h = (vv[k] - mu) * rs;
+        o[k] = rs * (av[k] * gv[k] - mg - h * mgx);
+      }
+      const int64_t off = (int64_t)ro * d + c;
+      if (dres) {
+        const float4 q = *reinterpret_cast<const float4*>(dres + off);
+        o[0] += q.x; o[1] += q.y; o[2] += q.z; o[3] += q.w;
+      }
+      *reinterpret_cast<float4*>(dx + off) = make_float4(o[0], o[1], o[2], o[3]);
+      if (dx_act) {
+        if (adt == BF16)
+          *reinterpret_cast<ushort4*>((bf16_t*)dx_act + off) =
+              make_ushort4(f32_to_bf16(o[0]), f32_to_bf16(o[1]), f32_to_bf16(o[2]), f32_to_bf16(o[3]));
+        else
+          *reinterpret_cast<float4*>((float*)dx_act + off) = make_float4(o[0], o[1], o[2], o[3]);
+      }
+    }
+  }
+  if (want_part && gw < nwaves)
+    for (int c = lane * 4; c < d; c += 256) {
+      *reinterpret_cast<float4*>(part_w + (int64_t)gw * d + c) = *reinterpret_cast<float4*>(aw + c);
+      if (layernorm && part_b)
+        *reinterpret_cast<float4*>(part_b + (int64_t)gw * d + c) = *reinterpret_cast<float4*>(ab + c);
+    }
+}
+
+static hipError_t norm_bwd_launch(bool layernorm, const float* dy, int64_t lddy, const float* x,
+                                  const float* w, const float* mean, const float* rstd,
+                                  int rstride, const float* dres, float* dx, void* dx_act,
+                                  int adt, float* part_w, float* part_b, int T, int d,
+                                  int row_out0, int* nblk_out, hipStream_t s) {
+  const int nw = norm_bwd_blocks(T);
+  const int rpw = (T + nw - 1) / nw;
+  if (nblk_out) *nblk_out = nw;
+  const size_t lds = part_w ? (size_t)(RT / 64) * (layernorm ? 2 : 1) * d * sizeof(float) : 0;
+  static bool attr = false;
+  if (!attr) {
+    hipError_t e = hipFuncSetAttribute((const void*)norm_bwd_kernel,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  hipLaunchKernelGGL(norm_bwd_kernel, dim3((nw + 3) / 4), dim3(RT), lds, s, (int)layernorm, dy,
+                     lddy, x, w, mean, rstd, rstride, dres, dx, dx_act, adt, part_w, part_b, T, d,
+                     rpw, nw, row_out0);
+  return hipGetLastError();
+}
+
+hipError_t launch_norm_bwd(bool layernorm, const float* dy, const float* x, const float* w,
+                           const float* mean, const float* rstd, const float* dres,
+                           float* dx, void* dx_act, int act_dtype, float* part_w,
+                           float* part_b, int T, int d, hipStream_t s, int* nblk_out) {
+  return norm_bwd_launch(layernorm, dy, (int64_t)d, x, w, mean, rstd, 1, dres, dx, dx_act,
+                         act_dtype, part_w, part_b, T, d, 0, nblk_out, s);
+}
+
+hipError_t launch_head_norm_bwd(bool layernorm, const float* dy, int64_t lddy, const float* x,
+                                const float* w, const float* mean, const float* rstd,
+                                int rstd_stride, float* dx, void* dx_act, int act_dtype,
+                                int row0, int rows, int d, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  return norm_bwd_launch(layernorm, dy, lddy, x, w, mean, rstd, rstd_stride, nullptr, dx, dx_act,
+                         act_dtype, nullptr, nullptr, rows, d, row0, nullptr, s);
+}
+
+// ------------------------------------------------------------- reductions
+// out[j] = (accumulate ? out[j] : 0) + scale * sum_b part[b, j]; a block
+// covers 64 columns with 4 row groups, each summing with 4 independent
+// accumulators; the 4 group sums combine in a fixed order (deterministic).
+__global__ void __launch_bounds__(256) reduce_rows_kernel(const float* __restrict__ part, int nblk,
+                                                          int d, float* __restrict__ out,
+                                                          float scale, int accumulate) {
+  __shared__ float red[4][64];
+  const int j = blockIdx.x * 64 + (threadIdx.x & 63);
+  const int grp = threadIdx.x >> 6;
+  float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+  if (j < d) {
+    int b = grp;
+    for (; b + 12 < nblk; b += 16) {
+      a0 += part[(int64_t)b * d + j];
+      a1 += part[(int64_t)(b + 4) * d + j];
+      a2 += part[(int64_t)(b + 8) * d + j];
+      a3 += part[(int64_t)(b + 12) * d + j];
+    }
+    for (; b < nblk; b += 4) a0 += part[(int64_t)b * d + j];
+  }
+  red[grp][threadIdx.x & 63] = (a0 + a1) + (a2 + a3);
+  __syncthreads();
+  if (grp == 0 && j < d) {
+    const float t = ((red[0][threadIdx.x] + red[1][threadIdx.x]) + red[2][threadIdx.x]) + red[3][threadIdx.x];
+    const float v = scale * t;
+    out[j] = accumulate ? out[j] + v : v;
+  }
+}
+
+hipError_t launch_reduce_rows(const float* part, int nblk, int d, float* out, float scale,
+                              int accumulate, hipStream_t s) {
+  if (d <= 0) return hipSuccess;
+  hipLaunchKernelGGL(reduce_rows_kernel, dim3((d + 63) / 64), dim3(256), 0, s, part, nblk, d, out,
+                     scale, accumulate);
+  return hipGetLastError();
+}
+
+int colsum_blocks(int T) { return T < 256 ? (T > 0 ? T : 1) : 256; }
+
+__global__ void colsum_kernel(const void* __restrict__ x, int64_t ldx, int dt, int T, int n,
+                              int rpb, float* __restrict__ part) {
+  const int r0 = blockIdx.y * rpb, r1 = min(T, r0 + rpb);
+  for (int c = blockIdx.x * blockDim.x + threadIdx.x; c < n; c += gridDim.x * blockDim.x) {
+    float s0 = 0.f, s1 = 0.f;
+    int r = r0;
+    for (; r + 1 < r1; r += 2) {
+      s0 += ldf(x, dt, (int64_t)r * ldx + c);
+      s1 += ldf(x, dt, (int64_t)(r + 1) * ldx + c);
+    }
+    if (r < r1) s0 += ldf(x, dt, (int64_t)r * ldx + c);
+    part[(int64_t)blockIdx.y * n + c] = s0 + s1;
+  }
+}
+
+hipError_t launch_colsum_partial(const void* x, int64_t ldx, int dtype, int T, int n,
+                                 float* part, int* nblk_out, hipStream_t s) {
+  const int nblk = colsum_blocks(T);
+  const int rpb = (T + nblk - 1) / nblk;
+  *nblk_out = nblk;
+  dim3 grid((n + 255) / 256, nblk);
+  hipLaunchKernelGGL(colsum_kernel, grid, dim3(256), 0, s, x, ldx, dtype, T, n, rpb, part);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------ elementwise
+__global__ void cast_kernel(const void* __restrict__ src, int sdt, void* __restrict__ dst,
+                            int ddt, size_t n) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n;
+       i += (size_t)gridDim.x * blockDim.x)
+    stf(dst, ddt, i, ldf(src, sdt, i));
+}
+
+hipError_t launch_cast(const void* src, int sdtype, void* dst, int ddtype, size_t n,
+                       hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  size_t blocks = (n + 255) / 256;
+  if (blocks > 16384) blocks = 16384;
+  hipLaunchKernelGGL(cast_kernel, dim3((unsigned)blocks), dim3(256), 0, s, src, sdtype, dst,
+                     ddtype, n);
+  return hipGetLastError();
+}
+
+// mode 0: seq_lens (default S, clamped to [0, S]); mode 1: pos ids (default i % S)
+__global__ void copy_i32_kernel(const int32_t* __restrict__ src, int32_t* __restrict__ dst, int n,
+                                int mode, int S) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  if (mode == 0) {
+    int v = src ? src[i] : S;
+    dst[i] = v < 0 ? 0 : (v > S ? S : v);
+  } else {
+    dst[i] = src ? src[i] : (i % S);
+  }
+}
+
+hipError_t launch_copy_i32(const int32_t* src, int32_t* dst, int n, int fill_default, int mode,
+                           int S, hipStream_t s) {
+  (void)fill_default;
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(copy_i32_kernel, dim3((n + 255) / 256), dim3(256), 0, s, src, dst, n, mode,
+                     S);
+  return hipGetLastError();
+}
+
+// RoPE table: (cos, sin) of pos * theta^(-2j/hd), computed in double.
+__global__ void rope_table_kernel(float2* table, int max_pos, int half, double theta) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= max_pos * half) return;
+  const int p = i / half, j = i % half;
+  const double inv = pow(theta, -(2.0 * j) / (2.0 * half));
+  const double a = (double)p * inv;
+  table[i] = make_float2((float)cos(a), (float)sin(a));
+}
+
+hipError_t launch_rope_table(float2* table, int max_pos, int half, double theta,
+                             hipStream_t s) {
+  const int n = max_pos * half;
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(rope_table_kernel, dim3((n + 255) / 256), dim3(256), 0, s, table, max_pos,
+                     half, theta);
+  return hipGetLastError();
+}
+
+// u'_j = u_j c - u_{j+h} s*sign ; u'_{j+h} = u_{j+h} c + u_j s*sign
+__global__ void rope_kernel(void* __restrict__ qkv, int64_t ld, int dt,
+                            const int32_t* __restrict__ pos, const float2* __restrict__ table,
+                            int max_pos, int T, int nheads, int hd, float sign) {
+  const int half = hd / 2;
+  const int64_t n = (int64_t)T * nheads * half;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int j = (int)(i % half);
+    const int64_t th = i / half;
+    const int h = (int)(th % nheads);
+    const int t = (int)(th / nheads);
+    int p = pos[t];
+    p = p < 0 ? 0 : (p >= max_pos ? max_pos - 1 : p);
+    const float2 cs = table[(int64_t)p * half + j];
+    const float sn = cs.y * sign;
+    const int64_t o = (int64_t)t * ld + (int64_t)h * hd + j;
+    const float a = ldf(qkv, dt, o), b = ldf(qkv, dt, o + half);
+    stf(qkv, dt, o, a * cs.x - b * sn);
+    stf(qkv, dt, o + half, b * cs.x + a * sn);
+  }
+}
+
+hipError_t launch_rope(void* qkv, int64_t ld, int dtype, const int32_t* pos, const float2* table,
+                       int max_pos, int T, int nheads_qk, int hd, int sign, hipStream_t s) {
+  const int64_t n = (int64_t)T * nheads_qk * (hd / 2);
+  if (n <= 0) return hipSuccess;
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  hipLaunchKernelGGL(rope_kernel, dim3((unsigned)blocks), dim3(256), 0, s, qkv, ld, dtype, pos,
+                     table, max_pos, T, nheads_qk, hd, (float)sign);
+  return hipGetLastError();
+}
+
+__global__ void swiglu_fwd_kernel(const void* __restrict__ gu, int64_t ldgu,
+                                  void* __restrict__ a, int64_t lda, int dt, int T, int ff) {
+  const int64_t n = (int64_t)T * ff;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t t = i / ff;
+    const int j = (int)(i % ff);
+    const float g = ldf(gu, dt, t * ldgu + j);
+    const float u = ldf(gu, dt, t * ldgu + ff + j);
+    stf(a, dt, t * lda + j, g / (1.f + __expf(-g)) * u);
+  }
+}
+
+hipError_t launch_swiglu_fwd(const void* gu, int64_t ldgu, void* a, int64_t lda, int dtype,
+                             int T, int ff, hipStream_t s) {
+  const int64_t n = (int64_t)T * ff;
+  if (n <= 0) return hipSuccess;
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  hipLaunchKernelGGL(swiglu_fwd_kernel, dim3((unsigned)blocks), dim3(256), 0, s, gu, ldgu, a,
+                     lda, dtype, T, ff);
+  return hipGetLastError();
+}
+
+}  // namespace zl

@@ -1,0 +1,899 @@
+// Host side of the C ABI (include/zl.h): configuration checks, the flat
+// parameter layout, the workspace plan, the call-order state machine and the
+// launch sequences of the chunk-local update.
+//
+// Order of work inside one update (Sec. III-B, in-stage steps S1-S3):
+//   forward    cast h_in -> X0 (fp32 residual stream); per layer:
+//              norm1 -> QKV GEMM (+bias) -> RoPE -> attention -> O GEMM +
+//              residual -> norm2 -> up GEMM (+GELU) [-> SwiGLU] -> down GEMM
+//              + residual; cast X_L -> h_out (early-forward point)
+//   objective  |Omega|; per row block of the head: head norm of h_out (and
+//              h_in) -> logits GEMM -> row stats, loss rows, dL/dz ->
+//              dz W_lm GEMM -> head-norm backward into dL/dh_out
+//   backward   per layer, last to first: down dgrad (+SwiGLU/GELU bwd),
+//              down wgrad, up dgrad, up wgrad, norm2 bwd, O dgrad, O wgrad,
+//              attention bwd, RoPE bwd, QKV dgrad, QKV wgrad, norm1 bwd;
+//              layer 0 forms no gradient into h_in (Remark 1)
+//   step       AdamW / SGD over the flat buffers, bf16 shadow refresh
+#include <math.h>
+#include <string.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/zl.h"
+#include "../../include/zl_inspect.h"
+#include "common.h"
+
+using namespace zl;
+
+static thread_local std::string g_err;
+
+static zl_status fail(zl_status s, const std::string& msg) {
+  g_err = msg;
+  return s;
+}
+
+#define ZL_HIP(call)                                                              \
+  do {                                                                            \
+    hipError_t e_ = (call);                                                       \
+    if (e_ != hipSuccess)                                                         \
+      return fail(ZL_ERR_HIP, std::string(#call) + ": " + hipGetErrorString(e_)); \
+  } while (0)
+
+// ----------------------------------------------------------------- layout
+namespace {
+
+constexpr size_t ALIGN_ELEMS = 64;
+constexpr size_t ALIGN_BYTES = 256;
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+struct LayerOff {
+  size_t ln1_w, ln1_b, w_qkv, b_qkv, w_o, b_o, ln2_w, ln2_b, w_up, b_up, w_down, b_down;
+};
+
+struct Dims {
+  int arch, L, d, hq, hkv, hd, ff, V, dq, dkv, nqkv, nup;
+  bool llama;
+};
+
+Dims dims_of(const zl_config& c) {
+  Dims m;
+  m.arch = c.arch;
+  m.llama = c.arch == ZL_ARCH_LLAMA;
+  m.L = c.n_layers;
+  m.d = c.d_model;
+  m.hq = c.n_heads;
+  m.hkv = c.n_kv_heads;
+  m.hd = c.head_dim;
+  m.ff = c.d_ff;
+  m.V = c.vocab;
+  m.dq = m.hq * m.hd;
+  m.dkv = m.hkv * m.hd;
+  m.nqkv = m.dq + 2 * m.dkv;
+  m.nup = m.llama ? 2 * m.ff : m.ff;
+  return m;
+}
+
+zl_status check_config(const zl_config* c) {
+  if (!c) return fail(ZL_ERR_INVALID_ARG, "config is NULL");
+  if (c->arch != ZL_ARCH_LLAMA && c->arch != ZL_ARCH_GPT2)
+    return fail(ZL_ERR_INVALID_ARG, "arch must be ZL_ARCH_LLAMA or ZL_ARCH_GPT2");
+  if (c->n_layers < 1) return fail(ZL_ERR_INVALID_ARG, "n_layers must be >= 1");
+  if (c->d_model < 64 || c->d_model % 64)
+    return fail(ZL_ERR_INVALID_ARG, "d_model must be a positive multiple of 64");
+  if (c->d_model > 8192) return fail(ZL_ERR_UNSUPPORTED, "d_model above 8192");
+  if (c->arch == ZL_ARCH_GPT2 && c->d_model > 4096)
+    return fail(ZL_ERR_UNSUPPORTED, "LayerNorm form above d_model 4096");
+  if (c->n_heads < 1 || c->n_kv_heads < 1 || c->n_heads % c->n_kv_heads)
+    return fail(ZL_ERR_INVALID_ARG, "n_heads must be a positive multiple of n_kv_heads");
+  if (c->head_dim < 8 || c->head_dim % 8)
+    return fail(ZL_ERR_INVALID_ARG, "head_dim must be a positive multiple of 8");
+  if (c->head_dim != 16 && c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128)
+    return fail(ZL_ERR_UNSUPPORTED, "head_dim must be 16, 32, 64 or 128");
+  if (c->d_ff < 64 || c->d_ff % 64)
+    return fail(ZL_ERR_INVALID_ARG, "d_ff must be a positive multiple of 64");
+  if (c->vocab < 2) return fail(ZL_ERR_INVALID_ARG, "vocab must be >= 2");
+  if (!(c->norm_eps > 0.f)) return fail(ZL_ERR_INVALID_ARG, "norm_eps must be > 0");
+  if (c->arch == ZL_ARCH_LLAMA && !(c->rope_theta > 1.f))
+    return fail(ZL_ERR_INVALID_ARG, "rope_theta must be > 1 for llama");
+  if (c->dtype != ZL_F32 && c->dtype != ZL_BF16)
+    return fail(ZL_ERR_INVALID_ARG, "dtype must be ZL_F32 or ZL_BF16");
+  if (!(c->alpha > 0.f && c->alpha <= 1.f))
+    return fail(ZL_ERR_INVALID_ARG, "alpha must be in (0, 1]");
+  if (c->consis != ZL_KL_REVERSE && c->consis != ZL_KL_FORWARD)
+    return fail(ZL_ERR_INVALID_ARG, "consis must be ZL_KL_REVERSE or ZL_KL_FORWARD");
+  if (c->optimizer != ZL_ADAMW && c->optimizer != ZL_SGD)
+    return fail(ZL_ERR_INVALID_ARG, "optimizer must be ZL_ADAMW or ZL_SGD");
+  if (!(c->lr >= 0.f)) return fail(ZL_ERR_INVALID_ARG, "lr must be >= 0");
+  if (c->optimizer == ZL_ADAMW) {
+    if (!(c->beta1 >= 0.f && c->beta1 < 1.f) || !(c->beta2 >= 0.f && c->beta2 < 1.f))
+      return fail(ZL_ERR_INVALID_ARG, "betas must be in [0, 1)");
+    if (!(c->eps > 0.f)) return fail(ZL_ERR_INVALID_ARG, "eps must be > 0");
+    if (!(c->weight_decay >= 0.f)) return fail(ZL_ERR_INVALID_ARG, "weight_decay must be >= 0");
+  }
+  if (c->max_batch < 1 || c->max_seq < 1)
+    return fail(ZL_ERR_INVALID_ARG, "max_batch and max_seq must be >= 1");
+  if ((int64_t)c->max_batch * c->max_seq > (int64_t)1 << 24)
+    return fail(ZL_ERR_UNSUPPORTED, "max_batch * max_seq above 2^24 tokens");
+  return ZL_OK;
+}
+
+struct Layout {
+  std::vector<zl_tensor_desc> descs;
+  std::vector<LayerOff> lay;
+  size_t n_params = 0;
+};
+
+void build_layout(const zl_config& c, Layout& out) {
+  const Dims m = dims_of(c);
+  size_t off = 0;
+  auto add = [&](const char* name, int layer, int64_t r, int64_t cols, int ndim) -> size_t {
+    zl_tensor_desc t;
+    memset(&t, 0, sizeof(t));
+    strncpy(t.name, name, sizeof(t.name) - 1);
+    t.layer = layer;
+    t.ndim = ndim;
+    t.shape[0] = r;
+    t.shape[1] = cols;
+    t.offset = off;
+    t.numel = (size_t)r * cols;
+    out.descs.push_back(t);
+    const size_t at = off;
+    off = round_up(off + t.numel, ALIGN_ELEMS);
+    return at;
+  };
+  out.lay.resize(m.L);
+  for (int l = 0; l < m.L; ++l) {
+    LayerOff& o = out.lay[l];
+    memset(&o, 0, sizeof(o));
+    if (m.llama) {
+      o.ln1_w = add("ln1_w", l, m.d, 1, 1);
+      o.w_qkv = add("wq", l, m.dq, m.d, 2);
+      add("wk", l, m.dkv, m.d, 2);
+      add("wv", l, m.dkv, m.d, 2);
+      o.w_o = add("wo", l, m.d, m.dq, 2);
+      o.ln2_w = add("ln2_w", l, m.d, 1, 1);
+      o.w_up = add("wg", l, m.ff, m.d, 2);
+      add("wu", l, m.ff, m.d, 2);
+      o.w_down = add("wd", l, m.d, m.ff, 2);
+    } else {
+      o.ln1_w = add("ln1_w", l, m.d, 1, 1);
+      o.ln1_b = add("ln1_b", l, m.d, 1, 1);
+      o.w_qkv = add("wqkv", l, m.nqkv, m.d, 2);
+      o.b_qkv = add("bqkv", l, m.nqkv, 1, 1);
+      o.w_o = add("wo", l, m.d, m.dq, 2);
+      o.b_o = add("bo", l, m.d, 1, 1);
+      o.ln2_w = add("ln2_w", l, m.d, 1, 1);
+      o.ln2_b = add("ln2_b", l, m.d, 1, 1);
+      o.w_up = add("wfc", l, m.ff, m.d, 2);
+      o.b_up = add("bfc", l, m.ff, 1, 1);
+      o.w_down = add("wproj", l, m.d, m.ff, 2);
+      o.b_down = add("bproj", l, m.d, 1, 1);
+    }
+  }
+  out.n_params = off;
+}
+
+// Workspace plan: byte offsets of every region, 256-byte aligned.
+struct Plan {
+  size_t total = 0;
+  int Tmax = 0, R = 0, Vpad = 0, stk = 1;
+  size_t rope, seqlens, pos;
+  std::vector<size_t> X;  // L + 1
+  std::vector<size_t> N1, RS1, MU1, QKV, O, LSE, X2, N2, RS2, MU2, UP, ACT;
+  size_t DX, DXA, DUP, DN, DO, DQKV, DELTA, PART;
+  size_t HN, HRS, HMU, ZC, DZ, DNF, ROWLOSS, NOMEGA;
+  size_t part_elems;
+};
+
+void build_plan(const zl_config& c, Plan& p) {
+  const Dims m = dims_of(c);
+  const size_t act = c.dtype == ZL_BF16 ? 2 : 4;
+  const size_t T = (size_t)c.max_batch * c.max_seq;
+  p.Tmax = (int)T;
+  p.R = (int)(T < 4096 ? T : 4096);
+  p.Vpad = (int)round_up((size_t)m.V, 8);
+  p.stk = c.alpha < 1.f ? 2 : 1;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = round_up(off + (bytes ? bytes : 1), ALIGN_BYTES);
+    return at;
+  };
+  p.rope = take(m.llama ? (size_t)c.max_seq * (m.hd / 2) * 8 : 0);
+  p.seqlens = take((size_t)c.max_batch * 4);
+  p.pos = take(T * 4);
+  p.X.resize(m.L + 1);
+  p.N1.resize(m.L); p.RS1.resize(m.L); p.MU1.resize(m.L); p.QKV.resize(m.L); p.O.resize(m.L);
+  p.LSE.resize(m.L); p.X2.resize(m.L); p.N2.resize(m.L); p.RS2.resize(m.L); p.MU2.resize(m.L);
+  p.UP.resize(m.L); p.ACT.resize(m.L);
+  for (int l = 0; l < m.L; ++l) {
+    p.X[l] = take(T * m.d * 4);
+    p.N1[l] = take(T * m.d * act);
+    p.RS1[l] = take(T * 4);
+    p.MU1[l] = take(m.llama ? 0 : T * 4);
+    p.QKV[l] = take(T * m.nqkv * act);
+    p.O[l] = take(T * m.dq * act);
+    p.LSE[l] = take(T * m.hq * 4);
+    p.X2[l] = take(T * m.d * 4);
+    p.N2[l] = take(T * m.d * act);
+    p.RS2[l] = take(T * 4);
+    p.MU2[l] = take(m.llama ? 0 : T * 4);
+    p.UP[l] = take(T * m.nup * act);
+    p.ACT[l] = take(T * m.ff * act);
+  }
+  p.X[m.L] = take(T * m.d * 4);
+  p.DX = take(T * m.d * 4);
+  p.DXA = take(T * m.d * act);
+  p.DUP = take(T * m.nup * act);
+  p.DN = take(T * m.d * 4);
+  p.DO = take(T * m.dq * act);
+  p.DQKV = take(T * m.nqkv * act);
+  p.DELTA = take(T * m.hq * 4);
+  size_t pe = (size_t)2 * norm_bwd_blocks((int)T) * m.d;
+  size_t widest = m.nqkv > m.ff ? m.nqkv : m.ff;
+  if (m.d > (int)widest) widest = m.d;
+  const size_t pc = (size_t)colsum_blocks((int)T) * widest;
+  p.part_elems = pe > pc ? pe : pc;
+  p.PART = take(p.part_elems * 4);
+  const size_t R = p.R, S2 = (size_t)p.stk * R;
+  p.HN = take(S2 * m.d * act);
+  p.HRS = take(S2 * 4);
+  p.HMU = take(S2 * 4);
+  p.ZC = take(S2 * p.Vpad * 4);
+  p.DZ = take(R * p.Vpad * act);
+  p.DNF = take(R * m.d * 4);
+  p.ROWLOSS = take(T * 4);
+  p.NOMEGA = take(4);
+  p.total = off;
+}
+
+enum State { ST_IDLE = 0, ST_FORWARD = 1, ST_OBJECTIVE = 2 };
+
+}  // namespace
+
+struct zl_chunk {
+  zl_config cfg;
+  zl_buffers buf;
+  Dims m;
+  Layout layout;
+  Plan plan;
+  char* ws;
+  int act;          // activation dtype (F32/BF16)
+  int state;        // State
+  bool has_grad;    // a backward ran since the last step
+  bool grad_fresh;  // next backward overwrites the gradient
+  int64_t step;
+  int B, S, T;
+  // profiling (zl_profile_begin / zl_profile_end)
+  struct Rec { const char* name; double flops, bytes; };
+  bool prof_on = false;
+  std::vector<hipEvent_t> prof_ev;  // 2 per record
+  std::vector<Rec> prof_rec;
+  size_t prof_used = 0;
+
+  int prof_start(hipStream_t s) {
+    if (!prof_on || prof_used >= prof_rec.size()) return -1;
+    const int i = (int)prof_used++;
+    hipEventRecord(prof_ev[2 * i], s);
+    return i;
+  }
+  void prof_stop(int i, hipStream_t s, const char* name, double flops, double bytes) {
+    if (i < 0) return;
+    hipEventRecord(prof_ev[2 * i + 1], s);
+    prof_rec[i] = {name, flops, bytes};
+  }
+
+  template <typename P> P* at(size_t off) const { return reinterpret_cast<P*>(ws + off); }
+  const void* W(size_t off) const {  // a weight matrix as the kernels consume it
+    if (act == BF16) return reinterpret_cast<const bf16_t*>(buf.shadow) + off;
+    return buf.master + off;
+  }
+  const float* V32(size_t off) const { return buf.master + off; }
+  float* G(size_t off) const { return buf.grad + off; }
+  size_t asz() const { return act == BF16 ? 2 : 4; }
+  void* A(size_t base_off, size_t elem_off) const { return ws + base_off + elem_off * asz(); }
+};
+
+static hipStream_t S_(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+// ------------------------------------------------------------ GEMM helpers
+static GemmDesc gdesc(int M, int N, int K, const void* A, int64_t lda, bool ak, const void* B,
+                      int64_t ldb, bool bk) {
+  GemmDesc g;
+  g.M = M; g.N = N; g.K = K; g.ka = K; g.kb = K;
+  g.A = A; g.lda = lda; g.a_kmajor = ak;
+  g.B = B; g.ldb = ldb; g.b_kmajor = bk;
+  return g;
+}
+
+static EpiArgs epi(EpiKind k, void* out, int64_t ldo, int dt) {
+  EpiArgs e;
+  memset(&e, 0, sizeof(e));
+  e.kind = k; e.out = out; e.ldo = ldo; e.out_dtype = dt; e.scale = 1.f;
+  return e;
+}
+
+// Launch wrappers that time the launch when profiling is on.
+static hipError_t run_gemm(zl_chunk* c, hipStream_t s, const GemmDesc& g, const EpiArgs& e,
+                           double k_alg = -1) {
+  const int pi = c->prof_start(s);
+  const char* kn = "gemm";
+  hipError_t err = launch_gemm(g, e, c->act, s, &kn);
+  c->prof_stop(pi, s, kn, 2.0 * g.M * g.N * (k_alg < 0 ? g.K : k_alg), 0.0);
+  return err;
+}
+
+#define ZL_RUN(name, flops, bytes, call)                                             \
+  do {                                                                              \
+    const int pi_ = c->prof_start(s);                                               \
+    hipError_t e_ = (call);                                                         \
+    c->prof_stop(pi_, s, name, (double)(flops), (double)(bytes));                   \
+    if (e_ != hipSuccess)                                                           \
+      return fail(ZL_ERR_HIP, std::string(#call) + ": " + hipGetErrorString(e_));   \
+  } while (0)
+
+// ---------------------------------------------------------------- public
+extern "C" {
+
+const char* zl_status_string(zl_status s) {
+  switch (s) {
+    case ZL_OK: return "ZL_OK";
+    case ZL_ERR_INVALID_ARG: return "ZL_ERR_INVALID_ARG";
+    case ZL_ERR_UNSUPPORTED: return "ZL_ERR_UNSUPPORTED";
+    case ZL_ERR_HIP: return "ZL_ERR_HIP";
+    case ZL_ERR_STATE: return "ZL_ERR_STATE";
+    case ZL_ERR_WORKSPACE: return "ZL_ERR_WORKSPACE";
+  }
+  return "unknown zl_status";
+}
+
+const char* zl_last_error(void) { return g_err.c_str(); }
+
+zl_status zl_param_layout(const zl_config* cfg, size_t* n_params, zl_tensor_desc* descs,
+                          int* n_descs) {
+  zl_status st = check_config(cfg);
+  if (st != ZL_OK) return st;
+  if (!n_params) return fail(ZL_ERR_INVALID_ARG, "n_params is NULL");
+  Layout L;
+  build_layout(*cfg, L);
+  *n_params = L.n_params;
+  if (descs) {
+    if (!n_descs) return fail(ZL_ERR_INVALID_ARG, "n_descs is NULL");
+    if (*n_descs < (int)L.descs.size())
+      return fail(ZL_ERR_INVALID_ARG, "descs array too small: need " +
+                                          std::to_string(L.descs.size()));
+    memcpy(descs, L.descs.data(), L.descs.size() * sizeof(zl_tensor_desc));
+  }
+  if (n_descs) *n_descs = (int)L.descs.size();
+  return ZL_OK;
+}
+
+zl_status zl_workspace_size(const zl_config* cfg, size_t* bytes) {
+  zl_status st = check_config(cfg);
+  if (st != ZL_OK) return st;
+  if (!bytes) return fail(ZL_ERR_INVALID_ARG, "bytes is NULL");
+  Plan p;
+  build_plan(*cfg, p);
+  *bytes = p.total;
+  return ZL_OK;
+}
+
+zl_status zl_chunk_create(const zl_config* cfg, const zl_buffers* bufs, void* workspace,
+                          size_t ws_bytes, zl_chunk** out) {
+  if (!out) return fail(ZL_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  zl_status st = check_config(cfg);
+  if (st != ZL_OK) return st;
+  if (!bufs) return fail(ZL_ERR_INVALID_ARG, "bufs is NULL");
+  if (!bufs->master || !bufs->grad) return fail(ZL_ERR_INVALID_ARG, "master and grad required");
+  if (cfg->dtype == ZL_BF16 && !bufs->shadow)
+    return fail(ZL_ERR_INVALID_ARG, "bf16 mode needs a shadow buffer");
+  if (cfg->optimizer == ZL_ADAMW && (!bufs->adam_m || !bufs->adam_v))
+    return fail(ZL_ERR_INVALID_ARG, "AdamW needs adam_m and adam_v");
+  if (!bufs->head_w || !bufs->head_norm_w)
+    return fail(ZL_ERR_INVALID_ARG, "head_w and head_norm_w required");
+  if (cfg->arch == ZL_ARCH_GPT2 && !bufs->head_norm_b)
+    return fail(ZL_ERR_INVALID_ARG, "gpt2 needs head_norm_b");
+  const uintptr_t al = (uintptr_t)bufs->master | (uintptr_t)bufs->grad |
+                       (uintptr_t)bufs->head_w | (uintptr_t)(bufs->shadow) |
+                       (uintptr_t)bufs->adam_m | (uintptr_t)bufs->adam_v;
+  if (al % 16) return fail(ZL_ERR_INVALID_ARG, "buffers must be 16-byte aligned");
+  Plan p;
+  build_plan(*cfg, p);
+  if (!workspace) return fail(ZL_ERR_WORKSPACE, "workspace is NULL");
+  if ((uintptr_t)workspace % ALIGN_BYTES)
+    return fail(ZL_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (ws_bytes < p.total)
+    return fail(ZL_ERR_WORKSPACE, "workspace too small: need " + std::to_string(p.total));
+  zl_chunk* c = new (std::nothrow) zl_chunk();
+  if (!c) return fail(ZL_ERR_INVALID_ARG, "out of host memory");
+  c->cfg = *cfg;
+  c->buf = *bufs;
+  c->m = dims_of(*cfg);
+  build_layout(*cfg, c->layout);
+  c->plan = p;
+  c->ws = reinterpret_cast<char*>(workspace);
+  c->act = cfg->dtype == ZL_BF16 ? BF16 : F32;
+  c->state = ST_IDLE;
+  c->has_grad = false;
+  c->grad_fresh = true;
+  c->step = 0;
+  c->B = c->S = c->T = 0;
+  if (c->m.llama) {
+    hipError_t e = launch_rope_table(c->at<float2>(p.rope), cfg->max_seq, c->m.hd / 2,
+                                     (double)cfg->rope_theta, nullptr);
+    if (e == hipSuccess) e = hipStreamSynchronize(nullptr);
+    if (e != hipSuccess) {
+      delete c;
+      return fail(ZL_ERR_HIP, std::string("rope table: ") + hipGetErrorString(e));
+    }
+  }
+  *out = c;
+  return ZL_OK;
+}
+
+void zl_chunk_destroy(zl_chunk* chunk) {
+  if (!chunk) return;
+  for (hipEvent_t e : chunk->prof_ev) hipEventDestroy(e);
+  delete chunk;
+}
+
+zl_status zl_refresh_shadow(zl_chunk* c, void* stream) {
+  if (!c) return fail(ZL_ERR_INVALID_ARG, "chunk is NULL");
+  if (c->act != BF16) return ZL_OK;
+  ZL_HIP(launch_shadow(c->buf.master, reinterpret_cast<bf16_t*>(c->buf.shadow),
+                       c->layout.n_params, S_(stream)));
+  return ZL_OK;
+}
+
+zl_status zl_get_step(const zl_chunk* c, int64_t* step) {
+  if (!c || !step) return fail(ZL_ERR_INVALID_ARG, "NULL argument");
+  *step = c->step;
+  return ZL_OK;
+}
+
+zl_status zl_set_step(zl_chunk* c, int64_t step) {
+  if (!c) return fail(ZL_ERR_INVALID_ARG, "chunk is NULL");
+  if (step < 0) return fail(ZL_ERR_INVALID_ARG, "step must be >= 0");
+  c->step = step;
+  return ZL_OK;
+}
+
+// --------------------------------------------------------------- forward
+zl_status zl_chunk_forward(zl_chunk* c, const void* h_in, const int32_t* seq_lens,
+                           const int32_t* pos_ids, int B, int S, void* h_out, void* stream) {
+  if (!c) return fail(ZL_ERR_INVALID_ARG, "chunk is NULL");
+  if (!h_in || !h_out) return fail(ZL_ERR_INVALID_ARG, "h_in and h_out required");
+  if (h_in == h_out) return fail(ZL_ERR_INVALID_ARG, "h_out must not alias h_in");
+  if (B < 1 || S < 1 || B > c->cfg.max_batch || S > c->cfg.max_seq)
+    return fail(ZL_ERR_INVALID_ARG, "B or S out of range");
+  if (((uintptr_t)h_in | (uintptr_t)h_out) % 16)
+    return fail(ZL_ERR_INVALID_ARG, "h_in and h_out must be 16-byte aligned");
+  hipStream_t s = S_(stream);
+  const Dims& m = c->m;
+  const Plan& p = c->plan;
+  const int T = B * S;
+  const int act = c->act;
+  const bool ln = !m.llama;
+  const float eps = c->cfg.norm_eps;
+  int32_t* sl = c->at<int32_t>(p.seqlens);
+  int32_t* pos = c->at<int32_t>(p.pos);
+  ZL_RUN("copy_inputs", 0, B * 8, launch_copy_i32(seq_lens, sl, B, 1, 0, S, s));
+  ZL_RUN("copy_inputs", 0, (double)T * 8, launch_copy_i32(pos_ids, pos, T, 1, 1, S, s));
+  ZL_RUN("cast", 0, (double)T * m.d * (4 + c->asz()), launch_cast(h_in, act, c->at<float>(p.X[0]), F32, (size_t)T * m.d, s));
+  for (int l = 0; l < m.L; ++l) {
+    const LayerOff& o = c->layout.lay[l];
+    float* X = c->at<float>(p.X[l]);
+    float* X2 = c->at<float>(p.X2[l]);
+    void* N1 = c->ws + p.N1[l];
+    void* N2 = c->ws + p.N2[l];
+    void* QKV = c->ws + p.QKV[l];
+    void* O = c->ws + p.O[l];
+    void* UP = c->ws + p.UP[l];
+    void* ACT = c->ws + p.ACT[l];
+    ZL_RUN("norm_fwd", 0, (double)T * m.d * (4 + c->asz()), launch_norm_fwd(ln, X, m.d, c->V32(o.ln1_w), ln ? c->V32(o.ln1_b) : nullptr, N1, m.d,
+                           act, ln ? c->at<float>(p.MU1[l]) : nullptr, c->at<float>(p.RS1[l]),
+                           T, m.d, eps, s));
+    // bf16: RoPE is applied in the QKV GEMM epilogue (one rounding of q, k)
+    const bool rope_in_gemm = m.llama && act == BF16 && m.hd <= 128;
+    {
+      EpiArgs e = epi(rope_in_gemm ? EPI_ROPE : EPI_STORE, QKV, m.nqkv, act);
+      e.bias = ln ? c->V32(o.b_qkv) : nullptr;
+      if (rope_in_gemm) {
+        e.pos = pos; e.rope = c->at<float2>(p.rope); e.max_pos = c->cfg.max_seq;
+        e.hd = m.hd; e.n_rot = (m.hq + m.hkv) * m.hd;
+      }
+      ZL_HIP(run_gemm(c, s, gdesc(T, m.nqkv, m.d, N1, m.d, true, c->W(o.w_qkv), m.d, true), e));
+    }
+    if (m.llama && !rope_in_gemm)
+      ZL_RUN("rope", 0, 2.0 * T * (m.hq + m.hkv) * m.hd * c->asz(),
+             launch_rope(QKV, m.nqkv, act, pos, c->at<float2>(p.rope), c->cfg.max_seq, T,
+                         m.hq + m.hkv, m.hd, +1, s));
+    {
+      AttnDesc a;
+      memset(&a, 0, sizeof(a));
+      a.B = B; a.S = S; a.Hq = m.hq; a.Hkv = m.hkv; a.hd = m.hd;
+      a.q = QKV; a.k = c->A(p.QKV[l], m.dq); a.v = c->A(p.QKV[l], m.dq + m.dkv);
+      a.ldq = a.ldk = a.ldv = m.nqkv;
+      a.o = O; a.ldo = m.dq;
+      a.lse = c->at<float>(p.LSE[l]);
+      a.seq_lens = sl;
+      a.scale = 1.f / sqrtf((float)m.hd);
+      ZL_RUN("attn_fwd", 2.0 * B * m.hq * m.hd * (double)S * (S + 1), 0, launch_attn_fwd(a, act, s));
+    }
+    {
+      EpiArgs e = epi(EPI_RESID, X2, m.d, F32);
+      e.resid = X; e.ldr = m.d;
+      e.bias = ln ? c->V32(o.b_o) : nullptr;
+      ZL_HIP(run_gemm(c, s, gdesc(T, m.d, m.dq, O, m.dq, true, c->W(o.w_o), m.dq, true), e));
+    }
+    ZL_RUN("norm_fwd", 0, (double)T * m.d * (4 + c->asz()), launch_norm_fwd(ln, X2, m.d, c->V32(o.ln2_w), ln ? c->V32(o.ln2_b) : nullptr, N2, m.d,
+                           act, ln ? c->at<float>(p.MU2[l]) : nullptr, c->at<float>(p.RS2[l]),
+                           T, m.d, eps, s));
+    if (m.llama) {
+      EpiArgs e = epi(EPI_STORE, UP, m.nup, act);
+      ZL_HIP(run_gemm(c, s, gdesc(T, m.nup, m.d, N2, m.d, true, c->W(o.w_up), m.d, true), e));
+      ZL_RUN("swiglu_fwd", 0, 3.0 * T * m.ff * c->asz(), launch_swiglu_fwd(UP, m.nup, ACT, m.ff, act, T, m.ff, s));
+    } else {
+      EpiArgs e = epi(EPI_GELU, ACT, m.ff, act);
+      e.out2 = UP; e.ldo2 = m.nup;
+      e.bias = c->V32(o.b_up);
+      ZL_HIP(run_gemm(c, s, gdesc(T, m.ff, m.d, N2, m.d, true, c->W(o.w_up), m.d, true), e));
+    }
+    {
+      EpiArgs e = epi(EPI_RESID, c->at<float>(p.X[l + 1]), m.d, F32);
+      e.resid = X2; e.ldr = m.d;
+      e.bias = ln ? c->V32(o.b_down) : nullptr;
+      ZL_HIP(run_gemm(c, s, gdesc(T, m.d, m.ff, ACT, m.ff, true, c->W(o.w_down), m.ff, true), e));
+    }
+  }
+  ZL_RUN("cast", 0, (double)T * m.d * (4 + c->asz()), launch_cast(c->at<float>(p.X[m.L]), F32, h_out, act, (size_t)T * m.d, s));
+  c->B = B; c->S = S; c->T = T;
+  c->state = ST_FORWARD;
+  return ZL_OK;
+}
+
+// ------------------------------------------------------------- objective
+zl_status zl_local_objective(zl_chunk* c, const int32_t* labels, float* loss_out, void* stream) {
+  if (!c) return fail(ZL_ERR_INVALID_ARG, "chunk is NULL");
+  if (!labels || !loss_out) return fail(ZL_ERR_INVALID_ARG, "labels and loss_out required");
+  if (c->state != ST_FORWARD && c->state != ST_OBJECTIVE)
+    return fail(ZL_ERR_STATE, "zl_local_objective needs a preceding zl_chunk_forward");
+  hipStream_t s = S_(stream);
+  const Dims& m = c->m;
+  const Plan& p = c->plan;
+  const int T = c->T;
+  const int act = c->act;
+  const bool ln = !m.llama;
+  const int stk = p.stk;
+  float* nomega = c->at<float>(p.NOMEGA);
+  ZL_RUN("count_omega", 0, (double)T * 4, launch_count_omega(labels, T, m.V, nomega, s));
+  const float* hout = c->at<float>(p.X[m.L]);
+  const float* hin = c->at<float>(p.X[0]);
+  for (int r0 = 0; r0 < T; r0 += p.R) {
+    const int rows = T - r0 < p.R ? T - r0 : p.R;
+    ZL_RUN("head_norm", 0, (double)stk * rows * m.d * (4 + c->asz()), launch_head_norm(ln, hout, stk == 2 ? hin : nullptr, m.d, r0, rows,
+                            c->buf.head_norm_w, c->buf.head_norm_b, c->ws + p.HN, act,
+                            ln ? c->at<float>(p.HMU) : nullptr, c->at<float>(p.HRS), m.d,
+                            c->cfg.norm_eps, s));
+    {
+      EpiArgs e = epi(EPI_STORE, c->at<float>(p.ZC), p.Vpad, F32);
+      ZL_HIP(run_gemm(c, s, gdesc(stk * rows, m.V, m.d, c->ws + p.HN, m.d, true, c->buf.head_w, m.d,
+                               true), e));
+    }
+    {
+      ObjDesc o;
+      o.zc = c->at<float>(p.ZC); o.ldz = p.Vpad; o.stacked = stk;
+      o.labels = labels + r0; o.rows = rows; o.V = m.V; o.Vpad = p.Vpad;
+      o.alpha = c->cfg.alpha; o.consis = c->cfg.consis; o.n_omega = nomega;
+      o.dz = c->ws + p.DZ; o.lddz = p.Vpad; o.dz_dtype = act;
+      o.row_loss = c->at<float>(p.ROWLOSS) + r0;
+      ZL_RUN("objective_rows", 0, (double)rows * (stk * 4.0 * m.V + c->asz() * p.Vpad), launch_objective_rows(o, s));
+    }
+    {
+      GemmDesc g = gdesc(rows, m.d, p.Vpad, c->ws + p.DZ, p.Vpad, true, c->buf.head_w, m.d, false);
+      g.kb = m.V;
+      EpiArgs e = epi(EPI_STORE, c->at<float>(p.DNF), m.d, F32);
+      ZL_HIP(run_gemm(c, s, g, e, (double)m.V));
+    }
+    ZL_RUN("head_norm_bwd", 0, (double)rows * m.d * (12 + c->asz()), launch_head_norm_bwd(ln, c->at<float>(p.DNF), m.d, hout, c->buf.head_norm_w,
+                                ln ? c->at<float>(p.HMU) : nullptr, c->at<float>(p.HRS), stk,
+                                c->at<float>(p.DX), c->ws + p.DXA, act, r0, rows, m.d, s));
+  }
+  ZL_RUN("loss_reduce", 0, (double)T * 4, launch_loss_reduce(c->at<float>(p.ROWLOSS), T, nomega, loss_out, s));
+  c->state = ST_OBJECTIVE;
+  return ZL_OK;
+}
+
+// -------------------------------------------------------------- backward
+zl_status zl_chunk_backward(zl_chunk* c, float grad_scale, int accumulate, void* stream) {
+  if (!c) return fail(ZL_ERR_INVALID_ARG, "chunk is NULL");
+  if (c->state != ST_OBJECTIVE)
+    return fail(ZL_ERR_STATE, "zl_chunk_backward needs a preceding zl_local_objective");
+  if (!isfinite(grad_scale)) return fail(ZL_ERR_INVALID_ARG, "grad_scale must be finite");
+  hipStream_t s = S_(stream);
+  const Dims& m = c->m;
+  const Plan& p = c->plan;
+  const int T = c->T;
+  const int act = c->act;
+  const bool ln = !m.llama;
+  const int acc = (accumulate && !c->grad_fresh) ? 1 : 0;
+  float* DX = c->at<float>(p.DX);
+  void* DXA = c->ws + p.DXA;
+  void* DUP = c->ws + p.DUP;
+  float* DN = c->at<float>(p.DN);
+  void* DO = c->ws + p.DO;
+  void* DQKV = c->ws + p.DQKV;
+  float* PART = c->at<float>(p.PART);
+  const size_t half_part = p.part_elems / 2;
+
+  auto wgrad = [&](int M, int N, const void* A, int64_t lda, const void* Bm, int64_t ldb,
+                   size_t goff) -> hipError_t {
+    EpiArgs e = epi(EPI_GRAD, c->G(goff), N, F32);
+    e.scale = grad_scale;
+    e.accumulate = acc;
+    return run_gemm(c, s, gdesc(M, N, T, A, lda, false, Bm, ldb, false), e);
+  };
+  auto bias_grad = [&](const void* x, int dt, int n, size_t goff) -> hipError_t {
+    int nblk = 0;
+    int pi = c->prof_start(s);
+    hipError_t e = launch_colsum_partial(x, n, dt, T, n, PART, &nblk, s);
+    c->prof_stop(pi, s, "colsum", 0, (double)T * n * (dt == BF16 ? 2 : 4));
+    if (e != hipSuccess) return e;
+    pi = c->prof_start(s);
+    e = launch_reduce_rows(PART, nblk, n, c->G(goff), grad_scale, acc, s);
+    c->prof_stop(pi, s, "reduce_rows", 0, 0);
+    return e;
+  };
+
+  for (int l = m.L - 1; l >= 0; --l) {
+    const LayerOff& o = c->layout.lay[l];
+    bool rope_fused = false;
+    // down projection
+    {
+      EpiArgs e = epi(m.llama ? EPI_SWIGLU_BWD : EPI_GELU_BWD, DUP, m.nup, act);
+      e.aux = c->ws + p.UP[l]; e.ldaux = m.nup; e.ff = m.ff;
+      ZL_HIP(run_gemm(c, s, gdesc(T, m.ff, m.d, DXA, m.d, true, c->W(o.w_down), m.ff, false), e));
+    }
+    ZL_HIP(wgrad(m.d, m.ff, DXA, m.d, c->ws + p.ACT[l], m.ff, o.w_down));
+    if (ln) ZL_HIP(bias_grad(DX, F32, m.d, o.b_down));
+    // up projection (gate|up or fc)
+    {
+      EpiArgs e = epi(EPI_STORE, DN, m.d, F32);
+      ZL_HIP(run_gemm(c, s, gdesc(T, m.d, m.nup, DUP, m.nup, true, c->W(o.w_up), m.d, false), e));
+    }
+    ZL_HIP(wgrad(m.nup, m.d, DUP, m.nup, c->ws + p.N2[l], m.d, o.w_up));
+    if (ln) ZL_HIP(bias_grad(DUP, act, m.nup, o.b_up));
+    // norm 2
+    {
+      int nblk = 0;
+      ZL_RUN("norm_bwd", 0, (double)T * m.d * (16 + c->asz()), launch_norm_bwd(ln, DN, c->at<float>(p.X2[l]), c->V32(o.ln2_w),
+                             ln ? c->at<float>(p.MU2[l]) : nullptr, c->at<float>(p.RS2[l]), DX, DX,
+                             DXA, act, PART, ln ? PART + half_part : nullptr, T, m.d, s, &nblk));
+      ZL_RUN("reduce_rows", 0, 0, launch_reduce_rows(PART, nblk, m.d, c->G(o.ln2_w), grad_scale, acc, s));
+      if (ln) ZL_RUN("reduce_rows", 0, 0, launch_reduce_rows(PART + half_part, nblk, m.d, c->G(o.ln2_b), grad_scale, acc, s));
+    }
+    // output projection
+    {
+      EpiArgs e = epi(EPI_STORE, DO, m.dq, act);
+      ZL_HIP(run_gemm(c, s, gdesc(T, m.dq, m.d, DXA, m.d, true, c->W(o.w_o), m.dq, false), e));
+    }
+    ZL_HIP(wgrad(m.d, m.dq, DXA, m.d, c->ws + p.O[l], m.dq, o.w_o));
+    if (ln) ZL_HIP(bias_grad(DX, F32, m.d, o.b_o));
+    // attention
+    {
+      AttnDesc a;
+      memset(&a, 0, sizeof(a));
+      a.B = c->B; a.S = c->S; a.Hq = m.hq; a.Hkv = m.hkv; a.hd = m.hd;
+      a.q = c->ws + p.QKV[l]; a.k = c->A(p.QKV[l], m.dq); a.v = c->A(p.QKV[l], m.dq + m.dkv);
+      a.ldq = a.ldk = a.ldv = m.nqkv;
+      a.o = c->ws + p.O[l]; a.ldo = m.dq;
+      a.lse = c->at<float>(p.LSE[l]);
+      a.seq_lens = c->at<int32_t>(p.seqlens);
+      a.dout = DO; a.lddo = m.dq;
+      a.delta = c->at<float>(p.DELTA);
+      a.dq = DQKV; a.dk = c->A(p.DQKV, m.dq); a.dv = c->A(p.DQKV, m.dq + m.dkv);
+      a.lddq = a.lddk = a.lddv = m.nqkv;
+      a.scale = 1.f / sqrtf((float)m.hd);
+      if (m.llama) {
+        a.pos = c->at<int32_t>(p.pos); a.rope = c->at<float2>(p.rope); a.max_pos = c->cfg.max_seq;
+      }
+      ZL_RUN("attn_bwd", 4.0 * c->B * m.hq * m.hd * (double)c->S * (c->S + 1), 0,
+             launch_attn_bwd(a, act, s, &rope_fused));
+    }
+    if (m.llama && !rope_fused)
+      ZL_RUN("rope", 0, 2.0 * T * (m.hq + m.hkv) * m.hd * c->asz(),
+             launch_rope(DQKV, m.nqkv, act, c->at<int32_t>(p.pos), c->at<float2>(p.rope),
+                         c->cfg.max_seq, T, m.hq + m.hkv, m.hd, -1, s));
+    // QKV projection
+    {
+      EpiArgs e = epi(EPI_STORE, DN, m.d, F32);
+      ZL_HIP(run_gemm(c, s, gdesc(T, m.d, m.nqkv, DQKV, m.nqkv, true, c->W(o.w_qkv), m.d, false), e));
+    }
+    ZL_HIP(wgrad(m.nqkv, m.d, DQKV, m.nqkv, c->ws + p.N1[l], m.d, o.w_qkv));
+    if (ln) ZL_HIP(bias_grad(DQKV, act, m.nqkv, o.b_qkv));
+    // norm 1; layer 0 forms no gradient into h_in
+    {
+      int nblk = 0;
+      float* dx = l > 0 ? DX : nullptr;
+      ZL_RUN("norm_bwd", 0, (double)T * m.d * (16 + c->asz()), launch_norm_bwd(ln, DN, c->at<float>(p.X[l]), c->V32(o.ln1_w),
+                             ln ? c->at<float>(p.MU1[l]) : nullptr, c->at<float>(p.RS1[l]), dx, dx,
+                             l > 0 ? DXA : nullptr, act, PART, ln ? PART + half_part : nullptr, T,
+                             m.d, s, &nblk));
+      ZL_RUN("reduce_rows", 0, 0, launch_reduce_rows(PART, nblk, m.d, c->G(o.ln1_w), grad_scale, acc, s));
+      if (ln) ZL_RUN("reduce_rows", 0, 0, launch_reduce_rows(PART + half_part, nblk, m.d, c->G(o.ln1_b), grad_scale, acc, s));
+    }
+  }
+  c->state = ST_IDLE;
+  c->has_grad = true;
+  c->grad_fresh = false;
+  return ZL_OK;
+}
+
+// ------------------------------------------------------------- optimizer
+zl_status zl_optimizer_step(zl_chunk* c, void* stream) {
+  if (!c) return fail(ZL_ERR_INVALID_ARG, "chunk is NULL");
+  if (!c->has_grad)
+    return fail(ZL_ERR_STATE, "zl_optimizer_step needs a zl_chunk_backward since the last step");
+  OptDesc o;
+  o.master = c->buf.master;
+  o.shadow = c->act == BF16 ? reinterpret_cast<bf16_t*>(c->buf.shadow) : nullptr;
+  o.grad = c->buf.grad;
+  o.m = c->buf.adam_m;
+  o.v = c->buf.adam_v;
+  o.n = c->layout.n_params;
+  o.optimizer = c->cfg.optimizer == ZL_ADAMW ? 0 : 1;
+  o.lr = c->cfg.lr; o.beta1 = c->cfg.beta1; o.beta2 = c->cfg.beta2;
+  o.eps = c->cfg.eps; o.wd = c->cfg.weight_decay;
+  const double t = (double)(c->step + 1);
+  o.bc1 = (float)(1.0 - pow((double)c->cfg.beta1, t));
+  o.bc2 = (float)(1.0 - pow((double)c->cfg.beta2, t));
+  hipStream_t s = S_(stream);
+  ZL_RUN("optimizer", 0, (double)o.n * (o.optimizer == 0 ? 28.0 : 12.0) + (o.shadow ? 2.0 * o.n : 0.0),
+         launch_optimizer(o, s));
+  c->step += 1;
+  c->has_grad = false;
+  c->grad_fresh = true;
+  return ZL_OK;
+}
+
+zl_status zl_chunk_update(zl_chunk* c, const void* h_in, const int32_t* seq_lens,
+                          const int32_t* pos_ids, const int32_t* labels, int B, int S,
+                          void* h_out, float* loss_out, void* stream) {
+  if (!c) return fail(ZL_ERR_INVALID_ARG, "chunk is NULL");
+  if (!labels || !loss_out) return fail(ZL_ERR_INVALID_ARG, "labels and loss_out required");
+  zl_status st = zl_chunk_forward(c, h_in, seq_lens, pos_ids, B, S, h_out, stream);
+  if (st != ZL_OK) return st;
+  st = zl_local_objective(c, labels, loss_out, stream);
+  if (st != ZL_OK) return st;
+  st = zl_chunk_backward(c, 1.f, 0, stream);
+  if (st != ZL_OK) return st;
+  return zl_optimizer_step(c, stream);
+}
+
+// ------------------------------------------------------------- inspection
+zl_status zl_inspect(const zl_chunk* c, const char* name, int layer, zl_view* v) {
+  if (!c || !name || !v) return fail(ZL_ERR_INVALID_ARG, "NULL argument");
+  const Dims& m = c->m;
+  const Plan& p = c->plan;
+  const int T = c->T;
+  const int act = c->act == BF16 ? ZL_BF16 : ZL_F32;
+  auto set = [&](size_t off, int64_t rows, int64_t cols, int dt) {
+    v->ptr = c->ws + off; v->rows = rows; v->cols = cols; v->ld = cols; v->dtype = dt;
+    return ZL_OK;
+  };
+  const std::string n(name);
+  if (n == "x") {
+    if (layer < 0 || layer > m.L) return fail(ZL_ERR_INVALID_ARG, "layer out of range");
+    return set(p.X[layer], T, m.d, ZL_F32);
+  }
+  if (n == "dh_out") return set(p.DX, T, m.d, ZL_F32);
+  if (n == "row_loss") return set(p.ROWLOSS, T, 1, ZL_F32);
+  if (n == "n_omega") return set(p.NOMEGA, 1, 1, ZL_F32);
+  if (layer < 0 || layer >= m.L) return fail(ZL_ERR_INVALID_ARG, "layer out of range");
+  if (n == "n1") return set(p.N1[layer], T, m.d, act);
+  if (n == "qkv") return set(p.QKV[layer], T, m.nqkv, act);
+  if (n == "o") return set(p.O[layer], T, m.dq, act);
+  if (n == "lse") return set(p.LSE[layer], (int64_t)c->B * m.hq, c->S, ZL_F32);
+  if (n == "x2") return set(p.X2[layer], T, m.d, ZL_F32);
+  if (n == "n2") return set(p.N2[layer], T, m.d, act);
+  if (n == "up") return set(p.UP[layer], T, m.nup, act);
+  if (n == "act") return set(p.ACT[layer], T, m.ff, act);
+  if (n == "rstd1") return set(p.RS1[layer], T, 1, ZL_F32);
+  if (n == "rstd2") return set(p.RS2[layer], T, 1, ZL_F32);
+  return fail(ZL_ERR_INVALID_ARG, "unknown view name: " + n);
+}
+
+zl_status zl_profile_begin(zl_chunk* c, int capacity) {
+  if (!c) return fail(ZL_ERR_INVALID_ARG, "chunk is NULL");
+  if (capacity < 1 || capacity > (1 << 20)) return fail(ZL_ERR_INVALID_ARG, "bad capacity");
+  while (c->prof_ev.size() < (size_t)capacity * 2) {
+    hipEvent_t e;
+    ZL_HIP(hipEventCreate(&e));
+    c->prof_ev.push_back(e);
+  }
+  c->prof_rec.assign((size_t)capacity, zl_chunk::Rec{nullptr, 0, 0});
+  c->prof_used = 0;
+  c->prof_on = true;
+  return ZL_OK;
+}
+
+zl_status zl_profile_end(zl_chunk* c, zl_profile_entry* out, int* n) {
+  if (!c || !n) return fail(ZL_ERR_INVALID_ARG, "NULL argument");
+  if (!c->prof_on) return fail(ZL_ERR_STATE, "profiling was not begun");
+  c->prof_on = false;
+  std::vector<zl_profile_entry> agg;
+  for (size_t i = 0; i < c->prof_used; ++i) {
+    const zl_chunk::Rec& r = c->prof_rec[i];
+    if (!r.name) continue;
+    ZL_HIP(hipEventSynchronize(c->prof_ev[2 * i + 1]));
+    float ms = 0.f;
+    ZL_HIP(hipEventElapsedTime(&ms, c->prof_ev[2 * i], c->prof_ev[2 * i + 1]));
+    zl_profile_entry* e = nullptr;
+    for (auto& a : agg)
+      if (strncmp(a.name, r.name, sizeof(a.name)) == 0) e = &a;
+    if (!e) {
+      zl_profile_entry z;
+      memset(&z, 0, sizeof(z));
+      strncpy(z.name, r.name, sizeof(z.name) - 1);
+      agg.push_back(z);
+      e = &agg.back();
+    }
+    e->launches += 1;
+    e->total_ms += ms;
+    e->flops += r.flops;
+    e->bytes += r.bytes;
+  }
+  const int cap = *n;
+  *n = (int)agg.size();
+  if (out) memcpy(out, agg.data(), sizeof(zl_profile_entry) * (size_t)(cap < *n ? cap : *n));
+  c->prof_used = 0;
+  return ZL_OK;
+}
+
+zl_status zl_kernel_gemm(int M, int N, int K, const void* A, int64_t lda, int a_kmajor,
+                         const void* B, int64_t ldb, int b_kmajor, float* C, int64_t ldc,
+                         int dtype, void* stream) {
+  if (M < 0 || N < 0 || K < 0 || !A || !B || !C) return fail(ZL_ERR_INVALID_ARG, "bad gemm args");
+  if (dtype != ZL_F32 && dtype != ZL_BF16) return fail(ZL_ERR_INVALID_ARG, "bad dtype");
+  if (dtype == ZL_BF16) {
+    const int64_t ca = a_kmajor ? K : M, cb = b_kmajor ? K : N;
+    if (ca % 8 || cb % 8 || lda % 8 || ldb % 8 || ((uintptr_t)A | (uintptr_t)B) % 16)
+      return fail(ZL_ERR_INVALID_ARG, "bf16 gemm needs 8-element contiguous dims and alignment");
+  }
+  GemmDesc g = gdesc(M, N, K, A, lda, a_kmajor != 0, B, ldb, b_kmajor != 0);
+  EpiArgs e = epi(EPI_STORE, C, ldc, F32);
+  ZL_HIP(launch_gemm(g, e, dtype == ZL_BF16 ? BF16 : F32, S_(stream)));
+  return ZL_OK;
+}
+
+zl_status zl_kernel_attention(int B, int S, int Hq, int Hkv, int hd, const void* q,
+                              const void* k, const void* v, int64_t ld_qkv,
+                              const int32_t* seq_lens, void* o, float* lse, const void* dout,
+                              void* dq, void* dk, void* dv, float* delta, int dtype,
+                              int backward, void* stream) {
+  if (B < 1 || S < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || !q || !k || !v || !o || !lse || !seq_lens)
+    return fail(ZL_ERR_INVALID_ARG, "bad attention args");
+  if (hd != 16 && hd != 32 && hd != 64 && hd != 128)
+    return fail(ZL_ERR_UNSUPPORTED, "head_dim must be 16, 32, 64 or 128");
+  if (backward && (!dout || !dq || !dk || !dv || !delta))
+    return fail(ZL_ERR_INVALID_ARG, "backward needs dout, dq, dk, dv and delta");
+  AttnDesc a;
+  memset(&a, 0, sizeof(a));
+  a.B = B; a.S = S; a.Hq = Hq; a.Hkv = Hkv; a.hd = hd;
+  a.q = q; a.k = k; a.v = v; a.ldq = a.ldk = a.ldv = ld_qkv;
+  a.o = o; a.ldo = (int64_t)Hq * hd; a.lse = lse; a.seq_lens = seq_lens;
+  a.dout = dout; a.lddo = (int64_t)Hq * hd; a.delta = delta;
+  a.dq = dq; a.dk = dk; a.dv = dv; a.lddq = a.lddk = a.lddv = ld_qkv;
+  a.scale = 1.f / sqrtf((float)hd);
+  const int dt = dtype == ZL_BF16 ? BF16 : F32;
+  bool fused = false;
+  if (backward) ZL_HIP(launch_attn_bwd(a, dt, S_(stream), &fused));
+  else ZL_HIP(launch_attn_fwd(a, dt, S_(stream)));
+  return ZL_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,121 @@
+"""The C-ABI library loads, exports every symbol its headers declare, and its
+host-only calls (layout, workspace, config validation) behave as documented.
+No compute call is made here (no GPU)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2608_07974_amd import zl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    names = set()
+    for h in ("zl.h", "zl_inspect.h"):
+        src = open(os.path.join(ROOT, "include", h)).read()
+        src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+        names |= set(re.findall(r"\b(zl_[a-z_]+)\s*\(", src))
+    return names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = zl.load()
+    declared = _declared()
+    assert {"zl_chunk_forward", "zl_local_objective", "zl_chunk_backward", "zl_optimizer_step",
+            "zl_chunk_update"} <= declared
+    for name in declared:
+        assert hasattr(lib, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", zl.LIB_PATH], capture_output=True,
+                         text=True).stdout
+    exported = set(re.findall(r" T (zl_[a-z_]+)", out))
+    assert declared <= exported, declared - exported
+    assert set(zl.EXPORTED) == declared
+
+
+def _cfg(**kw):
+    base = dict(rope_theta=1e4, max_batch=4, max_seq=32)
+    base.update(kw)
+    return zl.make_config(zl.ZL_ARCH_LLAMA, 2, 64, 4, 4, 16, 256, 256, **base)
+
+
+def test_layout_matches_workload_specs():
+    import workload
+    for name in ("tiny", "gpt2", "8b"):
+        shp = workload.get_config(name)
+        arch = zl.ZL_ARCH_LLAMA if shp.arch == "llama" else zl.ZL_ARCH_GPT2
+        cfg = zl.make_config(arch, shp.n_layers, shp.d_model, shp.n_heads, shp.n_kv_heads,
+                             shp.head_dim, shp.d_ff, shp.vocab, rope_theta=max(shp.rope_theta, 2.0),
+                             max_batch=1, max_seq=8)
+        n, lay = zl.zl_param_layout(cfg)
+        specs = workload.param_specs(shp)
+        assert [f"L{t['layer']}.{t['name']}" for t in lay] == [k for k, _, _ in specs]
+        for t, (_, shape, _) in zip(lay, specs):
+            assert tuple(t["shape"]) == tuple(shape)
+            assert t["offset"] % 64 == 0
+        ends = [t["offset"] + t["numel"] for t in lay]
+        assert n >= max(ends) and n % 64 == 0
+        # fused projections are adjacent
+        by = {(t["layer"], t["name"]): t for t in lay}
+        if shp.arch == "llama":
+            assert by[(0, "wk")]["offset"] == by[(0, "wq")]["offset"] + by[(0, "wq")]["numel"]
+            assert by[(0, "wv")]["offset"] == by[(0, "wk")]["offset"] + by[(0, "wk")]["numel"]
+            assert by[(0, "wu")]["offset"] == by[(0, "wg")]["offset"] + by[(0, "wg")]["numel"]
+    assert zl.zl_param_layout(zl.make_config(zl.ZL_ARCH_LLAMA, 8, 4096, 32, 8, 128, 14336, 128256,
+                                             rope_theta=5e5))[0] >= 1_744_896_000
+
+
+def test_workspace_grows_with_tokens():
+    a = zl.zl_workspace_size(_cfg(max_batch=1, max_seq=16))
+    b = zl.zl_workspace_size(_cfg(max_batch=2, max_seq=16))
+    assert b > a > 0
+
+
+@pytest.mark.parametrize("bad,status", [
+    (dict(d_model=60), zl.ZL_ERR_INVALID_ARG),
+    (dict(n_kv_heads=3), zl.ZL_ERR_INVALID_ARG),
+    (dict(alpha=0.0), zl.ZL_ERR_INVALID_ARG),
+    (dict(alpha=1.5), zl.ZL_ERR_INVALID_ARG),
+    (dict(dtype=7), zl.ZL_ERR_INVALID_ARG),
+    (dict(max_seq=0), zl.ZL_ERR_INVALID_ARG),
+    (dict(head_dim=24), zl.ZL_ERR_UNSUPPORTED),
+    (dict(consis=5), zl.ZL_ERR_INVALID_ARG),
+])
+def test_config_validation(bad, status):
+    base = dict(arch=zl.ZL_ARCH_LLAMA, n_layers=2, d_model=64, n_heads=4, n_kv_heads=4,
+                head_dim=16, d_ff=256, vocab=256, rope_theta=1e4, max_batch=4, max_seq=32)
+    base.update(bad)
+    args = [base.pop(k) for k in ("arch", "n_layers", "d_model", "n_heads", "n_kv_heads",
+                                  "head_dim", "d_ff", "vocab")]
+    cfg = zl.make_config(*args, **base)
+    with pytest.raises(zl.ZlError) as ei:
+        zl.zl_workspace_size(cfg)
+    assert ei.value.status == status
+    assert zl.load().zl_last_error()
+
+
+def test_create_rejects_bad_buffers_without_gpu():
+    cfg = _cfg()
+    bufs = zl.zl_buffers(0, 0, 0, 0, 0, 0, 0, 0)
+    with pytest.raises(zl.ZlError) as ei:
+        zl.zl_chunk_create(cfg, bufs, 0, 0)
+    assert ei.value.status == zl.ZL_ERR_INVALID_ARG
+    bufs = zl.zl_buffers(4096, 0, 8192, 12288, 16384, 20480, 24576, 0)
+    with pytest.raises(zl.ZlError) as ei:
+        zl.zl_chunk_create(cfg, bufs, 0, 0)
+    assert ei.value.status == zl.ZL_ERR_WORKSPACE
+    with pytest.raises(zl.ZlError) as ei:
+        zl.zl_chunk_create(cfg, bufs, 256, 16)
+    assert ei.value.status == zl.ZL_ERR_WORKSPACE
+
+
+def test_null_handle_calls_fail_cleanly():
+    lib = zl.load()
+    assert lib.zl_chunk_forward(None, None, None, None, 1, 1, None, None) == zl.ZL_ERR_INVALID_ARG
+    assert lib.zl_local_objective(None, None, None, None) == zl.ZL_ERR_INVALID_ARG
+    assert lib.zl_chunk_backward(None, 1.0, 0, None) == zl.ZL_ERR_INVALID_ARG
+    assert lib.zl_optimizer_step(None, None) == zl.ZL_ERR_INVALID_ARG
+    assert zl.status_string(zl.ZL_ERR_STATE) == "ZL_ERR_STATE"

@@ -1,0 +1,132 @@
+"""Single-kernel parity on the GPU through the C ABI (zl_inspect.h):
+the GEMM in its three operand layouts and causal GQA attention, against
+fp64 references computed on the CPU from the same (bf16-rounded) inputs."""
+import numpy as np
+import pytest
+
+import oracle
+from oracle import ops
+from tests.gpu_cases import rel_err
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _zl():
+    from paper_2608_07974_amd import zl
+    return zl
+
+
+def _dev():
+    return torch.device("cuda")
+
+
+def _stream():
+    return torch.cuda.current_stream().cuda_stream
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("layout", ["nt", "nn", "tn"])
+@pytest.mark.parametrize("M,N,K", [(8, 8, 8), (1, 8, 8), (304, 520, 200), (129, 136, 1000),
+                                   (4096, 3848, 264)])
+def test_gemm_layouts(dtype, layout, M, N, K):
+    """C = A B^T with A(m,k), B(n,k) stored K-major or MN-major (fwd: nt,
+    dgrad: nn, wgrad: tn), ragged in every dimension."""
+    zl = _zl()
+    if dtype == "bf16" and layout == "tn" and M % 8:
+        pytest.skip("an M-contiguous bf16 operand needs M % 8 == 0 (16-byte rows)")
+    if dtype == "f32" and M * N * K > 1e9:
+        pytest.skip("fp32 SIMT path is sized for small problems")
+    rng = np.random.default_rng(M + N + K)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    a_k = layout in ("nt", "nn")
+    b_k = layout == "nt"
+    A = rng.standard_normal((M, K) if a_k else (K, M)).astype(np.float32)
+    B = rng.standard_normal((N, K) if b_k else (K, N)).astype(np.float32)
+    At = torch.tensor(A, device=_dev()).to(tdt)
+    Bt = torch.tensor(B, device=_dev()).to(tdt)
+    C = torch.full((M, N), float("nan"), dtype=torch.float32, device=_dev())
+    torch.cuda.synchronize()
+    zl.zl_kernel_gemm(M, N, K, At.data_ptr(), At.shape[1], a_k, Bt.data_ptr(), Bt.shape[1], b_k,
+                      C.data_ptr(), N, zl.ZL_BF16 if dtype == "bf16" else zl.ZL_F32, _stream())
+    torch.cuda.synchronize()
+    a64 = At.double().cpu().numpy()
+    b64 = Bt.double().cpu().numpy()
+    ref = (a64 if a_k else a64.T) @ (b64 if b_k else b64.T).T
+    got = C.cpu().double().numpy()
+    assert np.all(np.isfinite(got))
+    bound = 1e-5 * np.sqrt(K) * (np.abs(a64).max() * np.abs(b64).max()) + 1e-6
+    assert np.max(np.abs(got - ref)) < bound * 8
+    assert rel_err(got, ref) < 2e-6
+
+
+def _attn_inputs(B, S, Hq, Hkv, hd, lens, seed):
+    rng = np.random.default_rng(seed)
+    q = rng.standard_normal((B, S, Hq, hd)).astype(np.float32)
+    k = rng.standard_normal((B, S, Hkv, hd)).astype(np.float32)
+    v = rng.standard_normal((B, S, Hkv, hd)).astype(np.float32)
+    do = rng.standard_normal((B, S, Hq, hd)).astype(np.float32)
+    return q, k, v, do, np.array(lens, np.int32)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("B,S,Hq,Hkv,hd,lens", [
+    (2, 37, 4, 2, 16, [37, 20]),
+    (1, 130, 8, 2, 64, [130]),
+    (2, 200, 4, 4, 128, [200, 77]),
+    (1, 5, 2, 1, 64, [0]),
+    (3, 64, 2, 2, 32, [1, 64, 63]),
+])
+def test_attention_fwd_bwd(dtype, B, S, Hq, Hkv, hd, lens):
+    zl = _zl()
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    q, k, v, do, lens = _attn_inputs(B, S, Hq, Hkv, hd, lens, S + hd)
+    ld = (Hq + 2 * Hkv) * hd
+    qkv = np.concatenate([q.reshape(B * S, -1), k.reshape(B * S, -1), v.reshape(B * S, -1)], 1)
+    QKV = torch.tensor(qkv, device=_dev()).to(tdt).contiguous()
+    DO = torch.tensor(do.reshape(B * S, -1), device=_dev()).to(tdt)
+    O = torch.zeros(B * S, Hq * hd, device=_dev(), dtype=tdt)
+    LSE = torch.zeros(B, Hq, S, dtype=torch.float32, device=_dev())
+    DQKV = torch.zeros_like(QKV)
+    DEL = torch.zeros(B, Hq, S, dtype=torch.float32, device=_dev())
+    SL = torch.tensor(lens, device=_dev())
+    base = QKV.data_ptr()
+    esz = QKV.element_size()
+    torch.cuda.synchronize()
+    args = (B, S, Hq, Hkv, hd, base, base + Hq * hd * esz, base + (Hq + Hkv) * hd * esz, ld,
+            SL.data_ptr(), O.data_ptr(), LSE.data_ptr())
+    dt = zl.ZL_BF16 if dtype == "bf16" else zl.ZL_F32
+    zl.zl_kernel_attention(*args, 0, 0, 0, 0, 0, dt, 0, _stream())
+    dbase = DQKV.data_ptr()
+    zl.zl_kernel_attention(*args, DO.data_ptr(), dbase, dbase + Hq * hd * esz,
+                           dbase + (Hq + Hkv) * hd * esz, DEL.data_ptr(), dt, 1, _stream())
+    torch.cuda.synchronize()
+    r = QKV.double().cpu().numpy()
+    q64 = r[:, : Hq * hd].reshape(B, S, Hq, hd)
+    k64 = r[:, Hq * hd: (Hq + Hkv) * hd].reshape(B, S, Hkv, hd)
+    v64 = r[:, (Hq + Hkv) * hd:].reshape(B, S, Hkv, hd)
+    do64 = DO.double().cpu().numpy().reshape(B, S, Hq, hd)
+    o_ref, cache = ops.attention_fwd(q64, k64, v64, lens)
+    dq_ref, dk_ref, dv_ref = ops.attention_bwd(do64, cache)
+    tol = 1e-5 if dtype == "f32" else 1.2e-2
+    o = O.double().cpu().numpy().reshape(B, S, Hq, hd)
+    assert rel_err(o, o_ref) < tol
+    d = DQKV.double().cpu().numpy()
+    assert rel_err(d[:, : Hq * hd].reshape(dq_ref.shape), dq_ref) < tol
+    assert rel_err(d[:, Hq * hd: (Hq + Hkv) * hd].reshape(dk_ref.shape), dk_ref) < tol
+    assert rel_err(d[:, (Hq + Hkv) * hd:].reshape(dv_ref.shape), dv_ref) < tol
+    # lse of rows with at least one visible key
+    lse = LSE.cpu().double().numpy()
+    scale = 1.0 / np.sqrt(hd)
+    for b in range(B):
+        for h in range(Hq):
+            g = h // (Hq // Hkv)
+            s = (q64[b, :, h] @ k64[b, :, g].T) * scale
+            allowed = ops.attention_mask(B, S, lens)[b]
+            for i in range(S):
+                if allowed[i].any():
+                    ref = np.log(np.sum(np.exp(s[i][allowed[i]] - s[i][allowed[i]].max()))) + s[i][allowed[i]].max()
+                    assert abs(lse[b, h, i] - ref) < 1e-4 * max(1, abs(ref))
+                else:
+                    assert lse[b, h, i] == -np.inf

@@ -1,0 +1,204 @@
+"""End-to-end parity of the chunk-local update: libzl through the C ABI vs
+the fp64 oracle on the same seeded inputs.
+
+Gates (rel-err = ||x - x_ref|| / ||x_ref|| per tensor): fp32 1e-4, bf16 2e-2,
+on the loss, h_out, dL/dh_out, every gradient tensor, the updated master
+parameters and the update deltas (SGD: -lr g; AdamW in fp32 after 1 and 3
+steps).  bf16 AdamW deltas are not gated: Adam's first step is about
+-lr sign(g), so a gradient element below bf16 noise may flip its delta."""
+import numpy as np
+import pytest
+
+import oracle
+import workload
+from oracle.chunk import chunk_forward_ref, init_opt_state
+from tests.gpu_cases import device_chunk, make_inputs, oracle_cfg, rel_err, to_dev
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def _run_device(shp, params, batch, steps=1, **kw):
+    ch = device_chunk(shp, params, batch, **kw)
+    d = to_dev(batch, shp.dtype)
+    out = dict(grads=[], masters=[ch.tensors(ch.master)], losses=[])
+    for _ in range(steps):
+        h_out = ch.forward(d["h_in"], d["seq_lens"], d["pos_ids"])
+        ch.objective(d["labels"])
+        if not out["grads"]:
+            out["h_out"] = h_out.double().cpu().numpy()
+            out["dh_out"] = ch.inspect("dh_out")
+        ch.backward(1.0, 0)
+        torch.cuda.synchronize()
+        out["losses"].append(float(ch.loss.item()))
+        out["grads"].append(ch.tensors(ch.grad))
+        ch.step()
+        out["masters"].append(ch.tensors(ch.master))
+    out["h_in_after"] = d["h_in"].double().cpu().numpy()
+    ch.close()
+    return out
+
+
+def _run_oracle(shp, params, batch, steps=1, **kw):
+    cfg = oracle_cfg(shp, **kw)
+    mb = dict(h_in=batch["h_in"], labels=batch["labels"], seq_lens=batch["seq_lens"],
+              pos_ids=batch["pos_ids"])
+    P, st = {k: np.asarray(v, np.float64) for k, v in params.items()}, init_opt_state()
+    res = dict(grads=[], masters=[P], losses=[])
+    for _ in range(steps):
+        r = oracle.chunk_update_ref(cfg, P, st, [mb], batch["head_w"], batch["head_norm_w"],
+                                    batch["head_norm_b"], grad_scale=1.0)
+        if not res["grads"]:
+            res["h_out"] = r["runs"][0]["h_out"]
+            res["dh_out"] = r["runs"][0]["dh_out"]
+        res["losses"].append(r["losses"][0])
+        res["grads"].append(r["grads"])
+        P, st = r["params"], r["state"]
+        res["masters"].append(P)
+    return res
+
+
+def _compare(shp, dev, ref, tol, lr, optimizer, gate_adam_delta=True):
+    report = {}
+    for s, (a, b) in enumerate(zip(dev["losses"], ref["losses"])):
+        report[f"loss{s}"] = abs(a - b) / max(abs(b), 1e-30)
+    report["h_out"] = rel_err(dev["h_out"].reshape(-1), ref["h_out"].reshape(-1))
+    report["dh_out"] = rel_err(dev["dh_out"].reshape(-1), ref["dh_out"].reshape(-1))
+    for s in range(len(dev["grads"])):
+        for k in ref["grads"][s]:
+            report[f"g{s}:{k}"] = rel_err(dev["grads"][s][k], ref["grads"][s][k])
+    for s in range(1, len(dev["masters"])):
+        for k in ref["masters"][s]:
+            report[f"p{s}:{k}"] = rel_err(dev["masters"][s][k], ref["masters"][s][k])
+            dd = dev["masters"][s][k] - dev["masters"][s - 1][k]
+            rd = ref["masters"][s][k] - ref["masters"][s - 1][k]
+            if optimizer == "sgd":
+                report[f"d{s}:{k}"] = rel_err(dd, rd)
+            elif gate_adam_delta:
+                # g -> g / (|g| + eps) is ill-conditioned where g is at rounding
+                # noise (e.g. the key bias, whose exact gradient is 0 because a
+                # shift of every score of a row leaves the softmax unchanged):
+                # gate the elements whose first-step gradient is resolvable.
+                g0 = np.abs(ref["grads"][0][k])
+                keep = g0 > 1e-4 * np.sqrt(np.mean(g0 ** 2)) + 1e-12
+                if keep.any():
+                    # the device keeps master in fp32: its delta is resolved only
+                    # to one ulp of the new value, so the gate is
+                    # ||dd - rd|| < tol ||rd|| + ||ulp(theta_new)||
+                    ulp = np.spacing(np.abs(ref["masters"][s][k]).astype(np.float32)).astype(np.float64)
+                    err = np.linalg.norm((dd - rd)[keep])
+                    report[f"d{s}:{k}"] = err / (np.linalg.norm(rd[keep]) + np.linalg.norm(ulp[keep]) / tol)
+    worst = max(report, key=report.get)
+    assert report[worst] < tol, (worst, report[worst], sorted(report.items(), key=lambda t: -t[1])[:6])
+    return report
+
+
+def _case(shp, steps=1, seed=0, stress=True, seq_lens=None, drop=0, alpha=0.5, consis="reverse",
+          optimizer="adamw", lr=1e-4, wd=0.01, h_in=None, gate_adam_delta=None):
+    params, batch = make_inputs(shp, seed=seed, stress=stress, seq_lens=seq_lens, drop=drop)
+    if h_in is not None:
+        batch["h_in"] = h_in
+    kw = dict(alpha=alpha, consis=consis, optimizer=optimizer, lr=lr, wd=wd)
+    dev = _run_device(shp, params, batch, steps=steps, **kw)
+    ref = _run_oracle(shp, params, batch, steps=steps, **kw)
+    np.testing.assert_array_equal(dev["h_in_after"].astype(np.float32), batch["h_in"])
+    gate = (shp.dtype == "f32") if gate_adam_delta is None else gate_adam_delta
+    return _compare(shp, dev, ref, TOL[shp.dtype], lr, optimizer, gate)
+
+
+# ----------------------------------------------------------------- fp32 tiny
+TINY = workload.get_config("tiny")
+
+
+@pytest.mark.parametrize("alpha,consis", [(0.5, "reverse"), (1.0, "reverse"), (0.3, "forward")])
+def test_tiny_fp32_chunk1(alpha, consis):
+    _case(TINY, alpha=alpha, consis=consis)
+
+
+def test_tiny_fp32_chunk2_input_from_chunk1():
+    """Chunk k = 2 of 2: its input is chunk 1's output (oracle forward)."""
+    p1, b1 = make_inputs(TINY, seed=0)
+    cfg = oracle_cfg(TINY)
+    h1, _ = chunk_forward_ref(cfg, p1, b1["h_in"], b1["seq_lens"], b1["pos_ids"])
+    _case(TINY, seed=1, h_in=h1.astype(np.float32))
+
+
+def test_tiny_fp32_padding_and_ignored_labels():
+    _case(TINY, seq_lens=[32, 17, 1, 9], drop=20, alpha=0.6)
+
+
+def test_tiny_fp32_three_adamw_steps():
+    _case(TINY, steps=3, lr=1e-3)
+
+
+def test_tiny_fp32_sgd():
+    _case(TINY, optimizer="sgd", lr=0.05, alpha=0.7, consis="forward")
+
+
+def test_tiny_gqa_fp32():
+    shp = TINY.with_(n_kv_heads=2, name="tiny-gqa")
+    _case(shp, alpha=0.4)
+
+
+def test_tiny_gpt2_fp32():
+    shp = workload.configs.ChunkShape("tiny-gpt2", "gpt2", 2, 64, 4, 4, 16, 256, 97, 4, 24, "f32",
+                                      0.0, 2)
+    _case(shp, alpha=0.5, seq_lens=[24, 20, 3, 24])
+
+
+# ---------------------------------------------------------- window (m = 2)
+def test_window_accumulation_fp32():
+    """Two micro-batches, grad_scale 1/2, accumulate -> one step (S3)."""
+    shp = TINY
+    params, b1 = make_inputs(shp, seed=0)
+    _, b2 = make_inputs(shp, seed=5)
+    b2["head_w"], b2["head_norm_w"] = b1["head_w"], b1["head_norm_w"]
+    ch = device_chunk(shp, params, b1)
+    for i, b in enumerate((b1, b2)):
+        d = to_dev(b, "f32")
+        ch.forward(d["h_in"], d["seq_lens"], d["pos_ids"])
+        ch.objective(d["labels"])
+        ch.backward(0.5, 1)
+    torch.cuda.synchronize()
+    g = ch.tensors(ch.grad)
+    ch.step()
+    p = ch.tensors(ch.master)
+    cfg = oracle_cfg(shp)
+    mbs = [dict(h_in=b["h_in"], labels=b["labels"], seq_lens=b["seq_lens"], pos_ids=b["pos_ids"])
+           for b in (b1, b2)]
+    r = oracle.chunk_update_ref(cfg, params, init_opt_state(), mbs, b1["head_w"], b1["head_norm_w"])
+    for k in params:
+        assert rel_err(g[k], r["grads"][k]) < 1e-4, k
+        assert rel_err(p[k], r["params"][k]) < 1e-4, k
+    ch.close()
+
+
+# --------------------------------------------------------------- bf16 shapes
+GPT2 = workload.get_config("gpt2")
+
+
+def test_gpt2_bf16_reduced_tokens():
+    _case(GPT2.with_(batch=2, seq=128), seq_lens=[128, 90], drop=10)
+
+
+def test_gpt2_bf16_sgd_delta():
+    _case(GPT2.with_(batch=2, seq=64), optimizer="sgd", lr=1e-2, alpha=0.7, consis="forward")
+
+
+def test_gpt2_bf16_full_shape():
+    _case(GPT2)
+
+
+def test_llama1b_bf16_one_layer_slice():
+    _case(workload.get_config("1b").with_(n_layers=1, batch=1, seq=512))
+
+
+def test_llama8b_bf16_one_layer_slice():
+    _case(workload.get_config("8b").with_(n_layers=1, batch=1, seq=256), alpha=0.5)
+
+
+def test_llama8b_bf16_two_layers_alpha1_sgd():
+    _case(workload.get_config("8b").with_(n_layers=2, batch=1, seq=128), alpha=1.0,
+          optimizer="sgd", lr=1e-3)

@@ -12,11 +12,8 @@ from oracle import ops
 from oracle.objective import loss_and_dlogits
 from tests.oracle_cases import rel_err, tiny_case
 
-torch.set_default_dtype(torch.float64)
-
-
 def T(a):
-    return torch.tensor(np.asarray(a, np.float64))
+    return torch.tensor(np.asarray(a, np.float64), dtype=torch.float64)
 
 
 def test_norms_and_activations():
@@ -78,7 +75,7 @@ def _torch_chunk_loss(c, params):
     Hq, Hkv, hd = cfg.n_heads, cfg.n_kv_heads, cfg.head_dim
     allowed = torch.tensor(ops.attention_mask(B, S, c["seq_lens"]))[:, None]
     pos = T(c["pos_ids"])
-    inv = cfg.rope_theta ** (-(2.0 * torch.arange(hd // 2)) / hd)
+    inv = cfg.rope_theta ** (-(2.0 * torch.arange(hd // 2, dtype=torch.float64)) / hd)
     ang = pos[..., None] * inv
     cos, sin = torch.cos(ang)[:, :, None], torch.sin(ang)[:, :, None]
 

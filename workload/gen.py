@@ -66,14 +66,15 @@ def init_params(specs, seed=0, std=0.02, perturb=False, stress=False):
 
     perturb=True draws norm weights 1 + N(0, 0.1) and biases N(0, 0.02) so
     every term of the update is exercised; stress=True widens the output
-    projections (wo, wd, wproj) to N(0, 0.2).
+    projections (wo, wd, wproj) to N(0, 0.2 * sqrt(64 / fan_in)), i.e. 0.2 at
+    fan-in 64, so their contribution keeps the same scale at every width.
     """
     rng = np.random.default_rng(seed)
     out = {}
     for key, shape, kind in specs:
         name = key.split(".", 1)[1]
         if kind == "weight":
-            s = 0.2 if (stress and name in ("wo", "wd", "wproj")) else std
+            s = 0.2 * np.sqrt(64.0 / shape[1]) if (stress and name in ("wo", "wd", "wproj")) else std
             out[key] = (rng.standard_normal(shape) * s).astype(np.float32)
         elif kind == "norm_w":
             out[key] = (1.0 + (rng.standard_normal(shape) * 0.1 if perturb else 0.0)) * np.ones(shape, np.float32)
@@ -106,7 +107,8 @@ def make_batch(cfg, seed_tokens=1, seed_embed=2, seed_head=3, stress=False,
         pos_table = (rng_e.standard_normal((S, cfg.d_model)) * 0.02).astype(np.float32)
     h_in = embed_tokens(tok, table, pos_table).astype(np.float32)
     rng_h = np.random.default_rng(seed_head)
-    head_std = 0.2 if stress else 0.02
+    # stress: head logits with std about 1.6 at any width (0.2 at d = 64)
+    head_std = 0.2 * np.sqrt(64.0 / cfg.d_model) if stress else 0.02
     head_w = (rng_h.standard_normal((cfg.vocab, cfg.d_model)) * head_std).astype(np.float32)
     if perturb_head:
         hn_w = (1.0 + 0.1 * rng_h.standard_normal(cfg.d_model)).astype(np.float32)
