@@ -136,10 +136,12 @@ def main():
     h_out = torch.empty_like(h_in)
     torch.cuda.synchronize()
 
-    for _ in range(args.warmup):
+    loss_first = None
+    for i in range(args.warmup):
         ch.update(h_in, labels, h_out=h_out)
+        if i == 0:
+            loss_first = float(ch.loss.item())   # loss of the initial weights
     torch.cuda.synchronize()
-    loss_warm = float(ch.loss.item())
 
     stream = torch.cuda.current_stream()
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
@@ -209,7 +211,7 @@ def main():
         "algorithmic_tflop_per_step": round(flops / 1e12, 2),
         "flop_split": {k: round(v / flops, 4) for k, v in parts.items()},
         "ms_per_step_min": round(min(step_ms), 3),
-        "loss_first_warmup_to_last": [round(loss_warm, 4), round(loss, 4)],
+        "loss_initial_and_last": [None if loss_first is None else round(loss_first, 4), round(loss, 4)],
         "roofline": roof,
         "kernels": kernels[:16],
         "cpu_baseline": cpu,

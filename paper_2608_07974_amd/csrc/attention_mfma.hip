@@ -3,132 +3,117 @@
 // right padding by seq_len, scores q.k / sqrt(hd), fp32 softmax statistics.
 //
 // MFMA 16x16x32 bf16.  Lane l of a wave: c = l % 16 (output column), g = l / 16.
-//  - Forward: each wave owns 16 queries.  S^T = K Q^T puts the scores of one
-//    query in one lane column (keys 16*blk + 4g + r), so the online softmax
-//    statistics live per lane and P feeds O^T += V^T P^T straight from
-//    registers: the MFMA only needs A and B to agree on which 8 keys each lane
-//    group carries, {32kk + 4g + r} and {32kk + 16 + 4g + r}.  V is staged in
-//    LDS transposed ([dim][key]).
-//  - dK/dV: one workgroup per (key block of 64, kv-head); it walks every
-//    q-head of its group and every later query tile, so the GQA sum needs no
-//    cross-workgroup reduction.  S = Q K^T keeps one key per lane column.
-//  - dQ: one workgroup per (query block of 64, q-head), as the forward.
-// LDS rows are XOR-swizzled in 16-byte chunks against bank conflicts.
+// A and B operands only have to agree on which 8 reduction indices each lane
+// group carries; here that set is {32kk + 4g + r} and {32kk + 16 + 4g + r},
+// r < 4, which is exactly how the C layout of a 16-row MFMA block hands out
+// rows (4g + r) -- so softmax probabilities feed the next MFMA straight from
+// registers.
+//  - Forward: each wave owns 2 x 16 queries; S^T = K Q^T puts one query per
+//    lane column, so the online-softmax statistics live per lane, and
+//    O^T += V^T P^T reads V^T with the LDS transpose read.
+//  - dK/dV: one workgroup per (128 keys, kv-head), walking every q-head of
+//    its group and every later query tile (no cross-workgroup reduction).
+//  - dQ: one workgroup per (128 queries, q-head).
+// Tiles of 64 rows are staged through registers into double-buffered LDS
+// (16-byte chunks XOR-swizzled by row) so global loads overlap the MFMAs.
+// Operands needed transposed are read from the same row-major tiles with
+// ds_read_b64_tr_b16: within each 16-lane group, lane r addresses row
+// q0 + r/4, columns d0 + 4 (r % 4) .. +3, and lane i receives column d0 + i
+// of rows q0 .. q0 + 3.
 #include "common.h"
 
 namespace zl {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef short s16x8_t __attribute__((ext_vector_type(8)));
 
 namespace {
 
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
-constexpr int BT = 64;  // rows per tile (queries or keys)
+constexpr int BT = 64;   // rows of a staged tile
+constexpr int BW = 128;  // rows (queries or keys) owned by a workgroup: 4 waves x 32
+constexpr int NTH = 256;
 
 __device__ inline f32x4_t mfma16(bf16x8_t a, bf16x8_t b, f32x4_t c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
 template <int HD>
-__device__ inline int swz_nat(int row) {
+__device__ inline int swz(int row) {
   return HD == 128 ? (row & 15) : ((row >> 1) & 7);
 }
-__device__ inline int swz_tr(int row) { return (row >> 1) & 7; }
 
 __device__ inline bf16x8_t zero8() {
-  bf16x8_t z;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) z[i] = (__bf16)0.f;
-  return z;
+  return __builtin_bit_cast(bf16x8_t, make_uint4(0, 0, 0, 0));
 }
 
-__device__ inline bf16x8_t as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8_t, u); }
+__device__ inline __bf16 to_bf16(float f) { return __builtin_bit_cast(__bf16, f32_to_bf16(f)); }
 
-__device__ inline __bf16 to_bf16(float f) {
-  return __builtin_bit_cast(__bf16, f32_to_bf16(f));
-}
-
-// Transpose an 8x8 bf16 block held as 8 rows (uint4 = 8 bf16 each).
-__device__ inline void tr8x8(const uint4 (&in)[8], uint4 (&out)[8]) {
-  const uint32_t* iw = reinterpret_cast<const uint32_t*>(in);
-  uint32_t* ow = reinterpret_cast<uint32_t*>(out);
-#pragma unroll
-  for (int j = 0; j < 8; ++j)
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint32_t lo = iw[(2 * q) * 4 + j / 2];
-      const uint32_t hi = iw[(2 * q + 1) * 4 + j / 2];
-      ow[j * 4 + q] = __builtin_amdgcn_perm(hi, lo, (j & 1) ? 0x07060302u : 0x05040100u);
-    }
-}
-
-// Natural tile: lds[i][0..HD) = G[rowbase + row0 + i][col0 ..], rows >= nvalid zero.
+// A 64 x HD tile staged global -> registers -> LDS (row-major, swizzled).
 template <int HD>
-__device__ inline void load_nat(bf16_t* lds, const bf16_t* G, int64_t ld, int64_t rowbase,
-                                int row0, int nvalid, int64_t col0) {
-  constexpr int CH = HD / 8;
-  for (int c = threadIdx.x; c < BT * CH; c += 256) {
-    const int i = c / CH, ch = c % CH;
-    const int t = row0 + i;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (t < nvalid) v = *reinterpret_cast<const uint4*>(G + (rowbase + t) * ld + col0 + ch * 8);
-    *reinterpret_cast<uint4*>(lds + i * HD + ((ch ^ swz_nat<HD>(i)) * 8)) = v;
-  }
-}
-
-// Transposed tile: lds[d][i] = G[rowbase + row0 + i][col0 + d], 64 columns i.
-template <int HD>
-__device__ inline void load_tr(bf16_t* lds, const bf16_t* G, int64_t ld, int64_t rowbase,
-                               int row0, int nvalid, int64_t col0) {
-  for (int bi = threadIdx.x; bi < 8 * (HD / 8); bi += 256) {
-    const int kb = bi & 7, db = bi >> 3;
-    uint4 in[8], out[8];
+struct TileStage {
+  static constexpr int CH = HD / 8;                 // 16-byte chunks per row
+  static constexpr int PER = BT * CH / NTH;         // chunks per thread
+  uint4 r[PER];
+  __device__ inline void load(const bf16_t* G, int64_t ld, int64_t rowbase, int row0,
+                              int nvalid, int64_t col0) {
 #pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      const int r = row0 + kb * 8 + t;
-      in[t] = r < nvalid ? *reinterpret_cast<const uint4*>(G + (rowbase + r) * ld + col0 + db * 8)
-                         : make_uint4(0, 0, 0, 0);
-    }
-    tr8x8(in, out);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int d = db * 8 + j;
-      *reinterpret_cast<uint4*>(lds + d * BT + ((kb ^ swz_tr(d)) * 8)) = out[j];
+    for (int i = 0; i < PER; ++i) {
+      const int c = threadIdx.x + i * NTH;
+      const int row = c / CH, ch = c % CH;
+      const int t = row0 + row;
+      r[i] = t < nvalid ? *reinterpret_cast<const uint4*>(G + (rowbase + t) * ld + col0 + ch * 8)
+                        : make_uint4(0, 0, 0, 0);
     }
   }
-}
+  __device__ inline void store(bf16_t* lds) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = threadIdx.x + i * NTH;
+      const int row = c / CH, ch = c % CH;
+      *reinterpret_cast<uint4*>(lds + row * HD + ((ch ^ swz<HD>(row)) * 8)) = r[i];
+    }
+  }
+};
 
-// 16-byte fragment of a natural tile: row i, 16-byte chunk ch.
+// 8 consecutive bf16 of row `row`, 16-byte chunk `ch`.
 template <int HD>
-__device__ inline bf16x8_t frag_nat(const bf16_t* lds, int i, int ch) {
-  return *reinterpret_cast<const bf16x8_t*>(lds + i * HD + ((ch ^ swz_nat<HD>(i)) * 8));
+__device__ inline bf16x8_t frag_row(const bf16_t* lds, int row, int ch) {
+  return *reinterpret_cast<const bf16x8_t*>(lds + row * HD + ((ch ^ swz<HD>(row)) * 8));
 }
 
-// Fragment of a transposed tile for lane group g and key/query step kk:
-// columns {32kk + 4g .. +3} then {32kk + 16 + 4g .. +3} of row d.
-__device__ inline bf16x8_t frag_tr(const bf16_t* lds, int d, int kk, int g) {
-  const int k1 = 32 * kk + 4 * g, k2 = k1 + 16;
-  const bf16_t* row = lds + d * BT;
-  const uint2 a = *reinterpret_cast<const uint2*>(row + (((k1 >> 3) ^ swz_tr(d)) * 8) + ((k1 >> 2) & 1) * 4);
-  const uint2 b = *reinterpret_cast<const uint2*>(row + (((k2 >> 3) ^ swz_tr(d)) * 8) + ((k2 >> 2) & 1) * 4);
-  return as_bf16x8(make_uint4(a.x, a.y, b.x, b.y));
+// Column d0 + c of rows {rb + 4g + k} then {rb + 16 + 4g + k}, k < 4 (the k-set
+// of lane group g), through the LDS transpose read.
+template <int HD>
+__device__ inline bf16x8_t frag_col(const bf16_t* lds, int rb, int g, int d0, int c) {
+  const int r1 = rb + 4 * g + (c >> 2), r2 = r1 + 16;
+  const int col = d0 + 4 * (c & 3);
+  const bf16_t* p1 = lds + r1 * HD + (((col >> 3) ^ swz<HD>(r1)) << 3) + (col & 7);
+  const bf16_t* p2 = lds + r2 * HD + (((col >> 3) ^ swz<HD>(r2)) << 3) + (col & 7);
+  const s16x4_t x = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) s16x4_t*)(p1));
+  const s16x4_t y = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) s16x4_t*)(p2));
+  const s16x8_t xy = __builtin_shufflevector(x, y, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8_t, xy);
 }
 
 // Inverse (transposed) rotate-half RoPE of one row held as HD/16 register
-// blocks x[db][r] (dims 16*db + c16): pairs (j, j + HD/2) sit HD/32 blocks
+// blocks x[db][r] (dims 16*db + c): pairs (j, j + HD/2) sit HD/32 blocks
 // apart in the same lane.  du_j = du'_j c + du'_{j+h} s,
 // du_{j+h} = du'_{j+h} c - du'_j s.
 template <int HD>
 __device__ inline void rope_back(f32x4_t (&x)[HD / 16], int r, const int32_t* pos, int64_t row,
-                                 const float2* table, int max_pos, int c16) {
+                                 const float2* table, int max_pos, int c) {
   int p = pos[row];
   p = p < 0 ? 0 : (p >= max_pos ? max_pos - 1 : p);
   constexpr int HB = HD / 32;
 #pragma unroll
   for (int db = 0; db < HB; ++db) {
-    const float2 cs = table[(int64_t)p * (HD / 2) + db * 16 + c16];
+    const float2 cs = table[(int64_t)p * (HD / 2) + db * 16 + c];
     const float a = x[db][r], b = x[db + HB][r];
     x[db][r] = a * cs.x + b * cs.y;
     x[db + HB][r] = b * cs.x - a * cs.y;
@@ -139,96 +124,133 @@ __device__ inline void rope_back(f32x4_t (&x)[HD / 16], int r, const int32_t* po
 
 // ------------------------------------------------------------------ forward
 template <int HD>
-__global__ void __launch_bounds__(256) attn_fwd_mfma(AttnDesc a) {
+__global__ void __launch_bounds__(NTH) attn_fwd_mfma(AttnDesc a) {
   extern __shared__ __align__(16) unsigned char smem[];
-  bf16_t* Ks = reinterpret_cast<bf16_t*>(smem);
-  bf16_t* Vt = Ks + BT * HD;
-  const int qb = gridDim.x - 1 - blockIdx.x;  // longest causal rows first
+  bf16_t* Ks = reinterpret_cast<bf16_t*>(smem);     // [2][BT * HD]
+  bf16_t* Vs = Ks + 2 * BT * HD;                    // [2][BT * HD]
+  const int qb = gridDim.x - 1 - blockIdx.x;        // longest causal rows first
   const int h = blockIdx.y, b = blockIdx.z;
   const int kvh = h / (a.Hq / a.Hkv);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int c16 = lane & 15, g = lane >> 4;
+  const int c = lane & 15, g = lane >> 4;
   const int L = a.seq_lens[b];
-  const int q0 = qb * BT;
-  const int qi = q0 + wave * 16 + c16;
+  const int q0 = qb * BW;
   const int64_t rowb = (int64_t)b * a.S;
   const bf16_t* Q = reinterpret_cast<const bf16_t*>(a.q);
   const bf16_t* K = reinterpret_cast<const bf16_t*>(a.k);
   const bf16_t* V = reinterpret_cast<const bf16_t*>(a.v);
 
-  bf16x8_t qf[HD / 32];
+  int qi[2];
+  bf16x8_t qf[2][HD / 32];
+  f32x4_t o[2][HD / 16];
+  float m[2], lsum[2];
 #pragma unroll
-  for (int kk = 0; kk < HD / 32; ++kk)
-    qf[kk] = qi < a.S ? *reinterpret_cast<const bf16x8_t*>(Q + (rowb + qi) * a.ldq +
-                                                           (int64_t)h * HD + 8 * g + 32 * kk)
-                      : zero8();
-  f32x4_t o[HD / 16];
+  for (int j = 0; j < 2; ++j) {
+    qi[j] = q0 + wave * 32 + j * 16 + c;
 #pragma unroll
-  for (int i = 0; i < HD / 16; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  float m = -INFINITY, lsum = 0.f;
+    for (int kk = 0; kk < HD / 32; ++kk)
+      qf[j][kk] = qi[j] < a.S ? *reinterpret_cast<const bf16x8_t*>(Q + (rowb + qi[j]) * a.ldq +
+                                                                   (int64_t)h * HD + 8 * g + 32 * kk)
+                              : zero8();
+#pragma unroll
+    for (int i = 0; i < HD / 16; ++i) o[j][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    m[j] = -INFINITY;
+    lsum[j] = 0.f;
+  }
   const float cs = a.scale * LOG2E;
-  const int kend = min(min(q0 + BT, a.S), L);
+  const int kend = min(min(q0 + BW, a.S), L);
+  const int nt = (kend + BT - 1) / BT;
 
-  for (int k0 = 0; k0 < kend; k0 += BT) {
-    __syncthreads();
-    load_nat<HD>(Ks, K, a.ldk, rowb, k0, kend, (int64_t)kvh * HD);
-    load_tr<HD>(Vt, V, a.ldv, rowb, k0, kend, (int64_t)kvh * HD);
-    __syncthreads();
-    f32x4_t s[4];
+  TileStage<HD> sk, sv;
+  if (nt > 0) {
+    sk.load(K, a.ldk, rowb, 0, kend, (int64_t)kvh * HD);
+    sv.load(V, a.ldv, rowb, 0, kend, (int64_t)kvh * HD);
+    sk.store(Ks);
+    sv.store(Vs);
+  }
+  __syncthreads();
+  for (int t = 0; t < nt; ++t) {
+    const int k0 = t * BT;
+    const bf16_t* kt = Ks + (t & 1) * BT * HD;
+    const bf16_t* vt = Vs + (t & 1) * BT * HD;
+    if (t + 1 < nt) {
+      sk.load(K, a.ldk, rowb, k0 + BT, kend, (int64_t)kvh * HD);
+      sv.load(V, a.ldv, rowb, k0 + BT, kend, (int64_t)kvh * HD);
+    }
+    f32x4_t s[2][4];
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) {
-      s[blk] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      s[0][blk] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      s[1][blk] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int kk = 0; kk < HD / 32; ++kk)
-        s[blk] = mfma16(frag_nat<HD>(Ks, blk * 16 + c16, g + 4 * kk), qf[kk], s[blk]);
-    }
-    float tmax = -INFINITY;
-#pragma unroll
-    for (int blk = 0; blk < 4; ++blk)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int key = k0 + blk * 16 + 4 * g + r;
-        const bool ok = key < kend && key <= qi;
-        const float v = ok ? s[blk][r] * cs : -INFINITY;
-        s[blk][r] = v;
-        tmax = fmaxf(tmax, v);
+      for (int kk = 0; kk < HD / 32; ++kk) {
+        const bf16x8_t kf = frag_row<HD>(kt, blk * 16 + c, g + 4 * kk);
+        s[0][blk] = mfma16(kf, qf[0][kk], s[0][blk]);
+        s[1][blk] = mfma16(kf, qf[1][kk], s[1][blk]);
       }
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    const float mnew = fmaxf(m, tmax);
-    const float alpha = mnew == -INFINITY ? 1.f : exp2f(m - mnew);
-    float psum = 0.f;
-    bf16x8_t pf[2];
-#pragma unroll
-    for (int blk = 0; blk < 4; ++blk)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float p = s[blk][r] == -INFINITY ? 0.f : exp2f(s[blk][r] - mnew);
-        psum += p;
-        pf[blk >> 1][(blk & 1) * 4 + r] = to_bf16(p);
-      }
-    lsum = lsum * alpha + psum;
-    m = mnew;
-#pragma unroll
-    for (int db = 0; db < HD / 16; ++db) {
-      o[db] *= alpha;
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) o[db] = mfma16(frag_tr(Vt, db * 16 + c16, kk, g), pf[kk], o[db]);
     }
+    bf16x8_t pf[2][2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      float tmax = -INFINITY;
+#pragma unroll
+      for (int blk = 0; blk < 4; ++blk)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = k0 + blk * 16 + 4 * g + r;
+          const float v = (key < kend && key <= qi[j]) ? s[j][blk][r] * cs : -INFINITY;
+          s[j][blk][r] = v;
+          tmax = fmaxf(tmax, v);
+        }
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+      const float mnew = fmaxf(m[j], tmax);
+      const float alpha = mnew == -INFINITY ? 1.f : exp2f(m[j] - mnew);
+      float psum = 0.f;
+#pragma unroll
+      for (int blk = 0; blk < 4; ++blk)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float p = s[j][blk][r] == -INFINITY ? 0.f : exp2f(s[j][blk][r] - mnew);
+          psum += p;
+          pf[j][blk >> 1][(blk & 1) * 4 + r] = to_bf16(p);
+        }
+      lsum[j] = lsum[j] * alpha + psum;
+      m[j] = mnew;
+#pragma unroll
+      for (int db = 0; db < HD / 16; ++db) o[j][db] *= alpha;
+    }
+#pragma unroll
+    for (int db = 0; db < HD / 16; ++db)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        const bf16x8_t vf = frag_col<HD>(vt, 32 * kk, g, 16 * db, c);
+        o[0][db] = mfma16(vf, pf[0][kk], o[0][db]);
+        o[1][db] = mfma16(vf, pf[1][kk], o[1][db]);
+      }
+    if (t + 1 < nt) {
+      sk.store(Ks + ((t + 1) & 1) * BT * HD);
+      sv.store(Vs + ((t + 1) & 1) * BT * HD);
+    }
+    __syncthreads();
   }
-  lsum += __shfl_xor(lsum, 16, 64);
-  lsum += __shfl_xor(lsum, 32, 64);
-  if (qi < a.S) {
-    const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
-    bf16_t* O = reinterpret_cast<bf16_t*>(a.o) + (rowb + qi) * a.ldo + (int64_t)h * HD;
 #pragma unroll
-    for (int db = 0; db < HD / 16; ++db) {
-      ushort4 w = make_ushort4(f32_to_bf16(o[db][0] * inv), f32_to_bf16(o[db][1] * inv),
-                               f32_to_bf16(o[db][2] * inv), f32_to_bf16(o[db][3] * inv));
-      *reinterpret_cast<ushort4*>(O + db * 16 + 4 * g) = w;
+  for (int j = 0; j < 2; ++j) {
+    float ls = lsum[j];
+    ls += __shfl_xor(ls, 16, 64);
+    ls += __shfl_xor(ls, 32, 64);
+    if (qi[j] < a.S) {
+      const float inv = ls > 0.f ? 1.f / ls : 0.f;
+      bf16_t* O = reinterpret_cast<bf16_t*>(a.o) + (rowb + qi[j]) * a.ldo + (int64_t)h * HD;
+#pragma unroll
+      for (int db = 0; db < HD / 16; ++db) {
+        const ushort4 w = make_ushort4(f32_to_bf16(o[j][db][0] * inv), f32_to_bf16(o[j][db][1] * inv),
+                                       f32_to_bf16(o[j][db][2] * inv), f32_to_bf16(o[j][db][3] * inv));
+        *reinterpret_cast<ushort4*>(O + db * 16 + 4 * g) = w;
+      }
+      if (g == 0)
+        a.lse[((int64_t)b * a.Hq + h) * a.S + qi[j]] = ls > 0.f ? m[j] * LN2 + __logf(ls) : -INFINITY;
     }
-    if (g == 0)
-      a.lse[((int64_t)b * a.Hq + h) * a.S + qi] = lsum > 0.f ? m * LN2 + __logf(lsum) : -INFINITY;
   }
 }
 
@@ -255,22 +277,18 @@ __global__ void __launch_bounds__(256) attn_delta_mfma(AttnDesc a) {
 
 // ------------------------------------------------------------------- dK dV
 template <int HD>
-__global__ void __launch_bounds__(256) attn_dkv_mfma(AttnDesc a) {
+__global__ void __launch_bounds__(NTH) attn_dkv_mfma(AttnDesc a) {
   extern __shared__ __align__(16) unsigned char smem[];
-  bf16_t* Qs = reinterpret_cast<bf16_t*>(smem);
-  bf16_t* Qt = Qs + BT * HD;
-  bf16_t* Ds = Qt + BT * HD;
-  bf16_t* Dt = Ds + BT * HD;
-  float* lse2s = reinterpret_cast<float*>(Dt + BT * HD);
-  float* dels = lse2s + BT;
-  const int kblk = gridDim.x - 1 - blockIdx.x;  // keys with the most queries first
+  bf16_t* Qs = reinterpret_cast<bf16_t*>(smem);     // [2][BT * HD]
+  bf16_t* Ds = Qs + 2 * BT * HD;                    // [2][BT * HD]
+  float* stat = reinterpret_cast<float*>(Ds + 2 * BT * HD);  // [2][lse2 64 | delta 64]
+  const int kblk = blockIdx.x;                      // early keys see the most queries: first
   const int kvh = blockIdx.y, b = blockIdx.z;
   const int grp = a.Hq / a.Hkv;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int c16 = lane & 15, g = lane >> 4;
+  const int c = lane & 15, g = lane >> 4;
   const int L = a.seq_lens[b];
-  const int k0 = kblk * BT;
-  const int kj = k0 + wave * 16 + c16;  // this lane's key
+  const int k0 = kblk * BW;
   const int klim = min(a.S, L);
   const int64_t rowb = (int64_t)b * a.S;
   const bf16_t* Q = reinterpret_cast<const bf16_t*>(a.q);
@@ -278,189 +296,270 @@ __global__ void __launch_bounds__(256) attn_dkv_mfma(AttnDesc a) {
   const bf16_t* V = reinterpret_cast<const bf16_t*>(a.v);
   const bf16_t* DO = reinterpret_cast<const bf16_t*>(a.dout);
 
-  bf16x8_t kf[HD / 32], vf[HD / 32];
+  int kj[2];
+  bf16x8_t kf[2][HD / 32], vf[2][HD / 32];
+  f32x4_t dk[2][HD / 16], dv[2][HD / 16];
 #pragma unroll
-  for (int kk = 0; kk < HD / 32; ++kk) {
-    const int64_t off = 8 * g + 32 * kk;
-    kf[kk] = kj < klim ? *reinterpret_cast<const bf16x8_t*>(K + (rowb + kj) * a.ldk + (int64_t)kvh * HD + off)
-                       : zero8();
-    vf[kk] = kj < klim ? *reinterpret_cast<const bf16x8_t*>(V + (rowb + kj) * a.ldv + (int64_t)kvh * HD + off)
-                       : zero8();
-  }
-  f32x4_t dk[HD / 16], dv[HD / 16];
+  for (int j = 0; j < 2; ++j) {
+    kj[j] = k0 + wave * 32 + j * 16 + c;
 #pragma unroll
-  for (int i = 0; i < HD / 16; ++i) {
-    dk[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    dv[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int kk = 0; kk < HD / 32; ++kk) {
+      const int64_t off = (int64_t)kvh * HD + 8 * g + 32 * kk;
+      kf[j][kk] = kj[j] < klim ? *reinterpret_cast<const bf16x8_t*>(K + (rowb + kj[j]) * a.ldk + off) : zero8();
+      vf[j][kk] = kj[j] < klim ? *reinterpret_cast<const bf16x8_t*>(V + (rowb + kj[j]) * a.ldv + off) : zero8();
+    }
+#pragma unroll
+    for (int i = 0; i < HD / 16; ++i) {
+      dk[j][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      dv[j][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    }
   }
   const float cs = a.scale * LOG2E;
-  if (k0 < klim) {
-    for (int hh = 0; hh < grp; ++hh) {
-      const int h = kvh * grp + hh;
-      const float* lse = a.lse + ((int64_t)b * a.Hq + h) * a.S;
-      const float* del = a.delta + ((int64_t)b * a.Hq + h) * a.S;
-      for (int q0 = k0; q0 < a.S; q0 += BT) {
-        __syncthreads();
-        load_nat<HD>(Qs, Q, a.ldq, rowb, q0, a.S, (int64_t)h * HD);
-        load_tr<HD>(Qt, Q, a.ldq, rowb, q0, a.S, (int64_t)h * HD);
-        load_nat<HD>(Ds, DO, a.lddo, rowb, q0, a.S, (int64_t)h * HD);
-        load_tr<HD>(Dt, DO, a.lddo, rowb, q0, a.S, (int64_t)h * HD);
-        if (threadIdx.x < BT) {
-          const int q = q0 + threadIdx.x;
-          lse2s[threadIdx.x] = q < a.S ? lse[q] * LOG2E : -INFINITY;
-          dels[threadIdx.x] = q < a.S ? del[q] : 0.f;
+  // (q-head, query tile) pairs in order; a key block's query tiles start at k0
+  const int ntq = k0 < klim ? (a.S - k0 + BT - 1) / BT : 0;
+  const int nt = grp * ntq;
+  TileStage<HD> sq, sd;
+  float st_l = 0.f, st_d = 0.f;
+  auto issue = [&](int t) {
+    const int h = kvh * grp + t / ntq;
+    const int q0 = k0 + (t % ntq) * BT;
+    sq.load(Q, a.ldq, rowb, q0, a.S, (int64_t)h * HD);
+    sd.load(DO, a.lddo, rowb, q0, a.S, (int64_t)h * HD);
+    if (threadIdx.x < BT) {
+      const int q = q0 + threadIdx.x;
+      const int64_t so = ((int64_t)b * a.Hq + h) * a.S;
+      st_l = q < a.S ? a.lse[so + q] * LOG2E : -INFINITY;
+      st_d = q < a.S ? a.delta[so + q] : 0.f;
+    }
+  };
+  auto commit = [&](int buf) {
+    sq.store(Qs + buf * BT * HD);
+    sd.store(Ds + buf * BT * HD);
+    if (threadIdx.x < BT) {
+      stat[buf * 2 * BT + threadIdx.x] = st_l;
+      stat[buf * 2 * BT + BT + threadIdx.x] = st_d;
+    }
+  };
+  if (nt > 0) {
+    issue(0);
+    commit(0);
+  }
+  __syncthreads();
+  for (int t = 0; t < nt; ++t) {
+    const int buf = t & 1;
+    const int q0 = k0 + (t % ntq) * BT;
+    const bf16_t* qt = Qs + buf * BT * HD;
+    const bf16_t* dt = Ds + buf * BT * HD;
+    const float* l2s = stat + buf * 2 * BT;
+    const float* dls = l2s + BT;
+    if (t + 1 < nt) issue(t + 1);
+    bf16x8_t pk[2][2], dsk[2][2];
+#pragma unroll
+    for (int qb = 0; qb < 4; ++qb) {
+      f32x4_t s[2], dp[2];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        s[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        dp[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      }
+#pragma unroll
+      for (int kk = 0; kk < HD / 32; ++kk) {
+        const bf16x8_t qa = frag_row<HD>(qt, qb * 16 + c, g + 4 * kk);
+        const bf16x8_t da = frag_row<HD>(dt, qb * 16 + c, g + 4 * kk);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          s[j] = mfma16(qa, kf[j][kk], s[j]);
+          dp[j] = mfma16(da, vf[j][kk], dp[j]);
         }
-        __syncthreads();
-        bf16x8_t pk[2], dsk[2];
+      }
 #pragma unroll
-        for (int qb = 0; qb < 4; ++qb) {
-          f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f}, dp = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int r = 0; r < 4; ++r) {
+        const int ql = qb * 16 + 4 * g + r;
+        const int q = q0 + ql;
+        const float l2 = l2s[ql], dl = dls[ql];
 #pragma unroll
-          for (int kk = 0; kk < HD / 32; ++kk) {
-            s = mfma16(frag_nat<HD>(Qs, qb * 16 + c16, g + 4 * kk), kf[kk], s);
-            dp = mfma16(frag_nat<HD>(Ds, qb * 16 + c16, g + 4 * kk), vf[kk], dp);
-          }
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int ql = qb * 16 + 4 * g + r;
-            const int q = q0 + ql;
-            const float l2 = lse2s[ql];
-            const bool ok = q < a.S && kj <= q && kj < klim && l2 != -INFINITY;
-            const float p = ok ? exp2f(s[r] * cs - l2) : 0.f;
-            const float ds = p * (dp[r] - dels[ql]);
-            pk[qb >> 1][(qb & 1) * 4 + r] = to_bf16(p);
-            dsk[qb >> 1][(qb & 1) * 4 + r] = to_bf16(ds);
-          }
+        for (int j = 0; j < 2; ++j) {
+          const bool ok = q < a.S && kj[j] <= q && kj[j] < klim && l2 != -INFINITY;
+          const float p = ok ? exp2f(s[j][r] * cs - l2) : 0.f;
+          pk[j][qb >> 1][(qb & 1) * 4 + r] = to_bf16(p);
+          dsk[j][qb >> 1][(qb & 1) * 4 + r] = to_bf16(p * (dp[j][r] - dl));
         }
-#pragma unroll
-        for (int db = 0; db < HD / 16; ++db)
-#pragma unroll
-          for (int kk = 0; kk < 2; ++kk) {
-            dv[db] = mfma16(pk[kk], frag_tr(Dt, db * 16 + c16, kk, g), dv[db]);
-            dk[db] = mfma16(dsk[kk], frag_tr(Qt, db * 16 + c16, kk, g), dk[db]);
-          }
       }
     }
+#pragma unroll
+    for (int db = 0; db < HD / 16; ++db)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        const bf16x8_t dob = frag_col<HD>(dt, 32 * kk, g, 16 * db, c);
+        const bf16x8_t qbv = frag_col<HD>(qt, 32 * kk, g, 16 * db, c);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          dv[j][db] = mfma16(pk[j][kk], dob, dv[j][db]);
+          dk[j][db] = mfma16(dsk[j][kk], qbv, dk[j][db]);
+        }
+      }
+    if (t + 1 < nt) commit((t + 1) & 1);
+    __syncthreads();
   }
   bf16_t* DK = reinterpret_cast<bf16_t*>(a.dk);
   bf16_t* DV = reinterpret_cast<bf16_t*>(a.dv);
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int key = k0 + wave * 16 + 4 * g + r;
-    if (key < a.S) {
-      if (a.rope) rope_back<HD>(dk, r, a.pos, rowb + key, a.rope, a.max_pos, c16);
+  for (int j = 0; j < 2; ++j)
 #pragma unroll
-      for (int db = 0; db < HD / 16; ++db) {
-        const int64_t col = (int64_t)kvh * HD + db * 16 + c16;
-        DK[(rowb + key) * a.lddk + col] = f32_to_bf16(dk[db][r] * a.scale);
-        DV[(rowb + key) * a.lddv + col] = f32_to_bf16(dv[db][r]);
+    for (int r = 0; r < 4; ++r) {
+      const int key = k0 + wave * 32 + j * 16 + 4 * g + r;
+      if (key < a.S) {
+        if (a.rope) rope_back<HD>(dk[j], r, a.pos, rowb + key, a.rope, a.max_pos, c);
+#pragma unroll
+        for (int db = 0; db < HD / 16; ++db) {
+          const int64_t col = (int64_t)kvh * HD + db * 16 + c;
+          DK[(rowb + key) * a.lddk + col] = f32_to_bf16(dk[j][db][r] * a.scale);
+          DV[(rowb + key) * a.lddv + col] = f32_to_bf16(dv[j][db][r]);
+        }
       }
     }
-  }
 }
 
 // ----------------------------------------------------------------------- dQ
 template <int HD>
-__global__ void __launch_bounds__(256) attn_dq_mfma(AttnDesc a) {
+__global__ void __launch_bounds__(NTH) attn_dq_mfma(AttnDesc a) {
   extern __shared__ __align__(16) unsigned char smem[];
-  bf16_t* Ks = reinterpret_cast<bf16_t*>(smem);
-  bf16_t* Kt = Ks + BT * HD;
-  bf16_t* Vs = Kt + BT * HD;
+  bf16_t* Ks = reinterpret_cast<bf16_t*>(smem);     // [2][BT * HD]
+  bf16_t* Vs = Ks + 2 * BT * HD;                    // [2][BT * HD]
   const int qblk = gridDim.x - 1 - blockIdx.x;
   const int h = blockIdx.y, b = blockIdx.z;
   const int kvh = h / (a.Hq / a.Hkv);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int c16 = lane & 15, g = lane >> 4;
+  const int c = lane & 15, g = lane >> 4;
   const int L = a.seq_lens[b];
-  const int q0 = qblk * BT;
-  const int qi = q0 + wave * 16 + c16;
+  const int q0 = qblk * BW;
   const int64_t rowb = (int64_t)b * a.S;
   const bf16_t* Q = reinterpret_cast<const bf16_t*>(a.q);
   const bf16_t* K = reinterpret_cast<const bf16_t*>(a.k);
   const bf16_t* V = reinterpret_cast<const bf16_t*>(a.v);
   const bf16_t* DO = reinterpret_cast<const bf16_t*>(a.dout);
 
-  bf16x8_t qf[HD / 32], df[HD / 32];
+  int qi[2];
+  bf16x8_t qf[2][HD / 32], df[2][HD / 32];
+  float l2[2], dl[2];
+  f32x4_t dq[2][HD / 16];
 #pragma unroll
-  for (int kk = 0; kk < HD / 32; ++kk) {
-    const int64_t col = (int64_t)h * HD + 8 * g + 32 * kk;
-    qf[kk] = qi < a.S ? *reinterpret_cast<const bf16x8_t*>(Q + (rowb + qi) * a.ldq + col) : zero8();
-    df[kk] = qi < a.S ? *reinterpret_cast<const bf16x8_t*>(DO + (rowb + qi) * a.lddo + col) : zero8();
+  for (int j = 0; j < 2; ++j) {
+    qi[j] = q0 + wave * 32 + j * 16 + c;
+#pragma unroll
+    for (int kk = 0; kk < HD / 32; ++kk) {
+      const int64_t col = (int64_t)h * HD + 8 * g + 32 * kk;
+      qf[j][kk] = qi[j] < a.S ? *reinterpret_cast<const bf16x8_t*>(Q + (rowb + qi[j]) * a.ldq + col) : zero8();
+      df[j][kk] = qi[j] < a.S ? *reinterpret_cast<const bf16x8_t*>(DO + (rowb + qi[j]) * a.lddo + col) : zero8();
+    }
+    const int64_t so = ((int64_t)b * a.Hq + h) * a.S + qi[j];
+    l2[j] = qi[j] < a.S ? a.lse[so] * LOG2E : -INFINITY;
+    dl[j] = qi[j] < a.S ? a.delta[so] : 0.f;
+#pragma unroll
+    for (int i = 0; i < HD / 16; ++i) dq[j][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   }
-  const float l2 = qi < a.S ? a.lse[((int64_t)b * a.Hq + h) * a.S + qi] * LOG2E : -INFINITY;
-  const float dl = qi < a.S ? a.delta[((int64_t)b * a.Hq + h) * a.S + qi] : 0.f;
-  f32x4_t dq[HD / 16];
-#pragma unroll
-  for (int i = 0; i < HD / 16; ++i) dq[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   const float cs = a.scale * LOG2E;
-  const int kend = min(min(q0 + BT, a.S), L);
-
-  for (int k0 = 0; k0 < kend; k0 += BT) {
-    __syncthreads();
-    load_nat<HD>(Ks, K, a.ldk, rowb, k0, kend, (int64_t)kvh * HD);
-    load_tr<HD>(Kt, K, a.ldk, rowb, k0, kend, (int64_t)kvh * HD);
-    load_nat<HD>(Vs, V, a.ldv, rowb, k0, kend, (int64_t)kvh * HD);
-    __syncthreads();
-    bf16x8_t dsk[2];
+  const int kend = min(min(q0 + BW, a.S), L);
+  const int nt = (kend + BT - 1) / BT;
+  TileStage<HD> sk, sv;
+  if (nt > 0) {
+    sk.load(K, a.ldk, rowb, 0, kend, (int64_t)kvh * HD);
+    sv.load(V, a.ldv, rowb, 0, kend, (int64_t)kvh * HD);
+    sk.store(Ks);
+    sv.store(Vs);
+  }
+  __syncthreads();
+  for (int t = 0; t < nt; ++t) {
+    const int k0 = t * BT;
+    const bf16_t* kt = Ks + (t & 1) * BT * HD;
+    const bf16_t* vt = Vs + (t & 1) * BT * HD;
+    if (t + 1 < nt) {
+      sk.load(K, a.ldk, rowb, k0 + BT, kend, (int64_t)kvh * HD);
+      sv.load(V, a.ldv, rowb, k0 + BT, kend, (int64_t)kvh * HD);
+    }
+    bf16x8_t dsk[2][2];
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) {
-      f32x4_t st = f32x4_t{0.f, 0.f, 0.f, 0.f}, dpt = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      f32x4_t st[2], dpt[2];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        st[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        dpt[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      }
 #pragma unroll
       for (int kk = 0; kk < HD / 32; ++kk) {
-        st = mfma16(frag_nat<HD>(Ks, blk * 16 + c16, g + 4 * kk), qf[kk], st);
-        dpt = mfma16(frag_nat<HD>(Vs, blk * 16 + c16, g + 4 * kk), df[kk], dpt);
+        const bf16x8_t ka = frag_row<HD>(kt, blk * 16 + c, g + 4 * kk);
+        const bf16x8_t va = frag_row<HD>(vt, blk * 16 + c, g + 4 * kk);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          st[j] = mfma16(ka, qf[j][kk], st[j]);
+          dpt[j] = mfma16(va, df[j][kk], dpt[j]);
+        }
       }
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int key = k0 + blk * 16 + 4 * g + r;
-        const bool ok = key < kend && key <= qi && l2 != -INFINITY;
-        const float p = ok ? exp2f(st[r] * cs - l2) : 0.f;
-        dsk[blk >> 1][(blk & 1) * 4 + r] = to_bf16(p * (dpt[r] - dl));
-      }
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = k0 + blk * 16 + 4 * g + r;
+          const bool ok = key < kend && key <= qi[j] && l2[j] != -INFINITY;
+          const float p = ok ? exp2f(st[j][r] * cs - l2[j]) : 0.f;
+          dsk[j][blk >> 1][(blk & 1) * 4 + r] = to_bf16(p * (dpt[j][r] - dl[j]));
+        }
     }
 #pragma unroll
     for (int db = 0; db < HD / 16; ++db)
 #pragma unroll
-      for (int kk = 0; kk < 2; ++kk) dq[db] = mfma16(dsk[kk], frag_tr(Kt, db * 16 + c16, kk, g), dq[db]);
+      for (int kk = 0; kk < 2; ++kk) {
+        const bf16x8_t kb = frag_col<HD>(kt, 32 * kk, g, 16 * db, c);
+        dq[0][db] = mfma16(dsk[0][kk], kb, dq[0][db]);
+        dq[1][db] = mfma16(dsk[1][kk], kb, dq[1][db]);
+      }
+    if (t + 1 < nt) {
+      sk.store(Ks + ((t + 1) & 1) * BT * HD);
+      sv.store(Vs + ((t + 1) & 1) * BT * HD);
+    }
+    __syncthreads();
   }
   bf16_t* DQ = reinterpret_cast<bf16_t*>(a.dq);
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int q = q0 + wave * 16 + 4 * g + r;
-    if (q < a.S) {
-      if (a.rope) rope_back<HD>(dq, r, a.pos, rowb + q, a.rope, a.max_pos, c16);
+  for (int j = 0; j < 2; ++j)
 #pragma unroll
-      for (int db = 0; db < HD / 16; ++db)
-        DQ[(rowb + q) * a.lddq + (int64_t)h * HD + db * 16 + c16] = f32_to_bf16(dq[db][r] * a.scale);
+    for (int r = 0; r < 4; ++r) {
+      const int q = q0 + wave * 32 + j * 16 + 4 * g + r;
+      if (q < a.S) {
+        if (a.rope) rope_back<HD>(dq[j], r, a.pos, rowb + q, a.rope, a.max_pos, c);
+#pragma unroll
+        for (int db = 0; db < HD / 16; ++db)
+          DQ[(rowb + q) * a.lddq + (int64_t)h * HD + db * 16 + c] = f32_to_bf16(dq[j][db][r] * a.scale);
+      }
     }
-  }
 }
 
 // ------------------------------------------------------------------ launch
-template <typename K>
-static hipError_t set_lds(K kern, size_t bytes) {
+template <typename Kern>
+static hipError_t set_lds(Kern kern, size_t bytes) {
   return hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
                              (int)bytes);
 }
 
 template <int HD>
 static hipError_t fwd(const AttnDesc& a, hipStream_t s) {
-  const size_t lds = (size_t)2 * BT * HD * sizeof(bf16_t);
+  const size_t lds = (size_t)4 * BT * HD * sizeof(bf16_t);
   static bool once = false;
   if (!once) {
     hipError_t e = set_lds(attn_fwd_mfma<HD>, lds);
     if (e != hipSuccess) return e;
     once = true;
   }
-  dim3 grid((a.S + BT - 1) / BT, a.Hq, a.B);
-  hipLaunchKernelGGL(attn_fwd_mfma<HD>, grid, dim3(256), lds, s, a);
+  dim3 grid((a.S + BW - 1) / BW, a.Hq, a.B);
+  hipLaunchKernelGGL(attn_fwd_mfma<HD>, grid, dim3(NTH), lds, s, a);
   return hipGetLastError();
 }
 
 template <int HD>
 static hipError_t bwd(const AttnDesc& a, hipStream_t s) {
-  const size_t lds_kv = (size_t)4 * BT * HD * sizeof(bf16_t) + 2 * BT * sizeof(float);
-  const size_t lds_q = (size_t)3 * BT * HD * sizeof(bf16_t);
+  const size_t lds_kv = (size_t)4 * BT * HD * sizeof(bf16_t) + 4 * BT * sizeof(float);
+  const size_t lds_q = (size_t)4 * BT * HD * sizeof(bf16_t);
   static bool once = false;
   if (!once) {
     hipError_t e = set_lds(attn_dkv_mfma<HD>, lds_kv);
@@ -473,12 +572,12 @@ static hipError_t bwd(const AttnDesc& a, hipStream_t s) {
                      s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  dim3 gk((a.S + BT - 1) / BT, a.Hkv, a.B);
-  hipLaunchKernelGGL(attn_dkv_mfma<HD>, gk, dim3(256), lds_kv, s, a);
+  dim3 gk((a.S + BW - 1) / BW, a.Hkv, a.B);
+  hipLaunchKernelGGL(attn_dkv_mfma<HD>, gk, dim3(NTH), lds_kv, s, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  dim3 gq((a.S + BT - 1) / BT, a.Hq, a.B);
-  hipLaunchKernelGGL(attn_dq_mfma<HD>, gq, dim3(256), lds_q, s, a);
+  dim3 gq((a.S + BW - 1) / BW, a.Hq, a.B);
+  hipLaunchKernelGGL(attn_dq_mfma<HD>, gq, dim3(NTH), lds_q, s, a);
   return hipGetLastError();
 }
 
@@ -498,8 +597,8 @@ hipError_t launch_attn_fwd_mfma(const AttnDesc& a, hipStream_t s, bool* handled)
   return a.hd == 128 ? fwd<128>(a, s) : fwd<64>(a, s);
 }
 
+// dq / dk leave with the inverse RoPE applied when a.rope is set.
 hipError_t launch_attn_bwd_mfma(const AttnDesc& a, hipStream_t s, bool* handled) {
-  // dq / dk leave with the inverse RoPE applied when a.rope is set
   *handled = mfma_ok(a) && a.lddo % 8 == 0 && (uintptr_t)a.dout % 16 == 0;
   if (!*handled) return hipSuccess;
   return a.hd == 128 ? bwd<128>(a, s) : bwd<64>(a, s);

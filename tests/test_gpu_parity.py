@@ -74,8 +74,12 @@ def _compare(shp, dev, ref, tol, lr, optimizer, gate_adam_delta=True):
             report[f"p{s}:{k}"] = rel_err(dev["masters"][s][k], ref["masters"][s][k])
             dd = dev["masters"][s][k] - dev["masters"][s - 1][k]
             rd = ref["masters"][s][k] - ref["masters"][s - 1][k]
+            # the device keeps master in fp32: a delta is resolved only to one
+            # ulp of the new value, so deltas are gated as
+            # ||dd - rd|| < tol ||rd|| + ||ulp(theta_new)||
+            ulp = np.spacing(np.abs(ref["masters"][s][k]).astype(np.float32)).astype(np.float64)
             if optimizer == "sgd":
-                report[f"d{s}:{k}"] = rel_err(dd, rd)
+                report[f"d{s}:{k}"] = np.linalg.norm(dd - rd) / (np.linalg.norm(rd) + np.linalg.norm(ulp) / tol)
             elif gate_adam_delta:
                 # g -> g / (|g| + eps) is ill-conditioned where g is at rounding
                 # noise (e.g. the key bias, whose exact gradient is 0 because a
@@ -84,10 +88,6 @@ def _compare(shp, dev, ref, tol, lr, optimizer, gate_adam_delta=True):
                 g0 = np.abs(ref["grads"][0][k])
                 keep = g0 > 1e-4 * np.sqrt(np.mean(g0 ** 2)) + 1e-12
                 if keep.any():
-                    # the device keeps master in fp32: its delta is resolved only
-                    # to one ulp of the new value, so the gate is
-                    # ||dd - rd|| < tol ||rd|| + ||ulp(theta_new)||
-                    ulp = np.spacing(np.abs(ref["masters"][s][k]).astype(np.float32)).astype(np.float64)
                     err = np.linalg.norm((dd - rd)[keep])
                     report[f"d{s}:{k}"] = err / (np.linalg.norm(rd[keep]) + np.linalg.norm(ulp[keep]) / tol)
     worst = max(report, key=report.get)
@@ -200,5 +200,5 @@ def test_llama8b_bf16_one_layer_slice():
 
 
 def test_llama8b_bf16_two_layers_alpha1_sgd():
-    _case(workload.get_config("8b").with_(n_layers=2, batch=1, seq=128), alpha=1.0,
+    _case(workload.get_config("8b").with_(n_layers=2, batch=1, seq=256), alpha=1.0,
           optimizer="sgd", lr=1e-3)
