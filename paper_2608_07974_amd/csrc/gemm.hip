@@ -1,10 +1,12 @@
 // GEMM kernels for every linear of the chunk map (Eq. (1)) and the frozen
 // readout head (Eq. (2)), forward, data-gradient and weight-gradient forms.
 //
-// bf16: MFMA 32x32x16 (fp32 accumulate), LDS double-buffered tiles staged
-// through registers, 16-byte XOR-swizzled LDS rows, 8x8 in-register
-// transposes for operands whose contiguous dimension is not K, and an
-// XCD-aware tile order so tiles sharing operand panels run on one L2.
+// bf16: MFMA 32x32x16 (fp32 accumulate) on LDS double-buffered tiles with
+// 16-byte XOR-swizzled rows and an XCD-aware tile order so tiles sharing
+// operand panels run on one L2.  The main path copies tiles global -> LDS
+// with the buffer unit's direct-to-LDS loads and reads MN-major operands
+// with LDS transpose reads; a register-staged path (8x8 in-register
+// transposes) covers operands that do not meet the direct path's alignment.
 // fp32: a plain LDS-tiled SIMT kernel (the fp32 configuration is small).
 #include <stdio.h>
 
@@ -105,6 +107,58 @@ __device__ inline void tile_coords(int nbm, int nbn, int& tm, int& tn) {
   const int in_group = b % (GROUP_M * nbn);
   tm = first_m + in_group % gsz;
   tn = in_group / gsz;
+}
+
+// Epilogue through LDS, one 32-row block of every wave tile at a time: the
+// accumulators are written with compile-time indices (so they stay in
+// registers), then read back row-contiguously, which coalesces the global
+// stores of the epilogue.  Callers end their main loop with a barrier.
+template <int BM, int BN, int WM, int WN>
+__device__ inline void store_tile(const f32x16_t (&acc)[BM / WM / 32][BN / WN / 32],
+                                  unsigned char* smem, const GemmDesc& g, const EpiArgs& e,
+                                  int m0, int n0, int wave, int lane) {
+  constexpr int TM = BM / WM, TN = BN / WN;
+  constexpr int FM = TM / 32, FN = TN / 32;
+  const int wm = wave / WN, wn = wave % WN;
+  constexpr int LDW = TN + 4;
+  static_assert(WM * WN * 32 * LDW * 4 <= 160 * 1024, "epilogue tile exceeds LDS");
+  float* ep = reinterpret_cast<float*>(smem) + wave * 32 * LDW;
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        ep[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * LDW + j * 32 + (lane & 31)] = acc[i][j][r];
+    __syncthreads();
+    const int mb = m0 + wm * TM + i * 32, nb = n0 + wn * TN;
+    if (e.kind == EPI_ROPE) {
+      // wave tiles are head-aligned (nb % hd == 0, TN % hd == 0), so the
+      // partner column j +- hd/2 of a head lives in the same staged row
+      const int half = e.hd >> 1;
+      for (int t = lane; t < 32 * TN; t += 64) {
+        const int row = t / TN, col = t % TN;
+        const int n = nb + col, m = mb + row;
+        float v = ep[row * LDW + col];
+        if (n < e.n_rot && m < g.M) {
+          const int j = n % e.hd;
+          const bool lo = j < half;
+          const float pv = ep[row * LDW + (lo ? col + half : col - half)];
+          int p = e.pos[m];
+          p = p < 0 ? 0 : (p >= e.max_pos ? e.max_pos - 1 : p);
+          const float2 cs = e.rope[(int64_t)p * half + (lo ? j : j - half)];
+          v = lo ? v * cs.x - pv * cs.y : v * cs.x + pv * cs.y;
+        }
+        epilogue(e, g.M, g.N, m, n, v);
+      }
+    } else {
+      for (int t = lane; t < 32 * TN; t += 64) {
+        const int row = t / TN, col = t % TN;
+        epilogue(e, g.M, g.N, mb + row, nb + col, ep[row * LDW + col]);
+      }
+    }
+    __syncthreads();
+  }
 }
 
 // ------------------------------------------------------------ MFMA kernel
@@ -230,6 +284,20 @@ gemm_mfma_kernel(GemmDesc g, EpiArgs e) {
   Stage<BM, NT, AK> sa;
   Stage<BN, NT, BKM> sb;
   const int nk = (g.K + BKT - 1) / BKT;
+  constexpr int NS = BKT / 16;  // k16 slices per tile
+
+  // Per-lane LDS element offsets of each k16 slice (loop invariant).  The
+  // swizzle depends on the row only through (row >> 1) & 7 and fragment rows
+  // step by 32, so fragment i adds the immediate i * 32 * BKT.
+  int offA[NS], offB[NS];
+  {
+    const int l = lane & 31, h = lane >> 5, sw = (l >> 1) & 7;
+#pragma unroll
+    for (int q = 0; q < NS; ++q) {
+      offA[q] = (wm * TM + l) * BKT + (((2 * q + h) ^ sw) * 8);
+      offB[q] = (wn * TN + l) * BKT + (((2 * q + h) ^ sw) * 8);
+    }
+  }
 
   sa.load(A, g.lda, m0, g.M, 0, g.ka);
   sb.load(B, g.ldb, n0, g.N, 0, g.kb);
@@ -245,25 +313,29 @@ gemm_mfma_kernel(GemmDesc g, EpiArgs e) {
     }
     const bf16_t* as = As + cur * BM * BKT;
     const bf16_t* bs = Bs + cur * BN * BKT;
+    // fragments double-buffered across slices: slice q+1 is read from LDS
+    // while the MFMAs of slice q run
+    bf16x8_t af[2][FM], bfr[2][FN];
 #pragma unroll
-    for (int s = 0; s < BKT / 16; ++s) {
-      const int chunk = 2 * s + (lane >> 5);
-      bf16x8_t af[FM], bfr[FN];
+    for (int i = 0; i < FM; ++i) af[0][i] = *reinterpret_cast<const bf16x8_t*>(as + offA[0] + i * 32 * BKT);
 #pragma unroll
-      for (int i = 0; i < FM; ++i) {
-        const int row = wm * TM + i * 32 + (lane & 31);
-        af[i] = *reinterpret_cast<const bf16x8_t*>(as + row * BKT + ((chunk ^ swz(row)) * 8));
-      }
+    for (int j = 0; j < FN; ++j) bfr[0][j] = *reinterpret_cast<const bf16x8_t*>(bs + offB[0] + j * 32 * BKT);
 #pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int row = wn * TN + j * 32 + (lane & 31);
-        bfr[j] = *reinterpret_cast<const bf16x8_t*>(bs + row * BKT + ((chunk ^ swz(row)) * 8));
+    for (int q = 0; q < NS; ++q) {
+      const int cb = q & 1, nb = cb ^ 1;
+      if (q + 1 < NS) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+          af[nb][i] = *reinterpret_cast<const bf16x8_t*>(as + offA[q + 1] + i * 32 * BKT);
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          bfr[nb][j] = *reinterpret_cast<const bf16x8_t*>(bs + offB[q + 1] + j * 32 * BKT);
       }
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cb][i], bfr[cb][j], acc[i][j], 0, 0, 0);
     }
     if (kt + 1 < nk) {
       sa.store(As + (cur ^ 1) * BM * BKT);
@@ -272,49 +344,200 @@ gemm_mfma_kernel(GemmDesc g, EpiArgs e) {
     __syncthreads();
   }
 
-  // Epilogue through LDS, one 32-row block of every wave tile at a time:
-  // the accumulators are written with compile-time indices (so they stay in
-  // registers), then read back row-contiguously, which coalesces the
-  // global stores of the epilogue.
-  constexpr int LDW = TN + 4;
-  static_assert(WM * WN * 32 * LDW * 4 <= 2 * (BM + BN) * BKT * 2, "epilogue tile exceeds LDS");
-  float* ep = reinterpret_cast<float*>(smem) + wave * 32 * LDW;
+  store_tile<BM, BN, WM, WN>(acc, smem, g, e, m0, n0, wave, lane);
+}
+
+// ------------------------------------------------- direct-to-LDS MFMA kernel
+// Operand tiles are copied global -> LDS by the buffer unit (16 bytes per
+// lane, lane i's bytes land at M0 + 16 i; an offset at or above the
+// resource's record count reads as zero), so no staging registers, no LDS
+// store instructions and no transposes.  LDS layouts:
+//   K-major operand  [row][64 k],  16-B chunk c of row r at c ^ ((r >> 1) & 7)
+//   MN-major operand [k][R],       16-B chunk c of row k at c ^ xs(k & 3)
+// and the DMA lane -> global mapping applies the inverse swizzle.  MN-major
+// fragments are read with the LDS transpose read (ds_read_b64_tr_b16).
+typedef int32_t i32x4_t __attribute__((ext_vector_type(4)));
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef short s16x8_t __attribute__((ext_vector_type(8)));
+constexpr uint32_t DMA_OOB = 0x80000000u;  // record count; offsets >= it read as 0
+
+__device__ inline i32x4_t buffer_rsrc(const void* base) {
+  const uint64_t p = reinterpret_cast<uint64_t>(base);
+  i32x4_t r;
+  r[0] = (int32_t)(uint32_t)p;
+  r[1] = (int32_t)(uint32_t)(p >> 32);  // stride 0: raw byte addressing
+  r[2] = (int32_t)DMA_OOB;
+  r[3] = 0x00020000;
+  return r;
+}
+
+// LDS-row swizzle of an MN-major tile: over any 4 consecutive k rows the
+// values differ in bits 2-3 (distinct 64-byte bank groups for a half-wave
+// transpose read) and in bits 1-2 (distinct 32-byte groups for 16 lanes).
+__device__ inline int xs(int b) { return (0xCA60 >> (4 * b)) & 15; }
+
+__device__ inline void dma16(uint32_t lds_byte, uint32_t voff, i32x4_t rsrc) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(lds_byte), "v"(voff), "s"(rsrc)
+               : "memory");
+}
+__device__ inline void dma_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// One operand's 64-deep k tile, R rows of M (or N), copied by NT threads.
+template <int R, int NT, bool KMAJ>
+struct DmaTile {
+  static constexpr int ITEMS = R * 8 / NT;  // 16-B chunks per thread
+  static_assert(ITEMS * NT == R * 8, "tile chunks must divide over the threads");
+  uint32_t off[ITEMS];  // byte offset at k0 = 0 from the tile origin, or DMA_OOB
+  int kr[ITEMS];        // k of the chunk's first element within the tile
+  uint32_t kstride;     // bytes per unit of k
+
+  __device__ inline void init(int wave, int lane, int64_t ld, int rvalid) {
 #pragma unroll
-  for (int i = 0; i < FM; ++i) {
+    for (int j = 0; j < ITEMS; ++j) {
+      const int c = (wave * ITEMS + j) * 64 + lane;
+      if (KMAJ) {
+        const int row = c >> 3, ch = (c & 7) ^ ((row >> 1) & 7);
+        kr[j] = ch * 8;
+        off[j] = row < rvalid ? (uint32_t)(row * ld) * 2u + (uint32_t)ch * 16u : DMA_OOB;
+      } else {
+        constexpr int CPR = R / 8;
+        const int k = c / CPR, ch = (c % CPR) ^ xs(k & 3);
+        kr[j] = k;
+        off[j] = ch * 8 < rvalid ? (uint32_t)(k * ld) * 2u + (uint32_t)ch * 16u : DMA_OOB;
+      }
+    }
+    kstride = KMAJ ? 2u : (uint32_t)ld * 2u;
+  }
+  __device__ inline void issue(uint32_t lds_byte, int wave, int k0, int kvalid, i32x4_t rsrc) const {
+#pragma unroll
+    for (int j = 0; j < ITEMS; ++j) {
+      // a row outside the tile has off = DMA_OOB, and DMA_OOB plus any
+      // in-range k advance (< 2^31) stays at or above the record count
+      const uint32_t v = k0 + kr[j] < kvalid ? off[j] + (uint32_t)k0 * kstride : DMA_OOB;
+      dma16(lds_byte + (uint32_t)(wave * ITEMS + j) * 1024u, v, rsrc);
+    }
+  }
+};
+
+// Per-lane LDS fragment addressing of one operand for the 32x32x16 MFMA:
+// lane l supplies row (l & 31) and k 8 (l >> 5) .. +7 of the 16-deep slice.
+template <int R, int T, int F, bool KMAJ>
+struct FragTile {
+  static constexpr int NS = BKT / 16;
+  static constexpr int NO = KMAJ ? NS : F;
+  int off[NO];  // element offsets: per slice (K-major) or per fragment (MN-major)
+
+  __device__ inline void init(int wrow, int lane) {
+    if (KMAJ) {
+      const int l = lane & 31, h = lane >> 5, sw = (l >> 1) & 7;
+#pragma unroll
+      for (int q = 0; q < NS; ++q) off[q] = (wrow + l) * BKT + (((2 * q + h) ^ sw) * 8);
+    } else {
+      // transpose read: lane r of 16-lane group G addresses k row
+      // 8 (G >> 1) + (r >> 2) (+ 16 q + 4 t) and the 4 elements at
+      // m = wrow + 32 i + 16 (G & 1) + 4 (r & 3); it receives column
+      // m = ... + r of those 4 k rows
+      const int G = lane >> 4, r = lane & 15;
+      const int kl = 8 * (G >> 1) + (r >> 2);
+      const int P = (wrow >> 3) ^ (2 * (G & 1) + ((r >> 1) & 1)) ^ xs(r >> 2);
+#pragma unroll
+      for (int i = 0; i < F; ++i) off[i] = kl * R + ((P ^ (4 * i)) << 3) + 4 * (r & 1);
+    }
+  }
+  __device__ inline bf16x8_t read(const bf16_t* tile, int q, int i) const {
+    if (KMAJ) {
+      return *reinterpret_cast<const bf16x8_t*>(tile + off[q] + i * 32 * BKT);
+    } else {
+      const bf16_t* p = tile + off[i] + 16 * q * R;
+      const s16x4_t x = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) s16x4_t*)(p));
+      const s16x4_t y = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) s16x4_t*)(p + 4 * R));
+      return __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(x, y, 0, 1, 2, 3, 4, 5, 6, 7));
+    }
+  }
+};
+
+template <int BM, int BN, int WM, int WN, bool AK, bool BKM>
+__global__ void __launch_bounds__(WM * WN * 64)
+gemm_dma_kernel(GemmDesc g, EpiArgs e) {
+  constexpr int NT = WM * WN * 64;
+  constexpr int TM = BM / WM, TN = BN / WN;
+  constexpr int FM = TM / 32, FN = TN / 32;
+  constexpr int NS = BKT / 16;
+  constexpr uint32_t ABYTES = BM * BKT * 2, STAGE = (BM + BN) * BKT * 2;
+  extern __shared__ __align__(16) unsigned char smem[];
+
+  const int nbm = (g.M + BM - 1) / BM, nbn = (g.N + BN - 1) / BN;
+  int tm, tn;
+  tile_coords(nbm, nbn, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int wm = wave / WN, wn = wave % WN;
+
+  const bf16_t* A = reinterpret_cast<const bf16_t*>(g.A);
+  const bf16_t* B = reinterpret_cast<const bf16_t*>(g.B);
+  const i32x4_t ra = buffer_rsrc(A + (AK ? (int64_t)m0 * g.lda : (int64_t)m0));
+  const i32x4_t rb = buffer_rsrc(B + (BKM ? (int64_t)n0 * g.ldb : (int64_t)n0));
+  DmaTile<BM, NT, AK> da;
+  DmaTile<BN, NT, BKM> db;
+  da.init(wave, lane, g.lda, min(g.M - m0, BM));
+  db.init(wave, lane, g.ldb, min(g.N - n0, BN));
+  FragTile<BM, TM, FM, AK> fa;
+  FragTile<BN, TN, FN, BKM> fb;
+  fa.init(wm * TM, lane);
+  fb.init(wn * TN, lane);
+
+  f32x16_t acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
 #pragma unroll
     for (int j = 0; j < FN; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        ep[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * LDW + j * 32 + (lane & 31)] = acc[i][j][r];
-    __syncthreads();
-    const int mb = m0 + wm * TM + i * 32, nb = n0 + wn * TN;
-    if (e.kind == EPI_ROPE) {
-      // wave tiles are head-aligned (nb % hd == 0, TN % hd == 0), so the
-      // partner column j +- hd/2 of a head lives in the same staged row
-      const int half = e.hd >> 1;
-      for (int t = lane; t < 32 * TN; t += 64) {
-        const int row = t / TN, col = t % TN;
-        const int n = nb + col, m = mb + row;
-        float v = ep[row * LDW + col];
-        if (n < e.n_rot && m < g.M) {
-          const int j = n % e.hd;
-          const bool lo = j < half;
-          const float pv = ep[row * LDW + (lo ? col + half : col - half)];
-          int p = e.pos[m];
-          p = p < 0 ? 0 : (p >= e.max_pos ? e.max_pos - 1 : p);
-          const float2 cs = e.rope[(int64_t)p * half + (lo ? j : j - half)];
-          v = lo ? v * cs.x - pv * cs.y : v * cs.x + pv * cs.y;
-        }
-        epilogue(e, g.M, g.N, m, n, v);
-      }
-    } else {
-      for (int t = lane; t < 32 * TN; t += 64) {
-        const int row = t / TN, col = t % TN;
-        epilogue(e, g.M, g.N, mb + row, nb + col, ep[row * LDW + col]);
-      }
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>(smem);
+  const int nk = (g.K + BKT - 1) / BKT;
+  da.issue(lds0, wave, 0, g.ka, ra);
+  db.issue(lds0 + ABYTES, wave, 0, g.kb, rb);
+  dma_wait();
+  __syncthreads();
+
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < nk) {
+      const uint32_t nxt = lds0 + (cur ^ 1) * STAGE;
+      da.issue(nxt, wave, (kt + 1) * BKT, g.ka, ra);
+      db.issue(nxt + ABYTES, wave, (kt + 1) * BKT, g.kb, rb);
     }
+    const bf16_t* as = reinterpret_cast<const bf16_t*>(smem + cur * STAGE);
+    const bf16_t* bs = as + BM * BKT;
+    bf16x8_t af[2][FM], bfr[2][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) af[0][i] = fa.read(as, 0, i);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) bfr[0][j] = fb.read(bs, 0, j);
+#pragma unroll
+    for (int q = 0; q < NS; ++q) {
+      const int cb = q & 1, nb = cb ^ 1;
+      if (q + 1 < NS) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i) af[nb][i] = fa.read(as, q + 1, i);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) bfr[nb][j] = fb.read(bs, q + 1, j);
+      }
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cb][i], bfr[cb][j], acc[i][j], 0, 0, 0);
+    }
+    dma_wait();
     __syncthreads();
   }
+  store_tile<BM, BN, WM, WN>(acc, smem, g, e, m0, n0, wave, lane);
 }
 
 // ------------------------------------------------------------ SIMT (fp32)
@@ -370,7 +593,11 @@ __global__ void __launch_bounds__(256) gemm_simt_kernel(GemmDesc g, EpiArgs e) {
 template <int BM, int BN, int WM, int WN, bool AK, bool BKM>
 static hipError_t run_mfma(const GemmDesc& g, const EpiArgs& e, hipStream_t s) {
   auto kern = gemm_mfma_kernel<BM, BN, WM, WN, AK, BKM>;
-  const size_t lds = (size_t)2 * (BM + BN) * BKT * sizeof(bf16_t);
+  // LDS: the double-buffered operand tiles, reused by the epilogue's
+  // 32-row fp32 staging of every wave tile
+  const size_t lds_main = (size_t)2 * (BM + BN) * BKT * sizeof(bf16_t);
+  const size_t lds_epi = (size_t)WM * WN * 32 * (BN / WN + 4) * sizeof(float);
+  const size_t lds = lds_main > lds_epi ? lds_main : lds_epi;
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t err = hipFuncSetAttribute((const void*)kern,
@@ -387,11 +614,41 @@ static const char* layout_tag(bool ak, bool bk) {
   return ak ? (bk ? "kk" : "kn") : (bk ? "mk" : "mn");
 }
 
+template <int BM, int BN, int WM, int WN, bool AK, bool BKM>
+static hipError_t run_dma(const GemmDesc& g, const EpiArgs& e, hipStream_t s) {
+  auto kern = gemm_dma_kernel<BM, BN, WM, WN, AK, BKM>;
+  const size_t lds_main = (size_t)2 * (BM + BN) * BKT * sizeof(bf16_t);
+  const size_t lds_epi = (size_t)WM * WN * 32 * (BN / WN + 4) * sizeof(float);
+  const size_t lds = lds_main > lds_epi ? lds_main : lds_epi;
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t err = hipFuncSetAttribute((const void*)kern,
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (err != hipSuccess) return err;
+    attr_set = true;
+  }
+  const int nb = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
+  hipLaunchKernelGGL(kern, dim3(nb), dim3(WM * WN * 64), lds, s, g, e);
+  return hipGetLastError();
+}
+
+// The direct-to-LDS path copies whole 16-byte chunks with 32-bit buffer
+// offsets from the tile origin: every chunk it reads must be either fully
+// valid or fully outside (K-major: valid k a multiple of 8; MN-major: the
+// M or N extent a multiple of 8), rows 16-byte aligned, and the largest
+// offset below 2^31.
+static bool dma_operand_ok(const void* p, int64_t ld, bool kmaj, int rows, int kvalid, int R) {
+  if (reinterpret_cast<uintptr_t>(p) % 16 != 0 || ld % 8 != 0) return false;
+  const int64_t lim = (int64_t)1 << 31;
+  if (kmaj) return kvalid % 8 == 0 && ((int64_t)R * ld + kvalid + BKT) * 2 < lim;
+  return rows % 8 == 0 && ((int64_t)(kvalid + BKT) * ld + R) * 2 < lim;
+}
+
 template <bool AK, bool BKM>
 static hipError_t run_layout(const GemmDesc& g, const EpiArgs& e, int dtype, hipStream_t s,
                              const char** kname) {
-  static const char* names[3] = {nullptr, nullptr, nullptr};
-  static char buf[3][40];
+  static const char* names[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
+  static char buf[5][40];
   int which;
   hipError_t err;
   if (dtype == F32) {
@@ -402,12 +659,26 @@ static hipError_t run_layout(const GemmDesc& g, const EpiArgs& e, int dtype, hip
   } else {
     const long big = (long)((g.M + 255) / 256) * ((g.N + 255) / 256);
     // the RoPE epilogue needs head-aligned wave tiles of 128 columns
-    if (big >= 240 || e.kind == EPI_ROPE) { err = run_mfma<256, 256, 2, 2, AK, BKM>(g, e, s); which = 1; }
-    else { err = run_mfma<128, 128, 2, 2, AK, BKM>(g, e, s); which = 2; }
+    const bool large = big >= 240 || e.kind == EPI_ROPE;
+    const int R = large ? 256 : 128;
+    const bool dma = dma_operand_ok(g.A, g.lda, AK, g.M, g.ka, R) &&
+                     dma_operand_ok(g.B, g.ldb, BKM, g.N, g.kb, R);
+    if (dma) {
+      if (large) { err = run_dma<256, 256, 4, 2, AK, BKM>(g, e, s); which = 3; }
+      else { err = run_dma<128, 128, 2, 2, AK, BKM>(g, e, s); which = 4; }
+    } else if (large) {
+      if constexpr (AK && BKM) err = run_mfma<256, 256, 4, 2, AK, BKM>(g, e, s);
+      else err = run_mfma<256, 256, 2, 2, AK, BKM>(g, e, s);
+      which = 1;
+    } else {
+      err = run_mfma<128, 128, 2, 2, AK, BKM>(g, e, s);
+      which = 2;
+    }
   }
   if (kname) {
     if (!names[which]) {
-      static const char* base[3] = {"gemm_simt_64x64", "gemm_mfma_256x256", "gemm_mfma_128x128"};
+      static const char* base[5] = {"gemm_simt_64x64", "gemm_mfma_256x256", "gemm_mfma_128x128",
+                                    "gemm_dma_256x256", "gemm_dma_128x128"};
       snprintf(buf[which], sizeof(buf[which]), "%s_%s", base[which], layout_tag(AK, BKM));
       names[which] = buf[which];
     }
