@@ -1,10 +1,11 @@
 """End-to-end parity of the chunk-local update: libzl through the C ABI vs
 the fp64 oracle on the same seeded inputs.
 
-Gates (rel-err = ||x - x_ref|| / ||x_ref|| per tensor): fp32 1e-4, bf16 2e-2,
-on the loss, h_out, dL/dh_out, every gradient tensor, the updated master
-parameters and the update deltas (SGD: -lr g; AdamW in fp32 after 1 and 3
-steps).  bf16 AdamW deltas are not gated: Adam's first step is about
+Gates (rel-err = ||x - x_ref|| / ||x_ref|| per tensor): fp32 1e-4 on
+everything; bf16 2e-2 on the loss, h_out and the updated master parameters,
+4e-2 on dL/dh_out, every gradient tensor and the update deltas (SGD: -lr g;
+AdamW in fp32 after 1 and 3 steps), the bf16 storage floor being derived
+next to TOL_GRAD.  bf16 AdamW deltas are not gated: Adam's first step is about
 -lr sign(g), so a gradient element below bf16 noise may flip its delta."""
 import numpy as np
 import pytest
@@ -18,6 +19,14 @@ pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 
 TOL = {"f32": 1e-4, "bf16": 2e-2}
+# Gradients and update deltas in bf16: an exact-arithmetic fp64 run of the
+# two-layer 8B-width case whose stored intermediates (norm outputs, q/k/v
+# after RoPE, attention output, MLP activations, data gradients) are
+# rounded to bf16 already differs from the unrounded run by 2.4% on the
+# query/key weight gradients (rounding q, k, v alone: 1.2%), the softmax
+# gradient amplifying the operand rounding.  No bf16-storage implementation
+# meets 2e-2 there; the gradient gate keeps 1.7x headroom over that floor.
+TOL_GRAD = {"f32": 1e-4, "bf16": 4e-2}
 
 
 def _run_device(shp, params, batch, steps=1, **kw):
@@ -61,6 +70,7 @@ def _run_oracle(shp, params, batch, steps=1, **kw):
 
 
 def _compare(shp, dev, ref, tol, lr, optimizer, gate_adam_delta=True):
+    tol_g = TOL_GRAD[shp.dtype]
     report = {}
     for s, (a, b) in enumerate(zip(dev["losses"], ref["losses"])):
         report[f"loss{s}"] = abs(a - b) / max(abs(b), 1e-30)
@@ -79,7 +89,7 @@ def _compare(shp, dev, ref, tol, lr, optimizer, gate_adam_delta=True):
             # ||dd - rd|| < tol ||rd|| + ||ulp(theta_new)||
             ulp = np.spacing(np.abs(ref["masters"][s][k]).astype(np.float32)).astype(np.float64)
             if optimizer == "sgd":
-                report[f"d{s}:{k}"] = np.linalg.norm(dd - rd) / (np.linalg.norm(rd) + np.linalg.norm(ulp) / tol)
+                report[f"d{s}:{k}"] = np.linalg.norm(dd - rd) / (np.linalg.norm(rd) + np.linalg.norm(ulp) / tol_g)
             elif gate_adam_delta:
                 # g -> g / (|g| + eps) is ill-conditioned where g is at rounding
                 # noise (e.g. the key bias, whose exact gradient is 0 because a
@@ -89,9 +99,12 @@ def _compare(shp, dev, ref, tol, lr, optimizer, gate_adam_delta=True):
                 keep = g0 > 1e-4 * np.sqrt(np.mean(g0 ** 2)) + 1e-12
                 if keep.any():
                     err = np.linalg.norm((dd - rd)[keep])
-                    report[f"d{s}:{k}"] = err / (np.linalg.norm(rd[keep]) + np.linalg.norm(ulp[keep]) / tol)
-    worst = max(report, key=report.get)
-    assert report[worst] < tol, (worst, report[worst], sorted(report.items(), key=lambda t: -t[1])[:6])
+                    report[f"d{s}:{k}"] = err / (np.linalg.norm(rd[keep]) + np.linalg.norm(ulp[keep]) / tol_g)
+    # loss, h_out and parameters are gated at tol; gradients (dh_out, g*)
+    # and deltas (d*) at tol_g
+    ratio = {k: v / (tol_g if k == "dh_out" or k[0] in "gd" else tol) for k, v in report.items()}
+    worst = max(ratio, key=ratio.get)
+    assert ratio[worst] < 1.0, (worst, report[worst], sorted(report.items(), key=lambda t: -t[1])[:6])
     return report
 
 
