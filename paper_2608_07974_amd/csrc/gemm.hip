@@ -100,7 +100,10 @@ __device__ inline void tile_coords(int nbm, int nbn, int& tm, int& tn) {
     const int x = b % 8, idx = b / 8;
     b = (x < rem ? x * (per + 1) : rem * (per + 1) + (x - rem) * per) + idx;
   }
-  const int GROUP_M = 8;
+#ifndef GEMM_GROUP_M
+#define GEMM_GROUP_M 8
+#endif
+  const int GROUP_M = GEMM_GROUP_M;
   const int group = b / (GROUP_M * nbn);
   const int first_m = group * GROUP_M;
   const int gsz = min(nbm - first_m, GROUP_M);
@@ -376,6 +379,13 @@ __device__ inline i32x4_t buffer_rsrc(const void* base) {
 // transpose read) and in bits 1-2 (distinct 32-byte groups for 16 lanes).
 __device__ inline int xs(int b) { return (0xCA60 >> (4 * b)) & 15; }
 
+extern "C" __device__ i32x4_t llvm_amdgcn_raw_buffer_load_v4i32(i32x4_t rsrc, uint32_t voffset,
+                                                                 uint32_t soffset, int aux)
+    __asm("llvm.amdgcn.raw.buffer.load.v4i32");
+__device__ inline i32x4_t buffer_load16(i32x4_t rsrc, uint32_t voff) {
+  return llvm_amdgcn_raw_buffer_load_v4i32(rsrc, voff, 0, 0);
+}
+
 __device__ inline void dma16(uint32_t lds_byte, uint32_t voff, i32x4_t rsrc) {
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                :
@@ -384,11 +394,17 @@ __device__ inline void dma16(uint32_t lds_byte, uint32_t voff, i32x4_t rsrc) {
 }
 __device__ inline void dma_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
-// One operand's 64-deep k tile, R rows of M (or N), copied by NT threads.
-template <int R, int NT, bool KMAJ>
+// K-major LDS rows of BK elements: 16-B chunk c of row r sits at
+// c ^ ((r / (128 / BK)) % (BK / 8)), so the 16 lanes of one LDS cycle (16
+// consecutive rows, one chunk each) hit 16 distinct 16-byte bank groups.
+template <int BK>
+__device__ inline int kswz(int row) { return (row / (128 / BK)) % (BK / 8); }
+
+// One operand's BK-deep k tile, R rows of M (or N), copied by NT threads.
+template <int R, int BK, int NT, bool KMAJ>
 struct DmaTile {
-  static constexpr int ITEMS = R * 8 / NT;  // 16-B chunks per thread
-  static_assert(ITEMS * NT == R * 8, "tile chunks must divide over the threads");
+  static constexpr int ITEMS = R * BK / 8 / NT;  // 16-B chunks per thread
+  static_assert(ITEMS >= 1 && ITEMS * NT == R * BK / 8, "tile chunks must divide over the threads");
   uint32_t off[ITEMS];  // byte offset at k0 = 0 from the tile origin, or DMA_OOB
   int kr[ITEMS];        // k of the chunk's first element within the tile
   uint32_t kstride;     // bytes per unit of k
@@ -398,7 +414,8 @@ struct DmaTile {
     for (int j = 0; j < ITEMS; ++j) {
       const int c = (wave * ITEMS + j) * 64 + lane;
       if (KMAJ) {
-        const int row = c >> 3, ch = (c & 7) ^ ((row >> 1) & 7);
+        constexpr int CR = BK / 8;
+        const int row = c / CR, ch = (c % CR) ^ kswz<BK>(row);
         kr[j] = ch * 8;
         off[j] = row < rvalid ? (uint32_t)(row * ld) * 2u + (uint32_t)ch * 16u : DMA_OOB;
       } else {
@@ -410,6 +427,29 @@ struct DmaTile {
     }
     kstride = KMAJ ? 2u : (uint32_t)ld * 2u;
   }
+  __device__ inline uint32_t voff(int j, int k0, int kvalid) const {
+    // a row outside the tile has off = DMA_OOB, and DMA_OOB plus any
+    // in-range k advance (< 2^31) stays at or above the record count
+    return k0 + kr[j] < kvalid ? off[j] + (uint32_t)k0 * kstride : DMA_OOB;
+  }
+  // Register path: the same chunks loaded into VGPRs (zero-filled in the
+  // same way), then stored to the same contiguous LDS slots.
+  __device__ inline void load(uint4 (&r)[ITEMS], int k0, int kvalid, i32x4_t rsrc) const {
+#pragma unroll
+    for (int j = 0; j < ITEMS; ++j)
+      r[j] = __builtin_bit_cast(uint4, buffer_load16(rsrc, voff(j, k0, kvalid)));
+  }
+  __device__ inline void store(const uint4 (&r)[ITEMS], unsigned char* lds, int wave, int lane) const {
+#pragma unroll
+    for (int j = 0; j < ITEMS; ++j)
+      *reinterpret_cast<uint4*>(lds + ((wave * ITEMS + j) * 64 + lane) * 16) = r[j];
+  }
+  __device__ inline void issue_one(int j, uint32_t lds_byte, int wave, int k0, int kvalid,
+                                   i32x4_t rsrc) const {
+    dma16(lds_byte + (uint32_t)(wave * ITEMS + j) * 1024u, voff(j, k0, kvalid), rsrc);
+  }
+  // Copy the tile starting at k0 into LDS at lds_byte.  Chunks at or past
+  // kvalid (and rows outside the matrix) are zero-filled.
   __device__ inline void issue(uint32_t lds_byte, int wave, int k0, int kvalid, i32x4_t rsrc) const {
 #pragma unroll
     for (int j = 0; j < ITEMS; ++j) {
@@ -423,17 +463,19 @@ struct DmaTile {
 
 // Per-lane LDS fragment addressing of one operand for the 32x32x16 MFMA:
 // lane l supplies row (l & 31) and k 8 (l >> 5) .. +7 of the 16-deep slice.
-template <int R, int T, int F, bool KMAJ>
+template <int R, int BK, int F, bool KMAJ>
 struct FragTile {
-  static constexpr int NS = BKT / 16;
+  static constexpr int NS = BK / 16;
   static constexpr int NO = KMAJ ? NS : F;
   int off[NO];  // element offsets: per slice (K-major) or per fragment (MN-major)
 
   __device__ inline void init(int wrow, int lane) {
     if (KMAJ) {
-      const int l = lane & 31, h = lane >> 5, sw = (l >> 1) & 7;
+      // fragment rows step by 32, which keeps kswz (period 128/BK rows x
+      // BK/8 chunks <= 32 rows) unchanged: fragment i adds i * 32 * BK
+      const int l = lane & 31, h = lane >> 5, sw = kswz<BK>(l);
 #pragma unroll
-      for (int q = 0; q < NS; ++q) off[q] = (wrow + l) * BKT + (((2 * q + h) ^ sw) * 8);
+      for (int q = 0; q < NS; ++q) off[q] = (wrow + l) * BK + (((2 * q + h) ^ sw) * 8);
     } else {
       // transpose read: lane r of 16-lane group G addresses k row
       // 8 (G >> 1) + (r >> 2) (+ 16 q + 4 t) and the 4 elements at
@@ -448,7 +490,7 @@ struct FragTile {
   }
   __device__ inline bf16x8_t read(const bf16_t* tile, int q, int i) const {
     if (KMAJ) {
-      return *reinterpret_cast<const bf16x8_t*>(tile + off[q] + i * 32 * BKT);
+      return *reinterpret_cast<const bf16x8_t*>(tile + off[q] + i * 32 * BK);
     } else {
       const bf16_t* p = tile + off[i] + 16 * q * R;
       const s16x4_t x = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
@@ -460,14 +502,31 @@ struct FragTile {
   }
 };
 
-template <int BM, int BN, int WM, int WN, bool AK, bool BKM>
+// s_waitcnt with only the vector-memory count constrained (gfx9 encoding:
+// vmcnt bits [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]).
+template <int N>
+__device__ inline void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// NST-stage pipeline: the tile NST - 1 steps ahead is in flight while the
+// current one is multiplied; one barrier per BK-deep tile.
+template <int BM, int BN, int WM, int WN, int BK, int NST, int DS, bool AK, bool BKM, bool RA, bool RB>
 __global__ void __launch_bounds__(WM * WN * 64)
 gemm_dma_kernel(GemmDesc g, EpiArgs e) {
   constexpr int NT = WM * WN * 64;
   constexpr int TM = BM / WM, TN = BN / WN;
   constexpr int FM = TM / 32, FN = TN / 32;
-  constexpr int NS = BKT / 16;
-  constexpr uint32_t ABYTES = BM * BKT * 2, STAGE = (BM + BN) * BKT * 2;
+  constexpr int NS = BK / 16;
+  constexpr uint32_t ABYTES = BM * BK * 2, STAGE = (BM + BN) * BK * 2;
+  using TA = DmaTile<BM, BK, NT, AK>;
+  using TB = DmaTile<BN, BK, NT, BKM>;
+  constexpr int PER_TILE = TA::ITEMS + TB::ITEMS;  // DMA instructions per wave per tile
+  static_assert(NST >= 2 && (NST - 2) * PER_TILE < 64, "pipeline depth");
+  static_assert(!(RA || RB) || NST == 2, "register staging uses two stages");
+  static_assert(DS >= 1 && DS < NS, "the tile copy is spread over slices before the last");
+  static_assert(NS % 2 == 0, "slice parity must repeat per tile");
   extern __shared__ __align__(16) unsigned char smem[];
 
   const int nbm = (g.M + BM - 1) / BM, nbn = (g.N + BN - 1) / BN;
@@ -481,12 +540,12 @@ gemm_dma_kernel(GemmDesc g, EpiArgs e) {
   const bf16_t* B = reinterpret_cast<const bf16_t*>(g.B);
   const i32x4_t ra = buffer_rsrc(A + (AK ? (int64_t)m0 * g.lda : (int64_t)m0));
   const i32x4_t rb = buffer_rsrc(B + (BKM ? (int64_t)n0 * g.ldb : (int64_t)n0));
-  DmaTile<BM, NT, AK> da;
-  DmaTile<BN, NT, BKM> db;
+  TA da;
+  TB db;
   da.init(wave, lane, g.lda, min(g.M - m0, BM));
   db.init(wave, lane, g.ldb, min(g.N - n0, BN));
-  FragTile<BM, TM, FM, AK> fa;
-  FragTile<BN, TN, FN, BKM> fb;
+  FragTile<BM, BK, FM, AK> fa;
+  FragTile<BN, BK, FN, BKM> fb;
   fa.init(wm * TM, lane);
   fb.init(wn * TN, lane);
 
@@ -499,26 +558,37 @@ gemm_dma_kernel(GemmDesc g, EpiArgs e) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>(smem);
-  const int nk = (g.K + BKT - 1) / BKT;
-  da.issue(lds0, wave, 0, g.ka, ra);
-  db.issue(lds0 + ABYTES, wave, 0, g.kb, rb);
-  dma_wait();
+  const int nk = (g.K + BK - 1) / BK;
+  // prologue: tiles 0 .. NST-2 (tiles past K are zero-filled, never used)
+#pragma unroll
+  for (int t = 0; t < NST - 1; ++t) {
+    da.issue(lds0 + t * STAGE, wave, t * BK, g.ka, ra);
+    db.issue(lds0 + t * STAGE + ABYTES, wave, t * BK, g.kb, rb);
+  }
+  wait_vmcnt<(NST - 2) * PER_TILE>();
   __syncthreads();
-
+  // Fragments are double-buffered in registers: the LDS reads of the next
+  // k16 slice are issued before the MFMAs of the current one (scheduling
+  // fences keep that order).  The barrier that publishes tile kt+1 sits
+  // before the MFMAs of tile kt's last slice, whose fragments are already
+  // in registers, so slice 0 of tile kt+1 is read while they run and the
+  // barrier also certifies that every wave is done reading tile kt.
+  bf16x8_t af[2][FM], bfr[2][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i) af[0][i] = fa.read(reinterpret_cast<const bf16_t*>(smem), 0, i);
+#pragma unroll
+  for (int j = 0; j < FN; ++j)
+    bfr[0][j] = fb.read(reinterpret_cast<const bf16_t*>(smem) + BM * BK, 0, j);
+  int rd = 0, wr = NST - 1;  // stage read this step, stage written this step
+  uint4 rga[RA ? TA::ITEMS : 1], rgb[RB ? TB::ITEMS : 1];
   for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) {
-      const uint32_t nxt = lds0 + (cur ^ 1) * STAGE;
-      da.issue(nxt, wave, (kt + 1) * BKT, g.ka, ra);
-      db.issue(nxt + ABYTES, wave, (kt + 1) * BKT, g.kb, rb);
-    }
-    const bf16_t* as = reinterpret_cast<const bf16_t*>(smem + cur * STAGE);
-    const bf16_t* bs = as + BM * BKT;
-    bf16x8_t af[2][FM], bfr[2][FN];
-#pragma unroll
-    for (int i = 0; i < FM; ++i) af[0][i] = fa.read(as, 0, i);
-#pragma unroll
-    for (int j = 0; j < FN; ++j) bfr[0][j] = fb.read(bs, 0, j);
+    const uint32_t dst = lds0 + wr * STAGE;
+    const int k0n = (kt + NST - 1) * BK;
+    if constexpr (RA) da.load(rga, k0n, g.ka, ra);
+    if constexpr (RB) db.load(rgb, k0n, g.kb, rb);
+    const int rn = rd + 1 == NST ? 0 : rd + 1;
+    const bf16_t* as = reinterpret_cast<const bf16_t*>(smem + rd * STAGE);
+    const bf16_t* an = reinterpret_cast<const bf16_t*>(smem + rn * STAGE);
 #pragma unroll
     for (int q = 0; q < NS; ++q) {
       const int cb = q & 1, nb = cb ^ 1;
@@ -526,17 +596,43 @@ gemm_dma_kernel(GemmDesc g, EpiArgs e) {
 #pragma unroll
         for (int i = 0; i < FM; ++i) af[nb][i] = fa.read(as, q + 1, i);
 #pragma unroll
-        for (int j = 0; j < FN; ++j) bfr[nb][j] = fb.read(bs, q + 1, j);
+        for (int j = 0; j < FN; ++j) bfr[nb][j] = fb.read(as + BM * BK, q + 1, j);
+      } else {
+        wait_vmcnt<(NST - 2) * PER_TILE>();  // this wave's share of tile kt+1
+        if constexpr (RA) da.store(rga, smem + wr * STAGE, wave, lane);
+        if constexpr (RB) db.store(rgb, smem + wr * STAGE + ABYTES, wave, lane);
+        __syncthreads();                      // everyone's share; tile kt fully read
+#pragma unroll
+        for (int i = 0; i < FM; ++i) af[nb][i] = fa.read(an, 0, i);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) bfr[nb][j] = fb.read(an + BM * BK, 0, j);
       }
+      // this slice's share of the copy of tile kt+NST-1: spreading the
+      // copies keeps the vector-memory queue from stalling the MFMA issue
+      if (q < DS) {
+        constexpr int TOT = (RA ? 0 : TA::ITEMS) + (RB ? 0 : TB::ITEMS);
+        const int lo = q * TOT / DS, hi = (q + 1) * TOT / DS;
+#pragma unroll
+        for (int t = 0; t < TOT; ++t) {
+          if (t < lo || t >= hi) continue;
+          const int ta = RA ? 0 : TA::ITEMS;
+          if (t < ta) da.issue_one(t, dst, wave, k0n, g.ka, ra);
+          else db.issue_one(t - ta, dst + ABYTES, wave, k0n, g.kb, rb);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cb][i], bfr[cb][j], acc[i][j], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    dma_wait();
-    __syncthreads();
+    rd = rn;
+    wr = wr + 1 == NST ? 0 : wr + 1;
   }
+  dma_wait();  // the zero-fill copies past K must land before LDS is reused
+  __syncthreads();
   store_tile<BM, BN, WM, WN>(acc, smem, g, e, m0, n0, wave, lane);
 }
 
@@ -614,12 +710,36 @@ static const char* layout_tag(bool ak, bool bk) {
   return ak ? (bk ? "kk" : "kn") : (bk ? "mk" : "mn");
 }
 
-template <int BM, int BN, int WM, int WN, bool AK, bool BKM>
+// Main-path configuration (compile-time; overridable for tuning builds)
+#ifndef GEMM_BK
+#define GEMM_BK 64
+#endif
+#ifndef GEMM_NST
+#define GEMM_NST 2
+#endif
+#ifndef GEMM_DS
+#define GEMM_DS 1
+#endif
+#ifndef GEMM_WM
+#define GEMM_WM 4
+#endif
+#ifndef GEMM_WN
+#define GEMM_WN 2
+#endif
+#ifndef GEMM_RA
+#define GEMM_RA false
+#endif
+#ifndef GEMM_RB
+#define GEMM_RB false
+#endif
+
+template <int BM, int BN, int WM, int WN, int BK, int NST, bool AK, bool BKM>
 static hipError_t run_dma(const GemmDesc& g, const EpiArgs& e, hipStream_t s) {
-  auto kern = gemm_dma_kernel<BM, BN, WM, WN, AK, BKM>;
-  const size_t lds_main = (size_t)2 * (BM + BN) * BKT * sizeof(bf16_t);
+  auto kern = gemm_dma_kernel<BM, BN, WM, WN, BK, NST, GEMM_DS, AK, BKM, GEMM_RA, GEMM_RB>;
+  const size_t lds_main = (size_t)NST * (BM + BN) * BK * sizeof(bf16_t);
   const size_t lds_epi = (size_t)WM * WN * 32 * (BN / WN + 4) * sizeof(float);
   const size_t lds = lds_main > lds_epi ? lds_main : lds_epi;
+  static_assert((size_t)NST * (BM + BN) * BK * 2 <= 160 * 1024, "pipeline exceeds LDS");
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t err = hipFuncSetAttribute((const void*)kern,
@@ -640,8 +760,8 @@ static hipError_t run_dma(const GemmDesc& g, const EpiArgs& e, hipStream_t s) {
 static bool dma_operand_ok(const void* p, int64_t ld, bool kmaj, int rows, int kvalid, int R) {
   if (reinterpret_cast<uintptr_t>(p) % 16 != 0 || ld % 8 != 0) return false;
   const int64_t lim = (int64_t)1 << 31;
-  if (kmaj) return kvalid % 8 == 0 && ((int64_t)R * ld + kvalid + BKT) * 2 < lim;
-  return rows % 8 == 0 && ((int64_t)(kvalid + BKT) * ld + R) * 2 < lim;
+  if (kmaj) return kvalid % 8 == 0 && ((int64_t)R * ld + kvalid + 64) * 2 < lim;
+  return rows % 8 == 0 && ((int64_t)(kvalid + 64) * ld + R) * 2 < lim;
 }
 
 template <bool AK, bool BKM>
@@ -664,8 +784,8 @@ static hipError_t run_layout(const GemmDesc& g, const EpiArgs& e, int dtype, hip
     const bool dma = dma_operand_ok(g.A, g.lda, AK, g.M, g.ka, R) &&
                      dma_operand_ok(g.B, g.ldb, BKM, g.N, g.kb, R);
     if (dma) {
-      if (large) { err = run_dma<256, 256, 4, 2, AK, BKM>(g, e, s); which = 3; }
-      else { err = run_dma<128, 128, 2, 2, AK, BKM>(g, e, s); which = 4; }
+      if (large) { err = run_dma<256, 256, GEMM_WM, GEMM_WN, GEMM_BK, GEMM_NST, AK, BKM>(g, e, s); which = 3; }
+      else { err = run_dma<128, 128, 2, 2, GEMM_BK, GEMM_NST, AK, BKM>(g, e, s); which = 4; }
     } else if (large) {
       if constexpr (AK && BKM) err = run_mfma<256, 256, 4, 2, AK, BKM>(g, e, s);
       else err = run_mfma<256, 256, 2, 2, AK, BKM>(g, e, s);
