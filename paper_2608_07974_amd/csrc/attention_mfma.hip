@@ -122,19 +122,85 @@ __device__ inline void rope_back(f32x4_t (&x)[HD / 16], int r, const int32_t* po
 
 }  // namespace
 
+// ------------------------------------------------------ direct-to-LDS copy
+// Tiles of BT rows x HD are copied global -> LDS by the buffer unit (16 bytes
+// per lane; lane i's bytes land at M0 + 16 i; offsets at or above the record
+// count read as zero), into the same row-major, chunk-swizzled layout the
+// fragment readers use.
+typedef int32_t i32x4_t __attribute__((ext_vector_type(4)));
+constexpr uint32_t DMA_OOB = 0x80000000u;
+
+__device__ inline i32x4_t buffer_rsrc(const void* base) {
+  const uint64_t p = reinterpret_cast<uint64_t>(base);
+  i32x4_t r;
+  r[0] = (int32_t)(uint32_t)p;
+  r[1] = (int32_t)(uint32_t)(p >> 32);
+  r[2] = (int32_t)DMA_OOB;
+  r[3] = 0x00020000;
+  return r;
+}
+__device__ inline void dma16(uint32_t lds_byte, uint32_t voff, i32x4_t rsrc) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(lds_byte), "v"(voff), "s"(rsrc)
+               : "memory");
+}
+__device__ inline void dma_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+template <int HD, int NT>
+struct TileDma {
+  static constexpr int CH = HD / 8;              // 16-byte chunks per row
+  static constexpr int ITEMS = BT * CH / NT;     // chunks per thread
+  static_assert(ITEMS >= 1 && ITEMS * NT == BT * CH, "tile chunks must divide over the threads");
+  uint32_t off[ITEMS];  // byte offset of the chunk in row `row` of the tile at row 0
+  int row[ITEMS];
+  uint32_t ldb;         // bytes per matrix row
+  __device__ inline void init(int wave, int lane, int64_t ld) {
+#pragma unroll
+    for (int j = 0; j < ITEMS; ++j) {
+      const int c = (wave * ITEMS + j) * 64 + lane;
+      const int r = c / CH, ch = (c % CH) ^ swz<HD>(r);
+      row[j] = r;
+      off[j] = (uint32_t)(r * ld) * 2u + (uint32_t)ch * 16u;
+    }
+    ldb = (uint32_t)ld * 2u;
+  }
+  // rows r0 .. r0+BT-1 of the matrix (rows >= rvalid read as zero)
+  __device__ inline void issue(uint32_t lds_byte, int wave, int r0, int rvalid, i32x4_t rsrc) const {
+#pragma unroll
+    for (int j = 0; j < ITEMS; ++j) {
+      const uint32_t v = r0 + row[j] < rvalid ? off[j] + (uint32_t)r0 * ldb : DMA_OOB;
+      dma16(lds_byte + (uint32_t)(wave * ITEMS + j) * 1024u, v, rsrc);
+    }
+  }
+};
+
 // ------------------------------------------------------------------ forward
-template <int HD>
-__global__ void __launch_bounds__(NTH) attn_fwd_mfma(AttnDesc a) {
+// Workgroup: 8 waves; HPW q-heads of one kv group (they share every K/V
+// tile) x 256 / HPW queries; each wave owns 32 queries of one head.
+// Online softmax in the log2 domain with a lazily moved reference maximum:
+// a row's reference only moves when the running maximum exceeds it by more
+// than 8 (probabilities stay <= 2^8, exact after the final division), so
+// the O rescale is skipped on most tiles.  Causal/length masks are applied
+// only on tiles that cross the diagonal or the end of the keys.
+constexpr int FW_WAVES = 8;
+constexpr int FW_NT = FW_WAVES * 64;
+constexpr float RESCALE_TAU = 8.f;
+
+template <int HD, int HPW>
+__global__ void __launch_bounds__(FW_NT) attn_fwd_mfma(AttnDesc a) {
+  constexpr int QW = FW_WAVES / HPW;   // query sub-blocks of 32 per head
+  constexpr int QB = QW * 32;          // queries per workgroup
+  constexpr uint32_t TB = BT * HD * 2; // bytes of one K or V tile
   extern __shared__ __align__(16) unsigned char smem[];
-  bf16_t* Ks = reinterpret_cast<bf16_t*>(smem);     // [2][BT * HD]
-  bf16_t* Vs = Ks + 2 * BT * HD;                    // [2][BT * HD]
-  const int qb = gridDim.x - 1 - blockIdx.x;        // longest causal rows first
-  const int h = blockIdx.y, b = blockIdx.z;
-  const int kvh = h / (a.Hq / a.Hkv);
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int qb = gridDim.x - 1 - blockIdx.x;  // longest causal rows first
+  const int hb = blockIdx.y * HPW, b = blockIdx.z;
+  const int kvh = hb / (a.Hq / a.Hkv);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int c = lane & 15, g = lane >> 4;
+  const int h = hb + wave % HPW;
+  const int q0 = qb * QB, qw0 = q0 + (wave / HPW) * 32;
   const int L = a.seq_lens[b];
-  const int q0 = qb * BW;
   const int64_t rowb = (int64_t)b * a.S;
   const bf16_t* Q = reinterpret_cast<const bf16_t*>(a.q);
   const bf16_t* K = reinterpret_cast<const bf16_t*>(a.k);
@@ -146,7 +212,7 @@ __global__ void __launch_bounds__(NTH) attn_fwd_mfma(AttnDesc a) {
   float m[2], lsum[2];
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
-    qi[j] = q0 + wave * 32 + j * 16 + c;
+    qi[j] = qw0 + j * 16 + c;
 #pragma unroll
     for (int kk = 0; kk < HD / 32; ++kk)
       qf[j][kk] = qi[j] < a.S ? *reinterpret_cast<const bf16x8_t*>(Q + (rowb + qi[j]) * a.ldq +
@@ -158,25 +224,32 @@ __global__ void __launch_bounds__(NTH) attn_fwd_mfma(AttnDesc a) {
     lsum[j] = 0.f;
   }
   const float cs = a.scale * LOG2E;
-  const int kend = min(min(q0 + BW, a.S), L);
+  const int kend = min(min(q0 + QB, a.S), L);        // keys any query here may see
+  const int kend_w = min(min(qw0 + 32, a.S), L);     // keys this wave's queries may see
   const int nt = (kend + BT - 1) / BT;
 
-  TileStage<HD> sk, sv;
+  const i32x4_t rk = buffer_rsrc(K + rowb * a.ldk + (int64_t)kvh * HD);
+  const i32x4_t rv = buffer_rsrc(V + rowb * a.ldv + (int64_t)kvh * HD);
+  TileDma<HD, FW_NT> dk, dv;
+  dk.init(wave, lane, a.ldk);
+  dv.init(wave, lane, a.ldv);
+  const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>(smem);  // [2][K | V]
   if (nt > 0) {
-    sk.load(K, a.ldk, rowb, 0, kend, (int64_t)kvh * HD);
-    sv.load(V, a.ldv, rowb, 0, kend, (int64_t)kvh * HD);
-    sk.store(Ks);
-    sv.store(Vs);
+    dk.issue(lds0, wave, 0, kend, rk);
+    dv.issue(lds0 + TB, wave, 0, kend, rv);
   }
-  __syncthreads();
   for (int t = 0; t < nt; ++t) {
     const int k0 = t * BT;
-    const bf16_t* kt = Ks + (t & 1) * BT * HD;
-    const bf16_t* vt = Vs + (t & 1) * BT * HD;
+    dma_wait();
+    __syncthreads();  // tile t everywhere; the other stage is no longer read
     if (t + 1 < nt) {
-      sk.load(K, a.ldk, rowb, k0 + BT, kend, (int64_t)kvh * HD);
-      sv.load(V, a.ldv, rowb, k0 + BT, kend, (int64_t)kvh * HD);
+      const uint32_t nxt = lds0 + ((t + 1) & 1) * 2 * TB;
+      dk.issue(nxt, wave, k0 + BT, kend, rk);
+      dv.issue(nxt + TB, wave, k0 + BT, kend, rv);
     }
+    if (k0 >= kend_w) continue;  // past every key this wave's queries see
+    const bf16_t* kt = reinterpret_cast<const bf16_t*>(smem + (t & 1) * 2 * TB);
+    const bf16_t* vt = kt + BT * HD;
     f32x4_t s[2][4];
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) {
@@ -189,36 +262,51 @@ __global__ void __launch_bounds__(NTH) attn_fwd_mfma(AttnDesc a) {
         s[1][blk] = mfma16(kf, qf[1][kk], s[1][blk]);
       }
     }
+    // some key of the tile lies after some query of the wave, or past kend
+    const bool masked = k0 + BT - 1 > qw0 || k0 + BT > kend;
     bf16x8_t pf[2][2];
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
+      float x[4][4];
       float tmax = -INFINITY;
 #pragma unroll
       for (int blk = 0; blk < 4; ++blk)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int key = k0 + blk * 16 + 4 * g + r;
-          const float v = (key < kend && key <= qi[j]) ? s[j][blk][r] * cs : -INFINITY;
-          s[j][blk][r] = v;
-          tmax = fmaxf(tmax, v);
-        }
+        for (int r = 0; r < 4; ++r) x[blk][r] = s[j][blk][r] * cs;
+      if (masked) {
+#pragma unroll
+        for (int blk = 0; blk < 4; ++blk)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int key = k0 + blk * 16 + 4 * g + r;
+            x[blk][r] = (key <= qi[j] && key < kend) ? x[blk][r] : -INFINITY;
+          }
+      }
+#pragma unroll
+      for (int blk = 0; blk < 4; ++blk)
+        tmax = fmaxf(tmax, fmaxf(fmaxf(x[blk][0], x[blk][1]), fmaxf(x[blk][2], x[blk][3])));
       tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
       tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-      const float mnew = fmaxf(m[j], tmax);
-      const float alpha = mnew == -INFINITY ? 1.f : exp2f(m[j] - mnew);
+      const bool move = tmax > m[j] + RESCALE_TAU;
+      if (__any(move)) {
+        const float mnew = move ? tmax : m[j];
+        const float alpha = move ? (m[j] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m[j] - mnew)) : 1.f;
+        m[j] = mnew;
+        lsum[j] *= alpha;
+#pragma unroll
+        for (int db = 0; db < HD / 16; ++db) o[j][db] *= alpha;
+      }
+      const float ms = m[j] == -INFINITY ? 0.f : m[j];
       float psum = 0.f;
 #pragma unroll
       for (int blk = 0; blk < 4; ++blk)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float p = s[j][blk][r] == -INFINITY ? 0.f : exp2f(s[j][blk][r] - mnew);
+          const float p = __builtin_amdgcn_exp2f(x[blk][r] - ms);
           psum += p;
-          pf[j][blk >> 1][(blk & 1) * 4 + r] = to_bf16(p);
+          pf[j][blk >> 1][(blk & 1) * 4 + r] = (__bf16)p;
         }
-      lsum[j] = lsum[j] * alpha + psum;
-      m[j] = mnew;
-#pragma unroll
-      for (int db = 0; db < HD / 16; ++db) o[j][db] *= alpha;
+      lsum[j] += psum;
     }
 #pragma unroll
     for (int db = 0; db < HD / 16; ++db)
@@ -228,12 +316,8 @@ __global__ void __launch_bounds__(NTH) attn_fwd_mfma(AttnDesc a) {
         o[0][db] = mfma16(vf, pf[0][kk], o[0][db]);
         o[1][db] = mfma16(vf, pf[1][kk], o[1][db]);
       }
-    if (t + 1 < nt) {
-      sk.store(Ks + ((t + 1) & 1) * BT * HD);
-      sv.store(Vs + ((t + 1) & 1) * BT * HD);
-    }
-    __syncthreads();
   }
+  dma_wait();
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     float ls = lsum[j];
@@ -542,18 +626,27 @@ static hipError_t set_lds(Kern kern, size_t bytes) {
                              (int)bytes);
 }
 
-template <int HD>
-static hipError_t fwd(const AttnDesc& a, hipStream_t s) {
-  const size_t lds = (size_t)4 * BT * HD * sizeof(bf16_t);
+template <int HD, int HPW>
+static hipError_t fwd_hpw(const AttnDesc& a, hipStream_t s) {
+  const size_t lds = (size_t)4 * BT * HD * sizeof(bf16_t);  // 2 stages x (K + V)
   static bool once = false;
   if (!once) {
-    hipError_t e = set_lds(attn_fwd_mfma<HD>, lds);
+    hipError_t e = set_lds(attn_fwd_mfma<HD, HPW>, lds);
     if (e != hipSuccess) return e;
     once = true;
   }
-  dim3 grid((a.S + BW - 1) / BW, a.Hq, a.B);
-  hipLaunchKernelGGL(attn_fwd_mfma<HD>, grid, dim3(NTH), lds, s, a);
+  constexpr int QB = (FW_WAVES / HPW) * 32;
+  dim3 grid((a.S + QB - 1) / QB, a.Hq / HPW, a.B);
+  hipLaunchKernelGGL((attn_fwd_mfma<HD, HPW>), grid, dim3(FW_NT), lds, s, a);
   return hipGetLastError();
+}
+
+template <int HD>
+static hipError_t fwd(const AttnDesc& a, hipStream_t s) {
+  const int grp = a.Hq / a.Hkv;
+  if (grp % 4 == 0) return fwd_hpw<HD, 4>(a, s);
+  if (grp % 2 == 0) return fwd_hpw<HD, 2>(a, s);
+  return fwd_hpw<HD, 1>(a, s);
 }
 
 template <int HD>
@@ -588,6 +681,9 @@ static bool mfma_ok(const AttnDesc& a) {
   for (int64_t l : lds)
     if (l % 8) return false;
   const uintptr_t p = (uintptr_t)a.q | (uintptr_t)a.k | (uintptr_t)a.v | (uintptr_t)a.o;
+  // K/V tiles are copied with 32-bit byte offsets from the batch row origin
+  const int64_t lim = (int64_t)1 << 31;
+  if (((int64_t)a.S + BT) * a.ldk * 2 >= lim || ((int64_t)a.S + BT) * a.ldv * 2 >= lim) return false;
   return p % 16 == 0;
 }
 
