@@ -150,26 +150,23 @@ __device__ inline void dma_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memor
 template <int HD, int NT>
 struct TileDma {
   static constexpr int CH = HD / 8;              // 16-byte chunks per row
+  static constexpr int RPI = 64 / CH;            // rows per copy instruction
   static constexpr int ITEMS = BT * CH / NT;     // chunks per thread
   static_assert(ITEMS >= 1 && ITEMS * NT == BT * CH, "tile chunks must divide over the threads");
-  uint32_t off[ITEMS];  // byte offset of the chunk in row `row` of the tile at row 0
-  int row[ITEMS];
-  uint32_t ldb;         // bytes per matrix row
-  __device__ inline void init(int wave, int lane, int64_t ld) {
-#pragma unroll
-    for (int j = 0; j < ITEMS; ++j) {
-      const int c = (wave * ITEMS + j) * 64 + lane;
-      const int r = c / CH, ch = (c % CH) ^ swz<HD>(r);
-      row[j] = r;
-      off[j] = (uint32_t)(r * ld) * 2u + (uint32_t)ch * 16u;
-    }
+  int rl, cl;       // lane's row within an instruction's rows, and its chunk
+  uint32_t ldb;     // bytes per matrix row
+  __device__ inline void init(int lane, int64_t ld) {
+    rl = lane / CH;
+    cl = lane % CH;
     ldb = (uint32_t)ld * 2u;
   }
   // rows r0 .. r0+BT-1 of the matrix (rows >= rvalid read as zero)
   __device__ inline void issue(uint32_t lds_byte, int wave, int r0, int rvalid, i32x4_t rsrc) const {
 #pragma unroll
     for (int j = 0; j < ITEMS; ++j) {
-      const uint32_t v = r0 + row[j] < rvalid ? off[j] + (uint32_t)r0 * ldb : DMA_OOB;
+      const int row = (wave * ITEMS + j) * RPI + rl;  // tile row this lane's chunk lands in
+      const int ch = cl ^ swz<HD>(row);               // source chunk for that LDS slot
+      const uint32_t v = r0 + row < rvalid ? (uint32_t)(r0 + row) * ldb + (uint32_t)ch * 16u : DMA_OOB;
       dma16(lds_byte + (uint32_t)(wave * ITEMS + j) * 1024u, v, rsrc);
     }
   }
@@ -231,8 +228,8 @@ __global__ void __launch_bounds__(FW_NT) attn_fwd_mfma(AttnDesc a) {
   const i32x4_t rk = buffer_rsrc(K + rowb * a.ldk + (int64_t)kvh * HD);
   const i32x4_t rv = buffer_rsrc(V + rowb * a.ldv + (int64_t)kvh * HD);
   TileDma<HD, FW_NT> dk, dv;
-  dk.init(wave, lane, a.ldk);
-  dv.init(wave, lane, a.ldv);
+  dk.init(lane, a.ldk);
+  dv.init(lane, a.ldv);
   const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>(smem);  // [2][K | V]
   if (nt > 0) {
     dk.issue(lds0, wave, 0, kend, rk);
@@ -360,19 +357,31 @@ __global__ void __launch_bounds__(256) attn_delta_mfma(AttnDesc a) {
 }
 
 // ------------------------------------------------------------------- dK dV
+// One workgroup per (128 keys, kv-head): 8 waves = 4 key groups of 32 x 2
+// sets.  The (q-head, query tile) pairs of the kv group are split between
+// the sets by parity; each set's Q and dO tiles are copied direct-to-LDS.
+// At the end the two sets' partial dK/dV are added through LDS in a fixed
+// order, so the result does not depend on timing.
+constexpr int KV_WAVES = 8;
+constexpr int KV_NT = KV_WAVES * 64;
+
 template <int HD>
-__global__ void __launch_bounds__(NTH) attn_dkv_mfma(AttnDesc a) {
+__global__ void __launch_bounds__(KV_NT) attn_dkv_mfma(AttnDesc a) {
+  constexpr uint32_t TB = BT * HD * 2;     // one Q or dO tile
+  constexpr uint32_t SET = 2 * TB;         // Q | dO of one set
+  constexpr uint32_t STAGE = 2 * SET;      // both sets
+  constexpr uint32_t STAT0 = 2 * STAGE;    // [stage][set][lse2 64 | delta 64] floats
   extern __shared__ __align__(16) unsigned char smem[];
-  bf16_t* Qs = reinterpret_cast<bf16_t*>(smem);     // [2][BT * HD]
-  bf16_t* Ds = Qs + 2 * BT * HD;                    // [2][BT * HD]
-  float* stat = reinterpret_cast<float*>(Ds + 2 * BT * HD);  // [2][lse2 64 | delta 64]
-  const int kblk = blockIdx.x;                      // early keys see the most queries: first
+  float* stat = reinterpret_cast<float*>(smem + STAT0);
+  const int kblk = blockIdx.x;             // early keys see the most queries: first
   const int kvh = blockIdx.y, b = blockIdx.z;
   const int grp = a.Hq / a.Hkv;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int kw = wave & 3, set = wave >> 2;
   const int c = lane & 15, g = lane >> 4;
   const int L = a.seq_lens[b];
   const int k0 = kblk * BW;
+  const int kw0 = k0 + kw * 32;
   const int klim = min(a.S, L);
   const int64_t rowb = (int64_t)b * a.S;
   const bf16_t* Q = reinterpret_cast<const bf16_t*>(a.q);
@@ -385,7 +394,7 @@ __global__ void __launch_bounds__(NTH) attn_dkv_mfma(AttnDesc a) {
   f32x4_t dk[2][HD / 16], dv[2][HD / 16];
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
-    kj[j] = k0 + wave * 32 + j * 16 + c;
+    kj[j] = kw0 + j * 16 + c;
 #pragma unroll
     for (int kk = 0; kk < HD / 32; ++kk) {
       const int64_t off = (int64_t)kvh * HD + 8 * g + 32 * kk;
@@ -399,124 +408,179 @@ __global__ void __launch_bounds__(NTH) attn_dkv_mfma(AttnDesc a) {
     }
   }
   const float cs = a.scale * LOG2E;
-  // (q-head, query tile) pairs in order; a key block's query tiles start at k0
+  // (q-head, query tile) pairs; a key block's query tiles start at k0
   const int ntq = k0 < klim ? (a.S - k0 + BT - 1) / BT : 0;
-  const int nt = grp * ntq;
-  TileStage<HD> sq, sd;
-  float st_l = 0.f, st_d = 0.f;
-  auto issue = [&](int t) {
-    const int h = kvh * grp + t / ntq;
-    const int q0 = k0 + (t % ntq) * BT;
-    sq.load(Q, a.ldq, rowb, q0, a.S, (int64_t)h * HD);
-    sd.load(DO, a.lddo, rowb, q0, a.S, (int64_t)h * HD);
-    if (threadIdx.x < BT) {
-      const int q = q0 + threadIdx.x;
-      const int64_t so = ((int64_t)b * a.Hq + h) * a.S;
-      st_l = q < a.S ? a.lse[so + q] * LOG2E : -INFINITY;
-      st_d = q < a.S ? a.delta[so + q] : 0.f;
-    }
-  };
-  auto commit = [&](int buf) {
-    sq.store(Qs + buf * BT * HD);
-    sd.store(Ds + buf * BT * HD);
-    if (threadIdx.x < BT) {
-      stat[buf * 2 * BT + threadIdx.x] = st_l;
-      stat[buf * 2 * BT + BT + threadIdx.x] = st_d;
-    }
-  };
-  if (nt > 0) {
-    issue(0);
-    commit(0);
-  }
-  __syncthreads();
-  for (int t = 0; t < nt; ++t) {
-    const int buf = t & 1;
-    const int q0 = k0 + (t % ntq) * BT;
-    const bf16_t* qt = Qs + buf * BT * HD;
-    const bf16_t* dt = Ds + buf * BT * HD;
-    const float* l2s = stat + buf * 2 * BT;
-    const float* dls = l2s + BT;
-    if (t + 1 < nt) issue(t + 1);
-    bf16x8_t pk[2][2], dsk[2][2];
-#pragma unroll
-    for (int qb = 0; qb < 4; ++qb) {
-      f32x4_t s[2], dp[2];
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        s[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        dp[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const int npair = grp * ntq;
+  const int nit = (npair + 1) / 2;  // iteration i: set 0 takes pair 2i, set 1 pair 2i+1
+
+  // copy engines: each set's 4 waves (256 threads) copy that set's tiles
+  TileDma<HD, KV_NT / 2> dq_, dd_;
+  dq_.init(lane, a.ldq);
+  dd_.init(lane, a.lddo);
+  const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>(smem);
+  const int64_t so_b = (int64_t)b * a.Hq * a.S;
+  float st_l = 0.f, st_d = 0.f;  // statistic of query (tile row kw*64+lane) held until stored
+  auto issue = [&](int it) {
+    const int pr = 2 * it + set;
+    if (pr < npair) {
+      const int h = kvh * grp + pr / ntq;
+      const int q0 = k0 + (pr % ntq) * BT;
+      const uint32_t dst = lds0 + (it & 1) * STAGE + set * SET;
+      const i32x4_t rq = buffer_rsrc(Q + rowb * a.ldq + (int64_t)h * HD);
+      const i32x4_t rd = buffer_rsrc(DO + rowb * a.lddo + (int64_t)h * HD);
+      dq_.issue(dst, kw, q0, a.S, rq);
+      dd_.issue(dst + TB, kw, q0, a.S, rd);
+      if (kw == 0) {
+        const int q = q0 + lane;
+        const int64_t so = so_b + (int64_t)h * a.S;
+        const float lse = q < a.S ? a.lse[so + q] : -INFINITY;
+        st_l = lse == -INFINITY ? INFINITY : lse * LOG2E;  // p = 0 for such queries
+        st_d = q < a.S ? a.delta[so + q] : 0.f;
       }
+    }
+  };
+  auto commit = [&](int it) {
+    if (kw == 0 && 2 * it + set < npair) {
+      float* sp = stat + ((it & 1) * 2 + set) * 2 * BT;
+      sp[lane] = st_l;
+      sp[BT + lane] = st_d;
+    }
+  };
+  issue(0);
+  commit(0);
+  for (int it = 0; it < nit; ++it) {
+    dma_wait();
+    __syncthreads();  // pair tiles of iteration it everywhere; the other stage is free
+    if (it + 1 < nit) issue(it + 1);
+    const int pr = 2 * it + set;
+    if (pr < npair) {
+      const int q0 = k0 + (pr % ntq) * BT;
+      const bf16_t* qt = reinterpret_cast<const bf16_t*>(smem + (it & 1) * STAGE + set * SET);
+      const bf16_t* dt = qt + BT * HD;
+      const float* l2s = stat + ((it & 1) * 2 + set) * 2 * BT;
+      const float* dls = l2s + BT;
+      // some key of the wave lies after some query of the tile, or keys or
+      // queries run past their ends
+      const bool masked = kw0 + 31 > q0 || q0 + BT > a.S || kw0 + 32 > klim;
 #pragma unroll
-      for (int kk = 0; kk < HD / 32; ++kk) {
-        const bf16x8_t qa = frag_row<HD>(qt, qb * 16 + c, g + 4 * kk);
-        const bf16x8_t da = frag_row<HD>(dt, qb * 16 + c, g + 4 * kk);
+      for (int half = 0; half < 2; ++half) {
+        bf16x8_t pk[2], dsk[2];
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          s[j] = mfma16(qa, kf[j][kk], s[j]);
-          dp[j] = mfma16(da, vf[j][kk], dp[j]);
+        for (int qq = 0; qq < 2; ++qq) {
+          const int qb = 2 * half + qq;
+          f32x4_t sc[2], dp[2];
+#pragma unroll
+          for (int j = 0; j < 2; ++j) {
+            sc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            dp[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+          }
+#pragma unroll
+          for (int kk = 0; kk < HD / 32; ++kk) {
+            const bf16x8_t qa = frag_row<HD>(qt, qb * 16 + c, g + 4 * kk);
+            const bf16x8_t da = frag_row<HD>(dt, qb * 16 + c, g + 4 * kk);
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+              sc[j] = mfma16(qa, kf[j][kk], sc[j]);
+              dp[j] = mfma16(da, vf[j][kk], dp[j]);
+            }
+          }
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int ql = qb * 16 + 4 * g + r;
+            const float l2 = l2s[ql], dl = dls[ql];
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+              float x = sc[j][r] * cs - l2;
+              if (masked) {
+                const int q = q0 + ql;
+                x = (kj[j] <= q && q < a.S && kj[j] < klim) ? x : -INFINITY;
+              }
+              const float p = __builtin_amdgcn_exp2f(x);
+              pk[j][qq * 4 + r] = (__bf16)p;
+              dsk[j][qq * 4 + r] = (__bf16)(p * (dp[j][r] - dl));
+            }
+          }
+        }
+        // dV += P^T dO, dK += dS^T Q over this half's 32 queries
+#pragma unroll
+        for (int db = 0; db < HD / 16; ++db) {
+          const bf16x8_t dob = frag_col<HD>(dt, 32 * half, g, 16 * db, c);
+          const bf16x8_t qbv = frag_col<HD>(qt, 32 * half, g, 16 * db, c);
+#pragma unroll
+          for (int j = 0; j < 2; ++j) {
+            dv[j][db] = mfma16(pk[j], dob, dv[j][db]);
+            dk[j][db] = mfma16(dsk[j], qbv, dk[j][db]);
+          }
         }
       }
+    }
+    commit(it + 1);
+  }
+  dma_wait();
+  __syncthreads();
+  // combine the sets: set 1 hands its dK to set 0, set 0 its dV to set 1
+  float* xk = reinterpret_cast<float*>(smem);                         // [4 waves][HD/16][2][4][64]
+  float* xv = xk + 4 * (HD / 16) * 2 * 4 * 64;
+  auto slot = [&](float* base, int db, int j, int r) -> float& {
+    return base[(((kw * (HD / 16) + db) * 2 + j) * 4 + r) * 64 + lane];
+  };
+#pragma unroll
+  for (int db = 0; db < HD / 16; ++db)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int ql = qb * 16 + 4 * g + r;
-        const int q = q0 + ql;
-        const float l2 = l2s[ql], dl = dls[ql];
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const bool ok = q < a.S && kj[j] <= q && kj[j] < klim && l2 != -INFINITY;
-          const float p = ok ? exp2f(s[j][r] * cs - l2) : 0.f;
-          pk[j][qb >> 1][(qb & 1) * 4 + r] = to_bf16(p);
-          dsk[j][qb >> 1][(qb & 1) * 4 + r] = to_bf16(p * (dp[j][r] - dl));
-        }
+        if (set == 1) slot(xk, db, j, r) = dk[j][db][r];
+        else slot(xv, db, j, r) = dv[j][db][r];
       }
-    }
-#pragma unroll
-    for (int db = 0; db < HD / 16; ++db)
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-        const bf16x8_t dob = frag_col<HD>(dt, 32 * kk, g, 16 * db, c);
-        const bf16x8_t qbv = frag_col<HD>(qt, 32 * kk, g, 16 * db, c);
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          dv[j][db] = mfma16(pk[j][kk], dob, dv[j][db]);
-          dk[j][db] = mfma16(dsk[j][kk], qbv, dk[j][db]);
-        }
-      }
-    if (t + 1 < nt) commit((t + 1) & 1);
-    __syncthreads();
-  }
+  __syncthreads();
   bf16_t* DK = reinterpret_cast<bf16_t*>(a.dk);
   bf16_t* DV = reinterpret_cast<bf16_t*>(a.dv);
 #pragma unroll
   for (int j = 0; j < 2; ++j)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int key = k0 + wave * 32 + j * 16 + 4 * g + r;
-      if (key < a.S) {
-        if (a.rope) rope_back<HD>(dk[j], r, a.pos, rowb + key, a.rope, a.max_pos, c);
+      const int key = kw0 + j * 16 + 4 * g + r;
+      if (set == 0) {
 #pragma unroll
-        for (int db = 0; db < HD / 16; ++db) {
-          const int64_t col = (int64_t)kvh * HD + db * 16 + c;
-          DK[(rowb + key) * a.lddk + col] = f32_to_bf16(dk[j][db][r] * a.scale);
-          DV[(rowb + key) * a.lddv + col] = f32_to_bf16(dv[j][db][r]);
+        for (int db = 0; db < HD / 16; ++db) dk[j][db][r] += slot(xk, db, j, r);
+        if (key < a.S) {
+          if (a.rope) rope_back<HD>(dk[j], r, a.pos, rowb + key, a.rope, a.max_pos, c);
+#pragma unroll
+          for (int db = 0; db < HD / 16; ++db)
+            DK[(rowb + key) * a.lddk + (int64_t)kvh * HD + db * 16 + c] = f32_to_bf16(dk[j][db][r] * a.scale);
+        }
+      } else {
+#pragma unroll
+        for (int db = 0; db < HD / 16; ++db) dv[j][db][r] = slot(xv, db, j, r) + dv[j][db][r];
+        if (key < a.S) {
+#pragma unroll
+          for (int db = 0; db < HD / 16; ++db)
+            DV[(rowb + key) * a.lddv + (int64_t)kvh * HD + db * 16 + c] = f32_to_bf16(dv[j][db][r]);
         }
       }
     }
 }
 
 // ----------------------------------------------------------------------- dQ
-template <int HD>
-__global__ void __launch_bounds__(NTH) attn_dq_mfma(AttnDesc a) {
+// Same decomposition as the forward: 8 waves, HPW q-heads of one kv group
+// share every K/V tile (direct-to-LDS copy); each wave owns 32 queries.
+// dS = P (dP - delta) with P recomputed from the saved log-sum-exp; masks
+// only on tiles crossing the diagonal or the end of the keys.
+template <int HD, int HPW>
+__global__ void __launch_bounds__(FW_NT) attn_dq_mfma(AttnDesc a) {
+  constexpr int QW = FW_WAVES / HPW;
+  constexpr int QB = QW * 32;
+  constexpr uint32_t TB = BT * HD * 2;
   extern __shared__ __align__(16) unsigned char smem[];
-  bf16_t* Ks = reinterpret_cast<bf16_t*>(smem);     // [2][BT * HD]
-  bf16_t* Vs = Ks + 2 * BT * HD;                    // [2][BT * HD]
   const int qblk = gridDim.x - 1 - blockIdx.x;
-  const int h = blockIdx.y, b = blockIdx.z;
-  const int kvh = h / (a.Hq / a.Hkv);
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int hb = blockIdx.y * HPW, b = blockIdx.z;
+  const int kvh = hb / (a.Hq / a.Hkv);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int c = lane & 15, g = lane >> 4;
+  const int h = hb + wave % HPW;
+  const int q0 = qblk * QB, qw0 = q0 + (wave / HPW) * 32;
   const int L = a.seq_lens[b];
-  const int q0 = qblk * BW;
   const int64_t rowb = (int64_t)b * a.S;
   const bf16_t* Q = reinterpret_cast<const bf16_t*>(a.q);
   const bf16_t* K = reinterpret_cast<const bf16_t*>(a.k);
@@ -529,38 +593,50 @@ __global__ void __launch_bounds__(NTH) attn_dq_mfma(AttnDesc a) {
   f32x4_t dq[2][HD / 16];
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
-    qi[j] = q0 + wave * 32 + j * 16 + c;
+    qi[j] = qw0 + j * 16 + c;
+    const bool ok = qi[j] < a.S;
 #pragma unroll
     for (int kk = 0; kk < HD / 32; ++kk) {
       const int64_t col = (int64_t)h * HD + 8 * g + 32 * kk;
-      qf[j][kk] = qi[j] < a.S ? *reinterpret_cast<const bf16x8_t*>(Q + (rowb + qi[j]) * a.ldq + col) : zero8();
-      df[j][kk] = qi[j] < a.S ? *reinterpret_cast<const bf16x8_t*>(DO + (rowb + qi[j]) * a.lddo + col) : zero8();
+      qf[j][kk] = ok ? *reinterpret_cast<const bf16x8_t*>(Q + (rowb + qi[j]) * a.ldq + col) : zero8();
+      df[j][kk] = ok ? *reinterpret_cast<const bf16x8_t*>(DO + (rowb + qi[j]) * a.lddo + col) : zero8();
     }
     const int64_t so = ((int64_t)b * a.Hq + h) * a.S + qi[j];
-    l2[j] = qi[j] < a.S ? a.lse[so] * LOG2E : -INFINITY;
-    dl[j] = qi[j] < a.S ? a.delta[so] : 0.f;
+    const float lse = ok ? a.lse[so] : -INFINITY;
+    // a query with no key (or outside the sequence) gets +inf: every p = 0
+    l2[j] = lse == -INFINITY ? INFINITY : lse * LOG2E;
+    dl[j] = ok ? a.delta[so] : 0.f;
 #pragma unroll
     for (int i = 0; i < HD / 16; ++i) dq[j][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   }
   const float cs = a.scale * LOG2E;
-  const int kend = min(min(q0 + BW, a.S), L);
+  const int kend = min(min(q0 + QB, a.S), L);
+  const int kend_w = min(min(qw0 + 32, a.S), L);
   const int nt = (kend + BT - 1) / BT;
-  TileStage<HD> sk, sv;
+
+  const i32x4_t rk = buffer_rsrc(K + rowb * a.ldk + (int64_t)kvh * HD);
+  const i32x4_t rv = buffer_rsrc(V + rowb * a.ldv + (int64_t)kvh * HD);
+  TileDma<HD, FW_NT> dkm, dvm;
+  dkm.init(lane, a.ldk);
+  dvm.init(lane, a.ldv);
+  const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>(smem);  // [2][K | V]
   if (nt > 0) {
-    sk.load(K, a.ldk, rowb, 0, kend, (int64_t)kvh * HD);
-    sv.load(V, a.ldv, rowb, 0, kend, (int64_t)kvh * HD);
-    sk.store(Ks);
-    sv.store(Vs);
+    dkm.issue(lds0, wave, 0, kend, rk);
+    dvm.issue(lds0 + TB, wave, 0, kend, rv);
   }
-  __syncthreads();
   for (int t = 0; t < nt; ++t) {
     const int k0 = t * BT;
-    const bf16_t* kt = Ks + (t & 1) * BT * HD;
-    const bf16_t* vt = Vs + (t & 1) * BT * HD;
+    dma_wait();
+    __syncthreads();
     if (t + 1 < nt) {
-      sk.load(K, a.ldk, rowb, k0 + BT, kend, (int64_t)kvh * HD);
-      sv.load(V, a.ldv, rowb, k0 + BT, kend, (int64_t)kvh * HD);
+      const uint32_t nxt = lds0 + ((t + 1) & 1) * 2 * TB;
+      dkm.issue(nxt, wave, k0 + BT, kend, rk);
+      dvm.issue(nxt + TB, wave, k0 + BT, kend, rv);
     }
+    if (k0 >= kend_w) continue;
+    const bf16_t* kt = reinterpret_cast<const bf16_t*>(smem + (t & 1) * 2 * TB);
+    const bf16_t* vt = kt + BT * HD;
+    const bool masked = k0 + BT - 1 > qw0 || k0 + BT > kend;
     bf16x8_t dsk[2][2];
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) {
@@ -584,10 +660,13 @@ __global__ void __launch_bounds__(NTH) attn_dq_mfma(AttnDesc a) {
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int key = k0 + blk * 16 + 4 * g + r;
-          const bool ok = key < kend && key <= qi[j] && l2[j] != -INFINITY;
-          const float p = ok ? exp2f(st[j][r] * cs - l2[j]) : 0.f;
-          dsk[j][blk >> 1][(blk & 1) * 4 + r] = to_bf16(p * (dpt[j][r] - dl[j]));
+          float x = st[j][r] * cs - l2[j];
+          if (masked) {
+            const int key = k0 + blk * 16 + 4 * g + r;
+            x = (key <= qi[j] && key < kend) ? x : -INFINITY;
+          }
+          const float p = __builtin_amdgcn_exp2f(x);
+          dsk[j][blk >> 1][(blk & 1) * 4 + r] = (__bf16)(p * (dpt[j][r] - dl[j]));
         }
     }
 #pragma unroll
@@ -598,18 +677,14 @@ __global__ void __launch_bounds__(NTH) attn_dq_mfma(AttnDesc a) {
         dq[0][db] = mfma16(dsk[0][kk], kb, dq[0][db]);
         dq[1][db] = mfma16(dsk[1][kk], kb, dq[1][db]);
       }
-    if (t + 1 < nt) {
-      sk.store(Ks + ((t + 1) & 1) * BT * HD);
-      sv.store(Vs + ((t + 1) & 1) * BT * HD);
-    }
-    __syncthreads();
   }
+  dma_wait();
   bf16_t* DQ = reinterpret_cast<bf16_t*>(a.dq);
 #pragma unroll
   for (int j = 0; j < 2; ++j)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int q = q0 + wave * 32 + j * 16 + 4 * g + r;
+      const int q = qw0 + j * 16 + 4 * g + r;
       if (q < a.S) {
         if (a.rope) rope_back<HD>(dq[j], r, a.pos, rowb + q, a.rope, a.max_pos, c);
 #pragma unroll
@@ -649,14 +724,31 @@ static hipError_t fwd(const AttnDesc& a, hipStream_t s) {
   return fwd_hpw<HD, 1>(a, s);
 }
 
+template <int HD, int HPW>
+static hipError_t dq_hpw(const AttnDesc& a, hipStream_t s) {
+  const size_t lds = (size_t)4 * BT * HD * sizeof(bf16_t);  // 2 stages x (K + V)
+  static bool once = false;
+  if (!once) {
+    hipError_t e = set_lds(attn_dq_mfma<HD, HPW>, lds);
+    if (e != hipSuccess) return e;
+    once = true;
+  }
+  constexpr int QB = (FW_WAVES / HPW) * 32;
+  dim3 grid((a.S + QB - 1) / QB, a.Hq / HPW, a.B);
+  hipLaunchKernelGGL((attn_dq_mfma<HD, HPW>), grid, dim3(FW_NT), lds, s, a);
+  return hipGetLastError();
+}
+
 template <int HD>
 static hipError_t bwd(const AttnDesc& a, hipStream_t s) {
-  const size_t lds_kv = (size_t)4 * BT * HD * sizeof(bf16_t) + 4 * BT * sizeof(float);
-  const size_t lds_q = (size_t)4 * BT * HD * sizeof(bf16_t);
+  // 2 stages x 2 sets x (Q + dO) tiles + statistics; the final combine
+  // reuses the start of it for 2 x 4 waves x HD/2 x 64 floats
+  const size_t lds_tiles = (size_t)8 * BT * HD * sizeof(bf16_t) + 8 * BT * sizeof(float);
+  const size_t lds_comb = (size_t)2 * 4 * (HD / 2) * 64 * sizeof(float);
+  const size_t lds_kv = lds_tiles > lds_comb ? lds_tiles : lds_comb;
   static bool once = false;
   if (!once) {
     hipError_t e = set_lds(attn_dkv_mfma<HD>, lds_kv);
-    if (e == hipSuccess) e = set_lds(attn_dq_mfma<HD>, lds_q);
     if (e != hipSuccess) return e;
     once = true;
   }
@@ -666,12 +758,13 @@ static hipError_t bwd(const AttnDesc& a, hipStream_t s) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 gk((a.S + BW - 1) / BW, a.Hkv, a.B);
-  hipLaunchKernelGGL(attn_dkv_mfma<HD>, gk, dim3(NTH), lds_kv, s, a);
+  hipLaunchKernelGGL(attn_dkv_mfma<HD>, gk, dim3(KV_NT), lds_kv, s, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  dim3 gq((a.S + BW - 1) / BW, a.Hq, a.B);
-  hipLaunchKernelGGL(attn_dq_mfma<HD>, gq, dim3(NTH), lds_q, s, a);
-  return hipGetLastError();
+  const int grp = a.Hq / a.Hkv;
+  if (grp % 4 == 0) return dq_hpw<HD, 4>(a, s);
+  if (grp % 2 == 0) return dq_hpw<HD, 2>(a, s);
+  return dq_hpw<HD, 1>(a, s);
 }
 
 static bool mfma_ok(const AttnDesc& a) {
