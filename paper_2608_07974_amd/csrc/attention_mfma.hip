@@ -357,209 +357,147 @@ __global__ void __launch_bounds__(256) attn_delta_mfma(AttnDesc a) {
 }
 
 // ------------------------------------------------------------------- dK dV
-// One workgroup per (128 keys, kv-head): 8 waves = 4 key groups of 32 x 2
-// sets.  The (q-head, query tile) pairs of the kv group are split between
-// the sets by parity; each set's Q and dO tiles are copied direct-to-LDS.
-// At the end the two sets' partial dK/dV are added through LDS in a fixed
-// order, so the result does not depend on timing.
+// One workgroup per (128 keys, kv-head): 8 waves of 16 keys walk every
+// (q-head, query tile) pair of the kv group; the pair's Q and dO tiles are
+// copied direct-to-LDS once for all waves.  16 keys per wave keeps the K/V
+// fragments and the fp32 dK/dV accumulators within two waves per SIMD.
 constexpr int KV_WAVES = 8;
 constexpr int KV_NT = KV_WAVES * 64;
 
 template <int HD>
 __global__ void __launch_bounds__(KV_NT) attn_dkv_mfma(AttnDesc a) {
   constexpr uint32_t TB = BT * HD * 2;     // one Q or dO tile
-  constexpr uint32_t SET = 2 * TB;         // Q | dO of one set
-  constexpr uint32_t STAGE = 2 * SET;      // both sets
-  constexpr uint32_t STAT0 = 2 * STAGE;    // [stage][set][lse2 64 | delta 64] floats
+  constexpr uint32_t STAGE = 2 * TB;       // Q | dO
+  constexpr uint32_t STAT0 = 2 * STAGE;    // [stage][lse2 64 | delta 64] floats
   extern __shared__ __align__(16) unsigned char smem[];
   float* stat = reinterpret_cast<float*>(smem + STAT0);
   const int kblk = blockIdx.x;             // early keys see the most queries: first
   const int kvh = blockIdx.y, b = blockIdx.z;
   const int grp = a.Hq / a.Hkv;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
-  const int kw = wave & 3, set = wave >> 2;
   const int c = lane & 15, g = lane >> 4;
   const int L = a.seq_lens[b];
   const int k0 = kblk * BW;
-  const int kw0 = k0 + kw * 32;
+  const int kw0 = k0 + wave * 16;
   const int klim = min(a.S, L);
+  const int kj = kw0 + c;
   const int64_t rowb = (int64_t)b * a.S;
   const bf16_t* Q = reinterpret_cast<const bf16_t*>(a.q);
   const bf16_t* K = reinterpret_cast<const bf16_t*>(a.k);
   const bf16_t* V = reinterpret_cast<const bf16_t*>(a.v);
   const bf16_t* DO = reinterpret_cast<const bf16_t*>(a.dout);
 
-  int kj[2];
-  bf16x8_t kf[2][HD / 32], vf[2][HD / 32];
-  f32x4_t dk[2][HD / 16], dv[2][HD / 16];
+  bf16x8_t kf[HD / 32], vf[HD / 32];
+  f32x4_t dk[HD / 16], dv[HD / 16];
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    kj[j] = kw0 + j * 16 + c;
+  for (int kk = 0; kk < HD / 32; ++kk) {
+    const int64_t off = (int64_t)kvh * HD + 8 * g + 32 * kk;
+    kf[kk] = kj < klim ? *reinterpret_cast<const bf16x8_t*>(K + (rowb + kj) * a.ldk + off) : zero8();
+    vf[kk] = kj < klim ? *reinterpret_cast<const bf16x8_t*>(V + (rowb + kj) * a.ldv + off) : zero8();
+  }
 #pragma unroll
-    for (int kk = 0; kk < HD / 32; ++kk) {
-      const int64_t off = (int64_t)kvh * HD + 8 * g + 32 * kk;
-      kf[j][kk] = kj[j] < klim ? *reinterpret_cast<const bf16x8_t*>(K + (rowb + kj[j]) * a.ldk + off) : zero8();
-      vf[j][kk] = kj[j] < klim ? *reinterpret_cast<const bf16x8_t*>(V + (rowb + kj[j]) * a.ldv + off) : zero8();
-    }
-#pragma unroll
-    for (int i = 0; i < HD / 16; ++i) {
-      dk[j][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-      dv[j][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    }
+  for (int i = 0; i < HD / 16; ++i) {
+    dk[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    dv[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   }
   const float cs = a.scale * LOG2E;
   // (q-head, query tile) pairs; a key block's query tiles start at k0
   const int ntq = k0 < klim ? (a.S - k0 + BT - 1) / BT : 0;
   const int npair = grp * ntq;
-  const int nit = (npair + 1) / 2;  // iteration i: set 0 takes pair 2i, set 1 pair 2i+1
 
-  // copy engines: each set's 4 waves (256 threads) copy that set's tiles
-  TileDma<HD, KV_NT / 2> dq_, dd_;
+  TileDma<HD, KV_NT> dq_, dd_;
   dq_.init(lane, a.ldq);
   dd_.init(lane, a.lddo);
   const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>(smem);
   const int64_t so_b = (int64_t)b * a.Hq * a.S;
-  float st_l = 0.f, st_d = 0.f;  // statistic of query (tile row kw*64+lane) held until stored
-  auto issue = [&](int it) {
-    const int pr = 2 * it + set;
-    if (pr < npair) {
-      const int h = kvh * grp + pr / ntq;
-      const int q0 = k0 + (pr % ntq) * BT;
-      const uint32_t dst = lds0 + (it & 1) * STAGE + set * SET;
-      const i32x4_t rq = buffer_rsrc(Q + rowb * a.ldq + (int64_t)h * HD);
-      const i32x4_t rd = buffer_rsrc(DO + rowb * a.lddo + (int64_t)h * HD);
-      dq_.issue(dst, kw, q0, a.S, rq);
-      dd_.issue(dst + TB, kw, q0, a.S, rd);
-      if (kw == 0) {
-        const int q = q0 + lane;
-        const int64_t so = so_b + (int64_t)h * a.S;
-        const float lse = q < a.S ? a.lse[so + q] : -INFINITY;
-        st_l = lse == -INFINITY ? INFINITY : lse * LOG2E;  // p = 0 for such queries
-        st_d = q < a.S ? a.delta[so + q] : 0.f;
-      }
+  float st_l = 0.f, st_d = 0.f;  // statistics of query (tile row lane), wave 0
+  auto issue = [&](int pr) {
+    const int h = kvh * grp + pr / ntq;
+    const int q0 = k0 + (pr % ntq) * BT;
+    const uint32_t dst = lds0 + (pr & 1) * STAGE;
+    dq_.issue(dst, wave, q0, a.S, buffer_rsrc(Q + rowb * a.ldq + (int64_t)h * HD));
+    dd_.issue(dst + TB, wave, q0, a.S, buffer_rsrc(DO + rowb * a.lddo + (int64_t)h * HD));
+    if (wave == 0) {
+      const int q = q0 + lane;
+      const int64_t so = so_b + (int64_t)h * a.S;
+      const float lse = q < a.S ? a.lse[so + q] : -INFINITY;
+      st_l = lse == -INFINITY ? INFINITY : lse * LOG2E;  // p = 0 for such queries
+      st_d = q < a.S ? a.delta[so + q] : 0.f;
     }
   };
-  auto commit = [&](int it) {
-    if (kw == 0 && 2 * it + set < npair) {
-      float* sp = stat + ((it & 1) * 2 + set) * 2 * BT;
+  auto commit = [&](int pr) {
+    if (wave == 0) {
+      float* sp = stat + (pr & 1) * 2 * BT;
       sp[lane] = st_l;
       sp[BT + lane] = st_d;
     }
   };
-  issue(0);
-  commit(0);
-  for (int it = 0; it < nit; ++it) {
+  if (npair > 0) {
+    issue(0);
+    commit(0);
+  }
+  for (int pr = 0; pr < npair; ++pr) {
     dma_wait();
-    __syncthreads();  // pair tiles of iteration it everywhere; the other stage is free
-    if (it + 1 < nit) issue(it + 1);
-    const int pr = 2 * it + set;
-    if (pr < npair) {
-      const int q0 = k0 + (pr % ntq) * BT;
-      const bf16_t* qt = reinterpret_cast<const bf16_t*>(smem + (it & 1) * STAGE + set * SET);
-      const bf16_t* dt = qt + BT * HD;
-      const float* l2s = stat + ((it & 1) * 2 + set) * 2 * BT;
-      const float* dls = l2s + BT;
-      // some key of the wave lies after some query of the tile, or keys or
-      // queries run past their ends
-      const bool masked = kw0 + 31 > q0 || q0 + BT > a.S || kw0 + 32 > klim;
+    __syncthreads();  // tiles of pair pr everywhere; the other stage is free
+    if (pr + 1 < npair) issue(pr + 1);
+    const int q0 = k0 + (pr % ntq) * BT;
+    const bf16_t* qt = reinterpret_cast<const bf16_t*>(smem + (pr & 1) * STAGE);
+    const bf16_t* dt = qt + BT * HD;
+    const float* l2s = stat + (pr & 1) * 2 * BT;
+    const float* dls = l2s + BT;
+    // some key of the wave lies after some query of the tile, or keys or
+    // queries run past their ends
+    const bool masked = kw0 + 15 > q0 || q0 + BT > a.S || kw0 + 16 > klim;
 #pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        bf16x8_t pk[2], dsk[2];
+    for (int half = 0; half < 2; ++half) {
+      bf16x8_t pk, dsk;
 #pragma unroll
-        for (int qq = 0; qq < 2; ++qq) {
-          const int qb = 2 * half + qq;
-          f32x4_t sc[2], dp[2];
+      for (int qq = 0; qq < 2; ++qq) {
+        const int qb = 2 * half + qq;
+        f32x4_t sc = f32x4_t{0.f, 0.f, 0.f, 0.f}, dp = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int j = 0; j < 2; ++j) {
-            sc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-            dp[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-          }
-#pragma unroll
-          for (int kk = 0; kk < HD / 32; ++kk) {
-            const bf16x8_t qa = frag_row<HD>(qt, qb * 16 + c, g + 4 * kk);
-            const bf16x8_t da = frag_row<HD>(dt, qb * 16 + c, g + 4 * kk);
-#pragma unroll
-            for (int j = 0; j < 2; ++j) {
-              sc[j] = mfma16(qa, kf[j][kk], sc[j]);
-              dp[j] = mfma16(da, vf[j][kk], dp[j]);
-            }
-          }
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int ql = qb * 16 + 4 * g + r;
-            const float l2 = l2s[ql], dl = dls[ql];
-#pragma unroll
-            for (int j = 0; j < 2; ++j) {
-              float x = sc[j][r] * cs - l2;
-              if (masked) {
-                const int q = q0 + ql;
-                x = (kj[j] <= q && q < a.S && kj[j] < klim) ? x : -INFINITY;
-              }
-              const float p = __builtin_amdgcn_exp2f(x);
-              pk[j][qq * 4 + r] = (__bf16)p;
-              dsk[j][qq * 4 + r] = (__bf16)(p * (dp[j][r] - dl));
-            }
-          }
+        for (int kk = 0; kk < HD / 32; ++kk) {
+          sc = mfma16(frag_row<HD>(qt, qb * 16 + c, g + 4 * kk), kf[kk], sc);
+          dp = mfma16(frag_row<HD>(dt, qb * 16 + c, g + 4 * kk), vf[kk], dp);
         }
-        // dV += P^T dO, dK += dS^T Q over this half's 32 queries
 #pragma unroll
-        for (int db = 0; db < HD / 16; ++db) {
-          const bf16x8_t dob = frag_col<HD>(dt, 32 * half, g, 16 * db, c);
-          const bf16x8_t qbv = frag_col<HD>(qt, 32 * half, g, 16 * db, c);
-#pragma unroll
-          for (int j = 0; j < 2; ++j) {
-            dv[j][db] = mfma16(pk[j], dob, dv[j][db]);
-            dk[j][db] = mfma16(dsk[j], qbv, dk[j][db]);
+        for (int r = 0; r < 4; ++r) {
+          const int ql = qb * 16 + 4 * g + r;
+          float x = sc[r] * cs - l2s[ql];
+          if (masked) {
+            const int q = q0 + ql;
+            x = (kj <= q && q < a.S && kj < klim) ? x : -INFINITY;
           }
+          const float p = __builtin_amdgcn_exp2f(x);
+          pk[qq * 4 + r] = (__bf16)p;
+          dsk[qq * 4 + r] = (__bf16)(p * (dp[r] - dls[ql]));
         }
+      }
+      // dV += P^T dO, dK += dS^T Q over this half's 32 queries
+#pragma unroll
+      for (int db = 0; db < HD / 16; ++db) {
+        dv[db] = mfma16(pk, frag_col<HD>(dt, 32 * half, g, 16 * db, c), dv[db]);
+        dk[db] = mfma16(dsk, frag_col<HD>(qt, 32 * half, g, 16 * db, c), dk[db]);
       }
     }
-    commit(it + 1);
+    if (pr + 1 < npair) commit(pr + 1);
   }
   dma_wait();
-  __syncthreads();
-  // combine the sets: set 1 hands its dK to set 0, set 0 its dV to set 1
-  float* xk = reinterpret_cast<float*>(smem);                         // [4 waves][HD/16][2][4][64]
-  float* xv = xk + 4 * (HD / 16) * 2 * 4 * 64;
-  auto slot = [&](float* base, int db, int j, int r) -> float& {
-    return base[(((kw * (HD / 16) + db) * 2 + j) * 4 + r) * 64 + lane];
-  };
-#pragma unroll
-  for (int db = 0; db < HD / 16; ++db)
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        if (set == 1) slot(xk, db, j, r) = dk[j][db][r];
-        else slot(xv, db, j, r) = dv[j][db][r];
-      }
-  __syncthreads();
   bf16_t* DK = reinterpret_cast<bf16_t*>(a.dk);
   bf16_t* DV = reinterpret_cast<bf16_t*>(a.dv);
 #pragma unroll
-  for (int j = 0; j < 2; ++j)
+  for (int r = 0; r < 4; ++r) {
+    const int key = kw0 + 4 * g + r;
+    if (key < a.S) {
+      if (a.rope) rope_back<HD>(dk, r, a.pos, rowb + key, a.rope, a.max_pos, c);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int key = kw0 + j * 16 + 4 * g + r;
-      if (set == 0) {
-#pragma unroll
-        for (int db = 0; db < HD / 16; ++db) dk[j][db][r] += slot(xk, db, j, r);
-        if (key < a.S) {
-          if (a.rope) rope_back<HD>(dk[j], r, a.pos, rowb + key, a.rope, a.max_pos, c);
-#pragma unroll
-          for (int db = 0; db < HD / 16; ++db)
-            DK[(rowb + key) * a.lddk + (int64_t)kvh * HD + db * 16 + c] = f32_to_bf16(dk[j][db][r] * a.scale);
-        }
-      } else {
-#pragma unroll
-        for (int db = 0; db < HD / 16; ++db) dv[j][db][r] = slot(xv, db, j, r) + dv[j][db][r];
-        if (key < a.S) {
-#pragma unroll
-          for (int db = 0; db < HD / 16; ++db)
-            DV[(rowb + key) * a.lddv + (int64_t)kvh * HD + db * 16 + c] = f32_to_bf16(dv[j][db][r]);
-        }
+      for (int db = 0; db < HD / 16; ++db) {
+        const int64_t col = (int64_t)kvh * HD + db * 16 + c;
+        DK[(rowb + key) * a.lddk + col] = f32_to_bf16(dk[db][r] * a.scale);
+        DV[(rowb + key) * a.lddv + col] = f32_to_bf16(dv[db][r]);
       }
     }
+  }
 }
 
 // ----------------------------------------------------------------------- dQ
@@ -741,11 +679,8 @@ static hipError_t dq_hpw(const AttnDesc& a, hipStream_t s) {
 
 template <int HD>
 static hipError_t bwd(const AttnDesc& a, hipStream_t s) {
-  // 2 stages x 2 sets x (Q + dO) tiles + statistics; the final combine
-  // reuses the start of it for 2 x 4 waves x HD/2 x 64 floats
-  const size_t lds_tiles = (size_t)8 * BT * HD * sizeof(bf16_t) + 8 * BT * sizeof(float);
-  const size_t lds_comb = (size_t)2 * 4 * (HD / 2) * 64 * sizeof(float);
-  const size_t lds_kv = lds_tiles > lds_comb ? lds_tiles : lds_comb;
+  // 2 stages x (Q + dO) tiles + 2 stages x (lse, delta) of 64 queries
+  const size_t lds_kv = (size_t)4 * BT * HD * sizeof(bf16_t) + 4 * BT * sizeof(float);
   static bool once = false;
   if (!once) {
     hipError_t e = set_lds(attn_dkv_mfma<HD>, lds_kv);
