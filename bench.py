@@ -75,11 +75,52 @@ def cpu_baseline(shp, alpha, seconds_hint=30.0):
     except AttributeError:
         cores = os.cpu_count()
     threads = int(os.environ.get("OMP_NUM_THREADS", cores) or cores)
+    try:
+        blas = np.show_config(mode="dicts")["Build Dependencies"]["blas"]["name"]
+    except Exception:  # numpy without the dict form
+        blas = "unknown"
     return {"value": S / t_full, "unit": "tokens/s", "cores": min(cores, threads), "kind": "oracle",
+            "blas": blas,
             "sample": (f"fp64 NumPy oracle, one update of 1 of {shp.n_layers} layers at full "
                        f"width with the full head and AdamW, B=1 S={S} ({t_slice:.1f} s, head "
                        f"{t_head:.1f} s); scaled to the {shp.n_layers}-layer chunk as "
                        f"t_head + L*t_layer = {t_full:.1f} s per {S} tokens")}
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+GEMM_SOURCE = os.path.join(ROOT, "paper_2608_07974_amd", "csrc", "gemm.hip")
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` from the committed counter runs
+    (FETCH_SIZE + WRITE_SIZE, scaled by a plain-copy calibration), or None if
+    none were taken for this kernel and workload or its source has changed
+    since."""
+    import hashlib
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+        with open(GEMM_SOURCE, "rb") as f:
+            sha = hashlib.sha256(f.read()).hexdigest()
+    except OSError:
+        return None
+    for r in rec.get("kernels", []):
+        if r["kernel"] == kernel and r["workload"] == workload and r["source_sha256"] == sha:
+            return r["hbm_bytes_per_launch"]
+    return None
+
+
+def copy_calibration(nbytes=1 << 30, reps=3):
+    """A plain device-to-device copy of known size, for scaling the
+    FETCH_SIZE / WRITE_SIZE counters (profiled separately)."""
+    import torch
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": nbytes, "reps": reps}))
 
 
 def main():
@@ -91,7 +132,12 @@ def main():
     ap.add_argument("--alpha", type=float, default=0.5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-json", default=None, help="write the per-kernel profile here")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a 1 GiB device copy (counter calibration) and exit")
     args = ap.parse_args()
+    if args.copy_calibration:
+        copy_calibration()
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py: this build runs one chunk on one GPU; --gpus {args.gpus} "
@@ -174,6 +220,7 @@ def main():
         achieved = dom["bytes"] / (dom["total_ms"] / 1e3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None}
+    roof["traffic"] = measured_traffic(dom["name"], shp.name)
     roof["kernel"] = dom["name"]
     roof["launches_per_step"] = dom["launches"] / args.steps
     roof["avg_launch_ms"] = round(per_launch_ms, 4)
@@ -208,6 +255,7 @@ def main():
                    "global_batch": B, "seq_len": S, "tokens_per_step": T,
                    "alpha": args.alpha, "optimizer": "adamw", "parallelism": "none (1 GPU)"},
         "mfma_util_pct": round(mfma_pct, 2),
+        "device": dict(zl.zl_device_info(0), peak_bf16_tflops_used=PEAK_BF16_TFLOPS),
         "algorithmic_tflop_per_step": round(flops / 1e12, 2),
         "flop_split": {k: round(v / flops, 4) for k, v in parts.items()},
         "ms_per_step_min": round(min(step_ms), 3),

@@ -77,6 +77,12 @@ typedef struct zl_profile_entry {
 zl_status zl_profile_begin(zl_chunk* chunk, int capacity);
 zl_status zl_profile_end(zl_chunk* chunk, zl_profile_entry* out, int* n);
 
+/* Properties of HIP device `device` that throughput figures are priced
+ * against: compute-unit count, peak shader clock (kHz) and the gfx
+ * architecture name (NUL-terminated, truncated to arch_len - 1 bytes).
+ * Any output pointer may be NULL.  ZL_ERR_HIP if the device query fails. */
+zl_status zl_device_info(int device, int* cu_count, int* clock_khz, char* arch, int arch_len);
+
 #ifdef __cplusplus
 }
 #endif

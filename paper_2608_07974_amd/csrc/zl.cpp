@@ -854,6 +854,18 @@ zl_status zl_profile_end(zl_chunk* c, zl_profile_entry* out, int* n) {
   return ZL_OK;
 }
 
+zl_status zl_device_info(int device, int* cu_count, int* clock_khz, char* arch, int arch_len) {
+  hipDeviceProp_t prop;
+  ZL_HIP(hipGetDeviceProperties(&prop, device));
+  if (cu_count) *cu_count = prop.multiProcessorCount;
+  if (clock_khz) *clock_khz = prop.clockRate;
+  if (arch && arch_len > 0) {
+    strncpy(arch, prop.gcnArchName, (size_t)arch_len - 1);
+    arch[arch_len - 1] = 0;
+  }
+  return ZL_OK;
+}
+
 zl_status zl_kernel_gemm(int M, int N, int K, const void* A, int64_t lda, int a_kmajor,
                          const void* B, int64_t ldb, int b_kmajor, float* C, int64_t ldc,
                          int dtype, void* stream) {

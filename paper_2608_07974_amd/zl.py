@@ -22,7 +22,7 @@ EXPORTED = [
     "zl_refresh_shadow", "zl_chunk_forward", "zl_local_objective", "zl_chunk_backward",
     "zl_optimizer_step", "zl_chunk_update", "zl_get_step", "zl_set_step",
     "zl_status_string", "zl_last_error", "zl_inspect", "zl_kernel_gemm", "zl_kernel_attention",
-    "zl_profile_begin", "zl_profile_end",
+    "zl_profile_begin", "zl_profile_end", "zl_device_info",
 ]
 
 
@@ -104,6 +104,7 @@ def load(path=None):
                                 c, c, vp],
         "zl_profile_begin": [vp, c],
         "zl_profile_end": [vp, P(zl_profile_entry), P(c)],
+        "zl_device_info": [c, P(c), P(c), ctypes.c_char_p, c],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -225,6 +226,15 @@ def zl_kernel_attention(B, S, Hq, Hkv, hd, q, k, v, ld_qkv, seq_lens, o, lse, do
 
 def zl_profile_begin(h, capacity=4096):
     _check(load().zl_profile_begin(h, capacity), "zl_profile_begin")
+
+
+def zl_device_info(device=0):
+    """Returns dict(cu_count, clock_khz, arch) of HIP device `device`."""
+    cu, clk = ctypes.c_int(0), ctypes.c_int(0)
+    arch = ctypes.create_string_buffer(64)
+    _check(load().zl_device_info(device, ctypes.byref(cu), ctypes.byref(clk), arch, 64),
+           "zl_device_info")
+    return dict(cu_count=cu.value, clock_khz=clk.value, arch=arch.value.decode())
 
 
 def zl_profile_end(h, max_entries=256):
