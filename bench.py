@@ -123,6 +123,95 @@ def copy_calibration(nbytes=1 << 30, reps=3):
     print(json.dumps({"copy_calibration_bytes": nbytes, "reps": reps}))
 
 
+def pipeline_bench(args):
+    """K chunks of `--config` chained as a stage pipeline on one GPU (one
+    stream per stage, early forwarding, update window `--window`) against
+    the same chunks run one after another on one stream.  One JSON line."""
+    import numpy as np
+    import torch
+
+    import workload
+    from paper_2608_07974_amd import zl
+    from paper_2608_07974_amd.chunk import TorchChunk, config_from_shape
+    from paper_2608_07974_amd.pipeline import Pipeline
+
+    shp = workload.get_config(args.config)
+    K, W = args.pipeline, args.window
+    B, S, T = shp.batch, shp.seq, shp.batch * shp.seq
+    dev = torch.device("cuda:0")
+    torch.manual_seed(0)
+    cfg = config_from_shape(shp, alpha=args.alpha)
+    pipe = Pipeline([cfg] * K, window=W, depth=2, device=dev)
+    head = (pipe.chunks[0].head_w, pipe.chunks[0].head_norm_w, pipe.chunks[0].head_norm_b)
+    head[0].normal_(0.0, 0.02)
+    for ch in pipe.chunks:
+        ch.master.normal_(0.0, 0.02)
+        for t in ch.layout:
+            v = ch.view(ch.master, f"L{t['layer']}.{t['name']}")
+            if t["name"].startswith("ln") and t["name"].endswith("_w"):
+                v.fill_(1.0)
+            elif len(t["shape"]) == 1:
+                v.zero_()
+        zl.zl_refresh_shadow(ch.handle, torch.cuda.current_stream().cuda_stream)
+    tokens = workload.zipf_tokens(B, S, shp.vocab, seed=1) if shp.vocab > 256 else \
+        workload.uniform_tokens(B, S, shp.vocab, seed=1)
+    labels = torch.tensor(workload.labels_from_tokens(tokens), device=dev)
+    table = torch.empty(shp.vocab, shp.d_model, dtype=pipe.dtype, device=dev).normal_(0.0, 0.02)
+    h0 = table[torch.tensor(tokens, device=dev, dtype=torch.long)].contiguous()
+    del table
+    torch.cuda.synchronize()
+
+    def timed(run, n):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        run(n)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / n
+
+    losses = torch.zeros(K, dtype=torch.float32, device=dev)
+
+    def run_pipe(n):
+        for _ in range(n):
+            pipe.submit(h0, labels, losses=losses)
+        pipe.sync()
+
+    run_pipe(args.warmup * W)
+    t_pipe = timed(run_pipe, args.steps * W)
+    # the same chunks, sequentially on one stream (no early forwarding)
+    outs = [torch.empty_like(h0) for _ in range(K)]
+    count = [0]
+
+    def run_seq(n):
+        for _ in range(n):
+            h = h0
+            i = count[0]
+            for k, ch in enumerate(pipe.chunks):
+                h = ch.forward(h, h_out=outs[k])
+                ch.objective(labels)
+                ch.backward(1.0 / W, 0 if i % W == 0 else 1)
+                if i % W == W - 1:
+                    ch.step()
+            count[0] += 1
+
+    run_seq(args.warmup * W)
+    t_seq = timed(run_seq, args.steps * W)
+    flops, _ = algorithmic_flops(shp, T, S, args.alpha)
+    out = {"metric": "stage-pipeline tokens/sec on 1 MI355X (K chunks, early forwarding)",
+           "value": round(T / t_pipe, 1), "unit": "tokens/s", "n_gpus": 1,
+           "ms_per_microbatch": round(t_pipe * 1e3, 3),
+           "sequential_tokens_per_s": round(T / t_seq, 1),
+           "sequential_ms_per_microbatch": round(t_seq * 1e3, 3),
+           "speedup_vs_sequential": round(t_seq / t_pipe, 4),
+           "mfma_util_pct": round(100.0 * K * flops / t_pipe / (PEAK_BF16_TFLOPS * 1e12), 2),
+           "config": {"workload": f"{K} x {shp.name} chunks ({K * shp.n_layers} layers)",
+                      "global_batch": B, "seq_len": S, "window": W, "depth": 2,
+                      "alpha": args.alpha},
+           "steps": args.steps * W, "warmup": args.warmup * W, "dtype": "bf16",
+           "data": "synthetic (Zipf(1.1) token ids, random-init N(0,0.02) weights)"}
+    print(json.dumps(out))
+    pipe.close()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -134,9 +223,18 @@ def main():
     ap.add_argument("--profile-json", default=None, help="write the per-kernel profile here")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (counter calibration) and exit")
+    ap.add_argument("--pipeline", type=int, default=0,
+                    help="K > 0: time K chunks as a stage pipeline instead (one JSON line)")
+    ap.add_argument("--window", type=int, default=1, help="update window (with --pipeline)")
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.pipeline > 0:
+        if args.gpus != 1:
+            print("bench.py: --pipeline runs on one GPU", file=sys.stderr)
+            sys.exit(2)
+        pipeline_bench(args)
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:

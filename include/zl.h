@@ -192,6 +192,13 @@ zl_status zl_chunk_update(zl_chunk* chunk, const void* h_in,
 zl_status zl_get_step(const zl_chunk* chunk, int64_t* step);
 zl_status zl_set_step(zl_chunk* chunk, int64_t step);
 
+/* The configuration and buffer pointers the chunk was created with (copies;
+ * the chunk keeps its own).  ZL_ERR_INVALID_ARG on NULL arguments. */
+zl_status zl_chunk_get_config(const zl_chunk* chunk, zl_config* out);
+zl_status zl_chunk_get_buffers(const zl_chunk* chunk, zl_buffers* out);
+/* Number of trainable parameters (length of master / grad / adam_m / adam_v). */
+zl_status zl_chunk_num_params(const zl_chunk* chunk, size_t* n_params);
+
 const char* zl_status_string(zl_status s);
 const char* zl_last_error(void);
 

@@ -35,7 +35,10 @@ def config_from_shape(shp, alpha=0.5, consis="reverse", optimizer="adamw", lr=1e
 
 
 class TorchChunk:
-    def __init__(self, cfg, device="cuda"):
+    """`head`: optional (head_w, head_norm_w, head_norm_b) device tensors to
+    share with other chunks (the frozen head is read-only)."""
+
+    def __init__(self, cfg, device="cuda", head=None):
         zl.load()
         self.cfg = cfg
         self.device = torch.device(device)
@@ -50,9 +53,13 @@ class TorchChunk:
         self.adam_m = torch.zeros(n, dtype=torch.float32, device=dev) if adam else None
         self.adam_v = torch.zeros(n, dtype=torch.float32, device=dev) if adam else None
         d, V = cfg.d_model, cfg.vocab
-        self.head_w = torch.zeros(V, d, dtype=self.dtype, device=dev)
-        self.head_norm_w = torch.ones(d, dtype=torch.float32, device=dev)
-        self.head_norm_b = torch.zeros(d, dtype=torch.float32, device=dev) if cfg.arch == zl.ZL_ARCH_GPT2 else None
+        if head is not None:
+            self.head_w, self.head_norm_w, self.head_norm_b = head
+        else:
+            self.head_w = torch.zeros(V, d, dtype=self.dtype, device=dev)
+            self.head_norm_w = torch.ones(d, dtype=torch.float32, device=dev)
+            self.head_norm_b = (torch.zeros(d, dtype=torch.float32, device=dev)
+                                if cfg.arch == zl.ZL_ARCH_GPT2 else None)
         self.ws_bytes = zl.zl_workspace_size(cfg)
         self._ws = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=dev)
         self.ws_ptr = (self._ws.data_ptr() + 255) // 256 * 256
@@ -133,6 +140,14 @@ class TorchChunk:
         zl.zl_chunk_update(self.handle, _ptr(h_in), _ptr(seq_lens), _ptr(pos_ids), _ptr(labels),
                            B, S, _ptr(h_out), _ptr(self.loss), current_stream())
         return h_out
+
+    def save(self, path, microbatches=0, windows=0):
+        """Checkpoint parameters, optimizer state and step (after the stream's work)."""
+        zl.zl_chunk_save(self.handle, path, microbatches, windows, current_stream())
+
+    def restore(self, path):
+        """Load a checkpoint; returns its (microbatches, windows) progress."""
+        return zl.zl_chunk_load(self.handle, path, current_stream())
 
     def inspect(self, name, layer=0):
         """Copy of a workspace view as a float64 numpy array."""

@@ -23,6 +23,7 @@
 
 #include "../../include/zl.h"
 #include "../../include/zl_inspect.h"
+#include "internal.h"
 #include "common.h"
 
 using namespace zl;
@@ -459,6 +460,38 @@ zl_status zl_set_step(zl_chunk* c, int64_t step) {
   if (!c) return fail(ZL_ERR_INVALID_ARG, "chunk is NULL");
   if (step < 0) return fail(ZL_ERR_INVALID_ARG, "step must be >= 0");
   c->step = step;
+  return ZL_OK;
+}
+
+}  // extern "C"
+
+namespace zl {
+zl_status set_error(zl_status s, const std::string& msg) { return fail(s, msg); }
+bool chunk_at_boundary(const zl_chunk* c) { return c->state == ST_IDLE && !c->has_grad; }
+void chunk_close_window(zl_chunk* c) {
+  c->state = ST_IDLE;
+  c->has_grad = false;
+  c->grad_fresh = true;
+}
+}  // namespace zl
+
+extern "C" {
+
+zl_status zl_chunk_get_config(const zl_chunk* c, zl_config* out) {
+  if (!c || !out) return fail(ZL_ERR_INVALID_ARG, "NULL argument");
+  *out = c->cfg;
+  return ZL_OK;
+}
+
+zl_status zl_chunk_get_buffers(const zl_chunk* c, zl_buffers* out) {
+  if (!c || !out) return fail(ZL_ERR_INVALID_ARG, "NULL argument");
+  *out = c->buf;
+  return ZL_OK;
+}
+
+zl_status zl_chunk_num_params(const zl_chunk* c, size_t* n) {
+  if (!c || !n) return fail(ZL_ERR_INVALID_ARG, "NULL argument");
+  *n = c->layout.n_params;
   return ZL_OK;
 }
 

@@ -23,6 +23,10 @@ EXPORTED = [
     "zl_optimizer_step", "zl_chunk_update", "zl_get_step", "zl_set_step",
     "zl_status_string", "zl_last_error", "zl_inspect", "zl_kernel_gemm", "zl_kernel_attention",
     "zl_profile_begin", "zl_profile_end", "zl_device_info",
+    "zl_chunk_get_config", "zl_chunk_get_buffers", "zl_chunk_num_params",
+    "zl_pipeline_entry_bytes", "zl_pipeline_create", "zl_pipeline_submit", "zl_pipeline_read_output",
+    "zl_pipeline_sync", "zl_pipeline_progress", "zl_pipeline_checkpoint", "zl_pipeline_destroy",
+    "zl_chunk_save", "zl_chunk_load", "zl_checkpoint_read_info",
 ]
 
 
@@ -60,6 +64,15 @@ class zl_buffers(ctypes.Structure):
 class zl_view(ctypes.Structure):
     _fields_ = [("ptr", ctypes.c_void_p), ("rows", ctypes.c_int64), ("cols", ctypes.c_int64),
                 ("ld", ctypes.c_int64), ("dtype", ctypes.c_int)]
+
+
+class zl_checkpoint_info(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int) for n in ("arch", "n_layers", "d_model", "n_heads",
+                                              "n_kv_heads", "head_dim", "d_ff", "vocab",
+                                              "dtype", "optimizer")] + \
+               [("n_params", ctypes.c_uint64), ("step", ctypes.c_int64),
+                ("microbatches", ctypes.c_int64), ("windows", ctypes.c_int64),
+                ("checksum", ctypes.c_uint64)]
 
 
 class zl_profile_entry(ctypes.Structure):
@@ -105,6 +118,20 @@ def load(path=None):
         "zl_profile_begin": [vp, c],
         "zl_profile_end": [vp, P(zl_profile_entry), P(c)],
         "zl_device_info": [c, P(c), P(c), ctypes.c_char_p, c],
+        "zl_chunk_get_config": [vp, P(zl_config)],
+        "zl_chunk_get_buffers": [vp, P(zl_buffers)],
+        "zl_chunk_num_params": [vp, P(sz)],
+        "zl_pipeline_entry_bytes": [vp, c, c, P(sz)],
+        "zl_pipeline_create": [P(vp), c, P(vp), c, c, vp, sz, P(vp)],
+        "zl_pipeline_submit": [vp, vp, vp, vp, vp, c, c, vp, P(i64)],
+        "zl_pipeline_read_output": [vp, i64, vp, vp],
+        "zl_pipeline_sync": [vp],
+        "zl_pipeline_progress": [vp, P(i64), P(i64)],
+        "zl_pipeline_checkpoint": [vp, c, ctypes.c_char_p],
+        "zl_pipeline_destroy": [vp],
+        "zl_chunk_save": [vp, ctypes.c_char_p, i64, i64, vp],
+        "zl_chunk_load": [vp, ctypes.c_char_p, P(i64), P(i64), vp],
+        "zl_checkpoint_read_info": [ctypes.c_char_p, P(zl_checkpoint_info)],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -235,6 +262,85 @@ def zl_device_info(device=0):
     _check(load().zl_device_info(device, ctypes.byref(cu), ctypes.byref(clk), arch, 64),
            "zl_device_info")
     return dict(cu_count=cu.value, clock_khz=clk.value, arch=arch.value.decode())
+
+
+def zl_chunk_get_config(h):
+    cfg = zl_config()
+    _check(load().zl_chunk_get_config(h, ctypes.byref(cfg)), "zl_chunk_get_config")
+    return cfg
+
+
+def zl_chunk_num_params(h):
+    n = ctypes.c_size_t()
+    _check(load().zl_chunk_num_params(h, ctypes.byref(n)), "zl_chunk_num_params")
+    return n.value
+
+
+def zl_pipeline_entry_bytes(first_chunk, K, depth):
+    n = ctypes.c_size_t()
+    _check(load().zl_pipeline_entry_bytes(first_chunk, K, depth, ctypes.byref(n)),
+           "zl_pipeline_entry_bytes")
+    return n.value
+
+
+def zl_pipeline_create(chunks, streams, window, depth, entries, entry_bytes):
+    K = len(chunks)
+    ch = (ctypes.c_void_p * K)(*chunks)
+    st = (ctypes.c_void_p * K)(*streams)
+    h = ctypes.c_void_p()
+    _check(load().zl_pipeline_create(ch, K, st, window, depth, entries, entry_bytes,
+                                     ctypes.byref(h)), "zl_pipeline_create")
+    return h.value
+
+
+def zl_pipeline_submit(p, h0, labels, pos_ids, seq_lens, B, S, losses):
+    mb = ctypes.c_int64()
+    _check(load().zl_pipeline_submit(p, h0, labels, pos_ids, seq_lens, B, S, losses,
+                                     ctypes.byref(mb)), "zl_pipeline_submit")
+    return mb.value
+
+
+def zl_pipeline_read_output(p, mb, dst, stream=0):
+    _check(load().zl_pipeline_read_output(p, mb, dst, stream), "zl_pipeline_read_output")
+
+
+def zl_pipeline_sync(p):
+    _check(load().zl_pipeline_sync(p), "zl_pipeline_sync")
+
+
+def zl_pipeline_progress(p):
+    mb, w = ctypes.c_int64(), ctypes.c_int64()
+    _check(load().zl_pipeline_progress(p, ctypes.byref(mb), ctypes.byref(w)),
+           "zl_pipeline_progress")
+    return mb.value, w.value
+
+
+def zl_pipeline_checkpoint(p, stage, path):
+    _check(load().zl_pipeline_checkpoint(p, stage, os.fsencode(path)), "zl_pipeline_checkpoint")
+
+
+def zl_pipeline_destroy(p):
+    load().zl_pipeline_destroy(p)
+
+
+def zl_chunk_save(h, path, microbatches=0, windows=0, stream=0):
+    _check(load().zl_chunk_save(h, os.fsencode(path), microbatches, windows, stream),
+           "zl_chunk_save")
+
+
+def zl_chunk_load(h, path, stream=0):
+    """Restores the chunk; returns (microbatches, windows) progress."""
+    mb, w = ctypes.c_int64(), ctypes.c_int64()
+    _check(load().zl_chunk_load(h, os.fsencode(path), ctypes.byref(mb), ctypes.byref(w), stream),
+           "zl_chunk_load")
+    return mb.value, w.value
+
+
+def zl_checkpoint_read_info(path):
+    info = zl_checkpoint_info()
+    _check(load().zl_checkpoint_read_info(os.fsencode(path), ctypes.byref(info)),
+           "zl_checkpoint_read_info")
+    return {n: getattr(info, n) for n, _ in zl_checkpoint_info._fields_}
 
 
 def zl_profile_end(h, max_entries=256):
