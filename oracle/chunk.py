@@ -52,6 +52,7 @@ class OracleConfig:
     beta2: float = 0.999
     eps: float = 1e-8
     weight_decay: float = 0.01
+    adapter_rank: int = 0
     extra: dict = field(default_factory=dict)
 
     @classmethod
@@ -59,7 +60,8 @@ class OracleConfig:
         base = dict(arch=shape.arch, n_layers=shape.n_layers, d_model=shape.d_model,
                     n_heads=shape.n_heads, n_kv_heads=shape.n_kv_heads,
                     head_dim=shape.head_dim, d_ff=shape.d_ff, vocab=shape.vocab,
-                    norm_eps=shape.norm_eps, rope_theta=shape.rope_theta, dtype=shape.dtype)
+                    norm_eps=shape.norm_eps, rope_theta=shape.rope_theta, dtype=shape.dtype,
+                    adapter_rank=getattr(shape, "adapter_rank", 0))
         base.update(kw)
         return cls(**base)
 
@@ -128,12 +130,20 @@ def chunk_grads_ref(cfg, params, h_in, labels, head_w, head_norm_w, head_norm_b=
     W = np.asarray(head_w, np.float64)
     if cfg.dtype == "bf16":
         W = bf16_round(W)
+    adapter = None
+    if cfg.adapter_rank:
+        pre = f"L{cfg.n_layers}."
+        adapter = (fw["P"][pre + "ad_w1"], fw["P"][pre + "ad_w2"])
     loss, dh, info = local_objective_ref(
         h_out.reshape(B * S, d), fw["h_in"].reshape(B * S, d), np.asarray(labels).reshape(-1),
         W, cfg.arch, np.asarray(head_norm_w, np.float64),
         None if head_norm_b is None else np.asarray(head_norm_b, np.float64),
-        cfg.norm_eps, cfg.alpha, cfg.consis)
+        cfg.norm_eps, cfg.alpha, cfg.consis, adapter=adapter)
     _, grads = chunk_backward_ref(cfg, dh.reshape(B, S, d), fw, need_dx=False)
+    if adapter is not None:
+        pre = f"L{cfg.n_layers}."
+        grads[pre + "ad_w1"] = info["adapter_grads"]["w1"]
+        grads[pre + "ad_w2"] = info["adapter_grads"]["w2"]
     return dict(loss=loss, grads=grads, h_out=h_out, dh_out=dh.reshape(B, S, d), info=info)
 
 

@@ -113,15 +113,37 @@ def loss_and_dlogits(z, zp, labels, alpha, consis):
     return loss, dz, dict(ce=ce, kl=kl, n_omega=n_omega)
 
 
+def adapter_fwd(h, w1, w2):
+    """Readout adapter (Sec. III-B, Local Update interface (b)): a residual
+    MLP h' = h + gelu(h W1^T) W2^T, W1 [r, d], W2 [d, r], that is the
+    identity when W2 = 0."""
+    u = h @ w1.T
+    a = ops.gelu_fwd(u)
+    return h + a @ w2.T, (h, u, a, w1, w2)
+
+
+def adapter_bwd(dhp, cache):
+    """dL/dh and the weight gradients from dL/dh'."""
+    h, u, a, w1, w2 = cache
+    du = ops.gelu_bwd(dhp @ w2, u)
+    return dhp + du @ w1, dict(w1=du.T @ h, w2=dhp.T @ a)
+
+
 def local_objective_ref(h_out, h_in, labels, head_w, arch, hn_w, hn_b, eps,
-                        alpha, consis="reverse"):
+                        alpha, consis="reverse", adapter=None):
     """Loss and dL/dh_out for one micro-batch.  h_* [T, d], labels [T].
 
     h_in enters only through the stop-gradient readout; no gradient to it is
-    formed.
+    formed.  adapter: optional (W1, W2); h_out is read out through it, the
+    consistency target from h_in is the static head's readout.  The adapter
+    weight gradients are returned in info["adapter_grads"].
     """
     h_out = np.asarray(h_out, np.float64)
     W = np.asarray(head_w, np.float64)
+    ad_cache = None
+    if adapter is not None:
+        h_out, ad_cache = adapter_fwd(h_out, np.asarray(adapter[0], np.float64),
+                                      np.asarray(adapter[1], np.float64))
     n, c = head_norm_fwd(h_out, arch, hn_w, hn_b, eps)
     z = n @ W.T
     zp = None
@@ -131,4 +153,8 @@ def local_objective_ref(h_out, h_in, labels, head_w, arch, hn_w, hn_b, eps,
     loss, dz, rows = loss_and_dlogits(z, zp, np.asarray(labels).reshape(-1), alpha, consis)
     dn = dz @ W
     dh = head_norm_bwd(dn, arch, c)
-    return loss, dh, dict(z=z, zp=zp, dz=dz, **rows)
+    info = dict(z=z, zp=zp, dz=dz, **rows)
+    if ad_cache is not None:
+        info["dh_adapted"] = dh
+        dh, info["adapter_grads"] = adapter_bwd(dh, ad_cache)
+    return loss, dh, info

@@ -6,10 +6,10 @@ from oracle import OracleConfig
 from workload.configs import ChunkShape
 
 
-def tiny_shape(arch="llama", gqa=False, L=2, d=8, hd=4, ff=16, V=11, B=2, S=5):
+def tiny_shape(arch="llama", gqa=False, L=2, d=8, hd=4, ff=16, V=11, B=2, S=5, adapter_rank=0):
     hq, hkv = (4, 2) if gqa else (2, 2)
     return ChunkShape("fd", arch, L, d, hq, hkv, hd, ff, V, B, S, "f32",
-                      1e4 if arch == "llama" else 0.0, 2)
+                      1e4 if arch == "llama" else 0.0, 2, adapter_rank=adapter_rank)
 
 
 def tiny_case(arch="llama", gqa=False, alpha=0.5, consis="reverse", seed=0, std=0.3,

@@ -53,6 +53,13 @@ def test_fd_gqa():
     _fd_check(tiny_case("llama", gqa=True, alpha=0.3))
 
 
+@pytest.mark.parametrize("arch", ["llama", "gpt2"])
+@pytest.mark.parametrize("alpha", [1.0, 0.5])
+def test_fd_readout_adapter(arch, alpha):
+    """The readout adapter's two weights and every layer tensor through it."""
+    _fd_check(tiny_case(arch, alpha=alpha, adapter_rank=3))
+
+
 def test_fd_no_padding_one_layer():
     _fd_check(tiny_case("gpt2", alpha=0.7, pad=False, drop_labels=False, L=1))
 

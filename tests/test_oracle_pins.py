@@ -287,3 +287,47 @@ def test_bf16_mode_rounds_matrices_only():
     x = np.array([1.0, 1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, 1.0 + 2 ** -9, -3.5, 65504.0])
     np.testing.assert_array_equal(oracle.bf16_round(x),
                                   [1.0, 1.0, 1.0 + 2 ** -6, 1.0, -3.5, 65536.0])
+
+
+def _adapter_case(arch, w1_zero=False, w2_zero=False):
+    c = tiny_case(arch, alpha=0.5, adapter_rank=3)
+    L = c["shape"].n_layers
+    if w1_zero:
+        c["P"][f"L{L}.ad_w1"] = np.zeros_like(c["P"][f"L{L}.ad_w1"])
+    if w2_zero:
+        c["P"][f"L{L}.ad_w2"] = np.zeros_like(c["P"][f"L{L}.ad_w2"])
+    base = tiny_case(arch, alpha=0.5)  # same seeds, no adapter
+    return c, base, L
+
+
+def _grads(c):
+    return oracle.chunk_grads_ref(c["cfg"], c["P"], c["h_in"], c["labels"], c["head_w"], c["hn_w"],
+                                  c["hn_b"], c["seq_lens"], c["pos_ids"])
+
+
+@pytest.mark.parametrize("arch", ["llama", "gpt2"])
+def test_p11_adapter_is_identity_at_zero_output(arch):
+    """Readout adapter (Sec. III-B (b)) with W2 = 0: exactly the static head,
+    and no gradient reaches W1 (it only acts through W2)."""
+    c, base, L = _adapter_case(arch, w2_zero=True)
+    r, r0 = _grads(c), _grads(base)
+    assert r["loss"] == r0["loss"]
+    np.testing.assert_array_equal(r["dh_out"], r0["dh_out"])
+    assert not np.any(r["grads"][f"L{L}.ad_w1"])
+    for k in r0["grads"]:
+        np.testing.assert_array_equal(r["grads"][k], r0["grads"][k])
+
+
+@pytest.mark.parametrize("arch", ["llama", "gpt2"])
+def test_p11_adapter_gradient_at_zero_input(arch):
+    """W1 = 0: h' = h (gelu(0) = 0), so dW2 = 0 and, with gelu'(0) = 1/2,
+    dW1 = 1/2 W2^T (dL/dh)^T h with dL/dh the static-head gradient."""
+    c, base, L = _adapter_case(arch, w1_zero=True)
+    r, r0 = _grads(c), _grads(base)
+    assert abs(r["loss"] - r0["loss"]) < 1e-13
+    assert not np.any(r["grads"][f"L{L}.ad_w2"])
+    B, S, d = c["h_in"].shape
+    h = r0["h_out"].reshape(B * S, d)
+    dh = r0["dh_out"].reshape(B * S, d)
+    want = 0.5 * c["P"][f"L{L}.ad_w2"].T @ (dh.T @ h)
+    assert rel_err(r["grads"][f"L{L}.ad_w1"], want) < 1e-12

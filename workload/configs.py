@@ -24,6 +24,7 @@ class ChunkShape:
     rope_theta: float
     n_chunks: int        # chunks the whole model is split into
     norm_eps: float = 1e-5
+    adapter_rank: int = 0  # readout adapter width r (0 = static head only)
 
     @property
     def tokens(self):
@@ -51,7 +52,9 @@ def param_specs(cfg):
     """Trainable tensors of one chunk, in order: list of (key, shape, kind).
 
     key is "L{layer}.{name}"; kind is one of "norm_w", "norm_b", "weight",
-    "bias".  Linear weights are [out, in] (y = x W^T, as in Eq. (2)).
+    "bias", "adapter_out" (the readout adapter's output projection, a weight
+    initialised to zero so the adapter starts as the identity).  Linear
+    weights are [out, in] (y = x W^T, as in Eq. (2)).
     """
     d, hd = cfg.d_model, cfg.head_dim
     dq, dkv, ff = cfg.n_heads * hd, cfg.n_kv_heads * hd, cfg.d_ff
@@ -87,4 +90,10 @@ def param_specs(cfg):
             ]
         else:
             raise ValueError(cfg.arch)
+    if cfg.adapter_rank:
+        # readout adapter h' = h + gelu(h W1^T) W2^T before the frozen head,
+        # listed as one extra pseudo-layer after the chunk's layers
+        p = f"L{cfg.n_layers}."
+        out += [(p + "ad_w1", (cfg.adapter_rank, d), "weight"),
+                (p + "ad_w2", (d, cfg.adapter_rank), "adapter_out")]
     return out
