@@ -300,7 +300,7 @@ def _adapter_case(arch, w1_zero=False, w2_zero=False):
     return c, base, L
 
 
-def _grads(c):
+def _adapter_grads(c):
     return oracle.chunk_grads_ref(c["cfg"], c["P"], c["h_in"], c["labels"], c["head_w"], c["hn_w"],
                                   c["hn_b"], c["seq_lens"], c["pos_ids"])
 
@@ -310,7 +310,7 @@ def test_p11_adapter_is_identity_at_zero_output(arch):
     """Readout adapter (Sec. III-B (b)) with W2 = 0: exactly the static head,
     and no gradient reaches W1 (it only acts through W2)."""
     c, base, L = _adapter_case(arch, w2_zero=True)
-    r, r0 = _grads(c), _grads(base)
+    r, r0 = _adapter_grads(c), _adapter_grads(base)
     assert r["loss"] == r0["loss"]
     np.testing.assert_array_equal(r["dh_out"], r0["dh_out"])
     assert not np.any(r["grads"][f"L{L}.ad_w1"])
@@ -323,7 +323,7 @@ def test_p11_adapter_gradient_at_zero_input(arch):
     """W1 = 0: h' = h (gelu(0) = 0), so dW2 = 0 and, with gelu'(0) = 1/2,
     dW1 = 1/2 W2^T (dL/dh)^T h with dL/dh the static-head gradient."""
     c, base, L = _adapter_case(arch, w1_zero=True)
-    r, r0 = _grads(c), _grads(base)
+    r, r0 = _adapter_grads(c), _adapter_grads(base)
     assert abs(r["loss"] - r0["loss"]) < 1e-13
     assert not np.any(r["grads"][f"L{L}.ad_w2"])
     B, S, d = c["h_in"].shape
