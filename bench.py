@@ -40,7 +40,11 @@ def algorithmic_flops(shp, T, S, alpha):
     lin = 6.0 * p_lin * T * shp.n_layers
     attn = 3.0 * 2.0 * dq * (S + 1) * T * shp.n_layers
     head = (3.0 if alpha < 1.0 else 2.0) * 2.0 * d * shp.vocab * T
-    return lin + attn + head, dict(linear=lin, attention=attn, head=head)
+    parts = dict(linear=lin, attention=attn, head=head)
+    r = getattr(shp, "adapter_rank", 0)
+    if r:  # readout adapter: 2 GEMMs forward, 4 backward (dU, dh, dW2, dW1)
+        parts["adapter"] = 6.0 * 2.0 * d * r * T
+    return sum(parts.values()), parts
 
 
 def cpu_baseline(shp, alpha, seconds_hint=30.0):
@@ -219,6 +223,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="8b")
     ap.add_argument("--alpha", type=float, default=0.5)
+    ap.add_argument("--adapter-rank", type=int, default=0,
+                    help="readout adapter width r (0 = static head)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-json", default=None, help="write the per-kernel profile here")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -250,7 +256,7 @@ def main():
     from paper_2608_07974_amd import zl
     from paper_2608_07974_amd.chunk import TorchChunk, config_from_shape, current_stream
 
-    shp = workload.get_config(args.config)
+    shp = workload.get_config(args.config, adapter_rank=args.adapter_rank)
     B, S = shp.batch, shp.seq
     T = B * S
     dev = torch.device("cuda:0")
@@ -351,7 +357,8 @@ def main():
                                f"{shp.head_dim}, ff={shp.d_ff}, vocab={shp.vocab}"
                                if shp.name == "8b" else shp.name,
                    "global_batch": B, "seq_len": S, "tokens_per_step": T,
-                   "alpha": args.alpha, "optimizer": "adamw", "parallelism": "none (1 GPU)"},
+                   "alpha": args.alpha, "optimizer": "adamw", "parallelism": "none (1 GPU)",
+                   "adapter_rank": shp.adapter_rank},
         "mfma_util_pct": round(mfma_pct, 2),
         "device": dict(zl.zl_device_info(0), peak_bf16_tflops_used=PEAK_BF16_TFLOPS),
         "algorithmic_tflop_per_step": round(flops / 1e12, 2),

@@ -78,6 +78,13 @@ typedef struct zl_config {
   float lr, beta1, beta2, eps, weight_decay; /* AdamW (SGD uses lr only)     */
   int max_batch;     /* >= 1                                                 */
   int max_seq;       /* >= 1; also the RoPE position bound                   */
+  int adapter_rank;  /* readout adapter width r (Sec. III-B, Local Update
+                        interface (b)), 0 = static head only; else a multiple
+                        of 16: h_out is read out as h' = h + gelu(h W1^T) W2^T
+                        (W1 [r, d], W2 [d, r], GELU tanh form) through the
+                        frozen norm and head; the consistency target from
+                        h_in uses the static head.  W1 and W2 are trainable
+                        (W2 = 0 makes the adapter the identity).             */
 } zl_config;
 
 /* One trainable tensor inside the flat parameter buffers (zl_param_layout).
@@ -86,6 +93,8 @@ typedef struct zl_config {
  *          ln2_w[d], wg[ff,d], wu[ff,d], wd[d,ff]
  *   gpt2:  ln1_w[d], ln1_b[d], wqkv[(hq+2hkv)*hd,d], bqkv[..], wo[d,hq*hd],
  *          bo[d], ln2_w[d], ln2_b[d], wfc[ff,d], bfc[ff], wproj[d,ff], bproj[d]
+ * With adapter_rank r > 0 two more tensors follow the last layer, listed
+ * with layer index n_layers: ad_w1[r,d], ad_w2[d,r].
  * Linear weights are row-major [out, in] (y = x W^T, as in Eq. (2)).  Offsets
  * are in elements and multiples of 64; wq/wk/wv (and wg/wu) are adjacent. */
 typedef struct zl_tensor_desc {

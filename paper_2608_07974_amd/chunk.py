@@ -31,7 +31,7 @@ def config_from_shape(shp, alpha=0.5, consis="reverse", optimizer="adamw", lr=1e
         consis=zl.ZL_KL_REVERSE if consis == "reverse" else zl.ZL_KL_FORWARD,
         optimizer=zl.ZL_ADAMW if optimizer == "adamw" else zl.ZL_SGD, lr=lr, beta1=0.9,
         beta2=0.999, eps=1e-8, weight_decay=wd, max_batch=max_batch or shp.batch,
-        max_seq=max_seq or shp.seq)
+        max_seq=max_seq or shp.seq, adapter_rank=getattr(shp, "adapter_rank", 0))
 
 
 class TorchChunk:

@@ -56,6 +56,7 @@ struct LayerOff {
 
 struct Dims {
   int arch, L, d, hq, hkv, hd, ff, V, dq, dkv, nqkv, nup;
+  int ar;  // readout adapter width (0 = none)
   bool llama;
 };
 
@@ -74,6 +75,7 @@ Dims dims_of(const zl_config& c) {
   m.dkv = m.hkv * m.hd;
   m.nqkv = m.dq + 2 * m.dkv;
   m.nup = m.llama ? 2 * m.ff : m.ff;
+  m.ar = c.adapter_rank;
   return m;
 }
 
@@ -118,12 +120,15 @@ zl_status check_config(const zl_config* c) {
     return fail(ZL_ERR_INVALID_ARG, "max_batch and max_seq must be >= 1");
   if ((int64_t)c->max_batch * c->max_seq > (int64_t)1 << 24)
     return fail(ZL_ERR_UNSUPPORTED, "max_batch * max_seq above 2^24 tokens");
+  if (c->adapter_rank < 0 || c->adapter_rank % 16 || c->adapter_rank > 8192)
+    return fail(ZL_ERR_INVALID_ARG, "adapter_rank must be 0 or a multiple of 16 up to 8192");
   return ZL_OK;
 }
 
 struct Layout {
   std::vector<zl_tensor_desc> descs;
   std::vector<LayerOff> lay;
+  size_t ad_w1 = 0, ad_w2 = 0;  // readout adapter (adapter_rank > 0)
   size_t n_params = 0;
 };
 
@@ -174,6 +179,10 @@ void build_layout(const zl_config& c, Layout& out) {
       o.b_down = add("bproj", l, m.d, 1, 1);
     }
   }
+  if (m.ar) {
+    out.ad_w1 = add("ad_w1", m.L, m.ar, m.d, 2);
+    out.ad_w2 = add("ad_w2", m.L, m.d, m.ar, 2);
+  }
   out.n_params = off;
 }
 
@@ -186,6 +195,9 @@ struct Plan {
   std::vector<size_t> N1, RS1, MU1, QKV, O, LSE, X2, N2, RS2, MU2, UP, ACT;
   size_t DX, DXA, DUP, DN, DO, DQKV, DELTA, PART;
   size_t HN, HRS, HMU, ZC, DZ, DNF, ROWLOSS, NOMEGA;
+  // readout adapter: act copy of h_out, pre-activation, activation, h',
+  // dL/dh' (fp32 and act), dL/dU
+  size_t AXO, AU, AG, AHP, ADHP, ADHPA, ADU;
   size_t part_elems;
 };
 
@@ -248,6 +260,14 @@ void build_plan(const zl_config& c, Plan& p) {
   p.DNF = take(R * m.d * 4);
   p.ROWLOSS = take(T * 4);
   p.NOMEGA = take(4);
+  const size_t ar = (size_t)m.ar;
+  p.AXO = take(ar && act == 2 ? T * m.d * act : 0);
+  p.AU = take(T * ar * act);
+  p.AG = take(T * ar * act);
+  p.AHP = take(ar ? T * m.d * 4 : 0);
+  p.ADHP = take(ar ? T * m.d * 4 : 0);
+  p.ADHPA = take(ar ? T * m.d * act : 0);
+  p.ADU = take(T * ar * act);
   p.total = off;
 }
 
@@ -606,6 +626,33 @@ zl_status zl_local_objective(zl_chunk* c, const int32_t* labels, float* loss_out
   ZL_RUN("count_omega", 0, (double)T * 4, launch_count_omega(labels, T, m.V, nomega, s));
   const float* hout = c->at<float>(p.X[m.L]);
   const float* hin = c->at<float>(p.X[0]);
+  // readout adapter (Sec. III-B (b)): h_out is read out as
+  // h' = h_out + gelu(h_out W1^T) W2^T; h_in keeps the static head
+  float* dh_read = c->at<float>(p.DX);  // dL/d(read-out rows of h_out)
+  void* dh_read_a = c->ws + p.DXA;
+  if (m.ar) {
+    const void* xo = hout;
+    if (act == BF16) {
+      ZL_RUN("cast", 0, (double)T * m.d * 6, launch_cast(hout, F32, c->ws + p.AXO, BF16, (size_t)T * m.d, s));
+      xo = c->ws + p.AXO;
+    }
+    {
+      EpiArgs e = epi(EPI_GELU, c->ws + p.AG, m.ar, act);
+      e.out2 = c->ws + p.AU;
+      e.ldo2 = m.ar;
+      ZL_HIP(run_gemm(c, s, gdesc(T, m.ar, m.d, xo, m.d, true, c->W(c->layout.ad_w1), m.d, true), e));
+    }
+    {
+      EpiArgs e = epi(EPI_RESID, c->at<float>(p.AHP), m.d, F32);
+      e.resid = hout;
+      e.ldr = m.d;
+      ZL_HIP(run_gemm(c, s, gdesc(T, m.d, m.ar, c->ws + p.AG, m.ar, true, c->W(c->layout.ad_w2), m.ar,
+                               true), e));
+    }
+    hout = c->at<float>(p.AHP);
+    dh_read = c->at<float>(p.ADHP);
+    dh_read_a = c->ws + p.ADHPA;
+  }
   for (int r0 = 0; r0 < T; r0 += p.R) {
     const int rows = T - r0 < p.R ? T - r0 : p.R;
     ZL_RUN("head_norm", 0, (double)stk * rows * m.d * (4 + c->asz()), launch_head_norm(ln, hout, stk == 2 ? hin : nullptr, m.d, r0, rows,
@@ -634,7 +681,26 @@ zl_status zl_local_objective(zl_chunk* c, const int32_t* labels, float* loss_out
     }
     ZL_RUN("head_norm_bwd", 0, (double)rows * m.d * (12 + c->asz()), launch_head_norm_bwd(ln, c->at<float>(p.DNF), m.d, hout, c->buf.head_norm_w,
                                 ln ? c->at<float>(p.HMU) : nullptr, c->at<float>(p.HRS), stk,
-                                c->at<float>(p.DX), c->ws + p.DXA, act, r0, rows, m.d, s));
+                                dh_read, dh_read_a, act, r0, rows, m.d, s));
+  }
+  if (m.ar) {
+    // dU = gelu'(U) (dh' W2), then dL/dh_out = dh' + dU W1
+    {
+      EpiArgs e = epi(EPI_GELU_BWD, c->ws + p.ADU, m.ar, act);
+      e.aux = c->ws + p.AU;
+      e.ldaux = m.ar;
+      ZL_HIP(run_gemm(c, s, gdesc(T, m.ar, m.d, c->ws + p.ADHPA, m.d, true, c->W(c->layout.ad_w2),
+                               m.ar, false), e));
+    }
+    {
+      EpiArgs e = epi(EPI_RESID, c->at<float>(p.DX), m.d, F32);
+      e.resid = c->at<float>(p.ADHP);
+      e.ldr = m.d;
+      ZL_HIP(run_gemm(c, s, gdesc(T, m.d, m.ar, c->ws + p.ADU, m.ar, true, c->W(c->layout.ad_w1), m.d,
+                               false), e));
+    }
+    ZL_RUN("cast", 0, (double)T * m.d * (4 + c->asz()),
+           launch_cast(c->at<float>(p.DX), F32, c->ws + p.DXA, act, (size_t)T * m.d, s));
   }
   ZL_RUN("loss_reduce", 0, (double)T * 4, launch_loss_reduce(c->at<float>(p.ROWLOSS), T, nomega, loss_out, s));
   c->state = ST_OBJECTIVE;
@@ -682,6 +748,11 @@ zl_status zl_chunk_backward(zl_chunk* c, float grad_scale, int accumulate, void*
     return e;
   };
 
+  if (m.ar) {  // readout adapter weights: dW2 = dh'^T A, dW1 = dU^T h_out
+    ZL_HIP(wgrad(m.d, m.ar, c->ws + p.ADHPA, m.d, c->ws + p.AG, m.ar, c->layout.ad_w2));
+    const void* xo = act == BF16 ? (const void*)(c->ws + p.AXO) : (const void*)c->at<float>(p.X[m.L]);
+    ZL_HIP(wgrad(m.ar, m.d, c->ws + p.ADU, m.ar, xo, m.d, c->layout.ad_w1));
+  }
   for (int l = m.L - 1; l >= 0; --l) {
     const LayerOff& o = c->layout.lay[l];
     bool rope_fused = false;

@@ -45,7 +45,7 @@ class zl_config(ctypes.Structure):
                 ("optimizer", ctypes.c_int), ("lr", ctypes.c_float), ("beta1", ctypes.c_float),
                 ("beta2", ctypes.c_float), ("eps", ctypes.c_float),
                 ("weight_decay", ctypes.c_float), ("max_batch", ctypes.c_int),
-                ("max_seq", ctypes.c_int)]
+                ("max_seq", ctypes.c_int), ("adapter_rank", ctypes.c_int)]
 
 
 class zl_tensor_desc(ctypes.Structure):
@@ -156,10 +156,10 @@ def _check(st, name):
 def make_config(arch, n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ff, vocab, *,
                 norm_eps=1e-5, rope_theta=1e4, dtype=ZL_F32, alpha=0.5, consis=ZL_KL_REVERSE,
                 optimizer=ZL_ADAMW, lr=1e-4, beta1=0.9, beta2=0.999, eps=1e-8,
-                weight_decay=0.01, max_batch=1, max_seq=1):
+                weight_decay=0.01, max_batch=1, max_seq=1, adapter_rank=0):
     return zl_config(arch, n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ff, vocab,
                      norm_eps, rope_theta, dtype, alpha, consis, optimizer, lr, beta1, beta2,
-                     eps, weight_decay, max_batch, max_seq)
+                     eps, weight_decay, max_batch, max_seq, adapter_rank)
 
 
 def zl_param_layout(cfg):

@@ -44,14 +44,15 @@ def _cfg(**kw):
     return zl.make_config(zl.ZL_ARCH_LLAMA, 2, 64, 4, 4, 16, 256, 256, **base)
 
 
-def test_layout_matches_workload_specs():
+@pytest.mark.parametrize("adapter_rank", [0, 32])
+def test_layout_matches_workload_specs(adapter_rank):
     import workload
     for name in ("tiny", "gpt2", "8b"):
-        shp = workload.get_config(name)
+        shp = workload.get_config(name, adapter_rank=adapter_rank)
         arch = zl.ZL_ARCH_LLAMA if shp.arch == "llama" else zl.ZL_ARCH_GPT2
         cfg = zl.make_config(arch, shp.n_layers, shp.d_model, shp.n_heads, shp.n_kv_heads,
                              shp.head_dim, shp.d_ff, shp.vocab, rope_theta=max(shp.rope_theta, 2.0),
-                             max_batch=1, max_seq=8)
+                             max_batch=1, max_seq=8, adapter_rank=adapter_rank)
         n, lay = zl.zl_param_layout(cfg)
         specs = workload.param_specs(shp)
         assert [f"L{t['layer']}.{t['name']}" for t in lay] == [k for k, _, _ in specs]
@@ -68,6 +69,14 @@ def test_layout_matches_workload_specs():
             assert by[(0, "wu")]["offset"] == by[(0, "wg")]["offset"] + by[(0, "wg")]["numel"]
     assert zl.zl_param_layout(zl.make_config(zl.ZL_ARCH_LLAMA, 8, 4096, 32, 8, 128, 14336, 128256,
                                              rope_theta=5e5))[0] >= 1_744_896_000
+
+
+@pytest.mark.parametrize("rank", [-16, 8, 24])
+def test_adapter_rank_validated(rank):
+    import ctypes
+    b = ctypes.c_size_t()
+    assert zl.load().zl_workspace_size(ctypes.byref(_cfg(adapter_rank=rank)), ctypes.byref(b)) == \
+        zl.ZL_ERR_INVALID_ARG
 
 
 def test_workspace_grows_with_tokens():

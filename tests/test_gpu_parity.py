@@ -215,3 +215,57 @@ def test_llama8b_bf16_one_layer_slice():
 def test_llama8b_bf16_two_layers_alpha1_sgd():
     _case(workload.get_config("8b").with_(n_layers=2, batch=1, seq=256), alpha=1.0,
           optimizer="sgd", lr=1e-3)
+
+
+# ------------------------------------------------------ readout adapter
+@pytest.mark.parametrize("alpha", [0.5, 1.0])
+def test_tiny_fp32_readout_adapter(alpha):
+    _case(TINY.with_(adapter_rank=16), alpha=alpha, seq_lens=[32, 17, 1, 9], drop=5)
+
+
+def test_tiny_fp32_readout_adapter_three_steps():
+    _case(TINY.with_(adapter_rank=16), steps=3, lr=1e-3)
+
+
+def test_tiny_gpt2_fp32_readout_adapter():
+    shp = workload.configs.ChunkShape("tiny-gpt2", "gpt2", 2, 64, 4, 4, 16, 256, 97, 4, 24, "f32",
+                                      0.0, 2, adapter_rank=32)
+    _case(shp, alpha=0.5)
+
+
+def test_gpt2_bf16_readout_adapter():
+    _case(GPT2.with_(batch=2, seq=128, adapter_rank=64))
+
+
+def test_llama1b_bf16_one_layer_readout_adapter():
+    _case(workload.get_config("1b").with_(n_layers=1, batch=1, seq=512, adapter_rank=256))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_readout_adapter_with_zero_output_is_the_static_head(dtype):
+    """W2 = 0: loss, dL/dh_out and every layer gradient equal those of the
+    chunk without an adapter bit for bit, and dW1 is exactly 0."""
+    shp = TINY.with_(dtype=dtype)
+    params, batch = make_inputs(shp, seed=0)
+    shp_a = shp.with_(adapter_rank=16)
+    pa = workload.init_params(workload.param_specs(shp_a), seed=0, perturb=False)
+    L = shp.n_layers
+    params_a = dict(params, **{f"L{L}.ad_w1": pa[f"L{L}.ad_w1"],
+                               f"L{L}.ad_w2": np.zeros_like(pa[f"L{L}.ad_w2"])})
+    out = []
+    for s, p in ((shp, params), (shp_a, params_a)):
+        ch = device_chunk(s, p, batch)
+        d = to_dev(batch, dtype)
+        ch.forward(d["h_in"], d["seq_lens"], d["pos_ids"])
+        ch.objective(d["labels"])
+        dh = ch.inspect("dh_out")
+        ch.backward(1.0, 0)
+        torch.cuda.synchronize()
+        out.append((float(ch.loss.item()), dh, ch.tensors(ch.grad)))
+        ch.close()
+    (l0, dh0, g0), (l1, dh1, g1) = out
+    assert l0 == l1
+    np.testing.assert_array_equal(dh0, dh1)
+    for k in g0:
+        np.testing.assert_array_equal(g0[k], g1[k], err_msg=k)
+    assert not np.any(g1[f"L{L}.ad_w1"])
