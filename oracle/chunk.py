@@ -53,7 +53,14 @@ class OracleConfig:
     eps: float = 1e-8
     weight_decay: float = 0.01
     adapter_rank: int = 0
+    lora_rank: int = 0
+    lora_alpha: float = 16.0
     extra: dict = field(default_factory=dict)
+
+    @property
+    def lora_scale(self):
+        """s = lora_alpha / r of y = x W^T + s (x A^T) B^T."""
+        return self.lora_alpha / self.lora_rank if self.lora_rank else 0.0
 
     @classmethod
     def from_shape(cls, shape, **kw):
@@ -61,13 +68,24 @@ class OracleConfig:
                     n_heads=shape.n_heads, n_kv_heads=shape.n_kv_heads,
                     head_dim=shape.head_dim, d_ff=shape.d_ff, vocab=shape.vocab,
                     norm_eps=shape.norm_eps, rope_theta=shape.rope_theta, dtype=shape.dtype,
-                    adapter_rank=getattr(shape, "adapter_rank", 0))
+                    adapter_rank=getattr(shape, "adapter_rank", 0),
+                    lora_rank=getattr(shape, "lora_rank", 0),
+                    lora_alpha=getattr(shape, "lora_alpha", 16.0))
         base.update(kw)
         return cls(**base)
 
 
 def _is_matrix(key, arr):
     return np.ndim(arr) == 2
+
+
+def is_trainable(cfg, key):
+    """With LoRA (Eq. (6)) only the low-rank factors and the readout adapter
+    are trained; the base weights, norms and biases stay frozen."""
+    if not cfg.lora_rank:
+        return True
+    name = key.split(".", 1)[1]
+    return name.endswith("_la") or name.endswith("_lb") or name.startswith("ad_")
 
 
 def effective_params(cfg, params):
@@ -118,7 +136,7 @@ def chunk_backward_ref(cfg, dh_out, fw, need_dx=False):
     for l in reversed(range(cfg.n_layers)):
         nd = need_dx or l > 0
         dx, G = bwd(dx, fw["P"], f"L{l}.", cfg, fw["caches"][l], need_dx=nd)
-        grads.update(G)
+        grads.update({k: g for k, g in G.items() if is_trainable(cfg, k)})
     return (dx.reshape(B, S, -1) if dx is not None else None), grads
 
 
@@ -148,10 +166,14 @@ def chunk_grads_ref(cfg, params, h_in, labels, head_w, head_norm_w, head_norm_b=
 
 
 def optimizer_step_ref(cfg, params, grads, state):
-    """Apply one step to every trainable tensor; returns (params, state)."""
+    """Apply one step to every trainable tensor (frozen ones pass through);
+    returns (params, state)."""
     t = state.get("t", 0) + 1
     newp, m, v = {}, {}, {}
     for k in params:
+        if not is_trainable(cfg, k):
+            newp[k] = params[k]
+            continue
         if cfg.optimizer == "adamw":
             newp[k], m[k], v[k] = adamw_step_ref(
                 params[k], grads[k], state["m"].get(k, 0.0), state["v"].get(k, 0.0), t,

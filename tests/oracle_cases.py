@@ -6,10 +6,12 @@ from oracle import OracleConfig
 from workload.configs import ChunkShape
 
 
-def tiny_shape(arch="llama", gqa=False, L=2, d=8, hd=4, ff=16, V=11, B=2, S=5, adapter_rank=0):
+def tiny_shape(arch="llama", gqa=False, L=2, d=8, hd=4, ff=16, V=11, B=2, S=5, adapter_rank=0,
+               lora_rank=0, lora_alpha=16.0):
     hq, hkv = (4, 2) if gqa else (2, 2)
     return ChunkShape("fd", arch, L, d, hq, hkv, hd, ff, V, B, S, "f32",
-                      1e4 if arch == "llama" else 0.0, 2, adapter_rank=adapter_rank)
+                      1e4 if arch == "llama" else 0.0, 2, adapter_rank=adapter_rank,
+                      lora_rank=lora_rank, lora_alpha=lora_alpha)
 
 
 def tiny_case(arch="llama", gqa=False, alpha=0.5, consis="reverse", seed=0, std=0.3,
@@ -19,6 +21,10 @@ def tiny_case(arch="llama", gqa=False, alpha=0.5, consis="reverse", seed=0, std=
     specs = workload.param_specs(shp)
     P = {k: v.astype(np.float64) for k, v in
          workload.init_params(specs, seed=seed, std=std, perturb=True).items()}
+    trainable = list(P)
+    if shp.lora_rank:  # the frozen base joins the forward's parameters
+        base = workload.init_params(workload.base_specs(shp), seed=seed + 50, std=std, perturb=True)
+        P.update({k: v.astype(np.float64) for k, v in base.items()})
     rng = np.random.default_rng(seed + 100)
     B, S, d, V = shp.batch, shp.seq, shp.d_model, shp.vocab
     tok = rng.integers(0, V, size=(B, S)).astype(np.int32)
@@ -32,7 +38,7 @@ def tiny_case(arch="llama", gqa=False, alpha=0.5, consis="reverse", seed=0, std=
     hn_b = 0.05 * rng.standard_normal(d) if arch == "gpt2" else None
     pos = np.tile(np.arange(S, dtype=np.int32), (B, 1))
     return dict(cfg=cfg, shape=shp, P=P, h_in=h_in, labels=labels, seq_lens=lens, pos_ids=pos,
-                head_w=head_w, hn_w=hn_w, hn_b=hn_b)
+                head_w=head_w, hn_w=hn_w, hn_b=hn_b, trainable=trainable)
 
 
 def rel_err(a, b):

@@ -21,9 +21,10 @@ def _loss(c, P):
 def _fd_check(c, tol=1e-6):
     r = oracle.chunk_grads_ref(c["cfg"], c["P"], c["h_in"], c["labels"], c["head_w"], c["hn_w"],
                                c["hn_b"], c["seq_lens"], c["pos_ids"])
-    assert set(r["grads"]) == set(c["P"])
+    assert set(r["grads"]) == set(c["trainable"])
     worst = 0.0
-    for key, val in c["P"].items():
+    for key in c["trainable"]:
+        val = c["P"][key]
         fd = np.zeros_like(val)
         flat = val.reshape(-1)
         for i in range(flat.size):
@@ -58,6 +59,14 @@ def test_fd_gqa():
 def test_fd_readout_adapter(arch, alpha):
     """The readout adapter's two weights and every layer tensor through it."""
     _fd_check(tiny_case(arch, alpha=alpha, adapter_rank=3))
+
+
+@pytest.mark.parametrize("arch", ["llama", "gpt2"])
+def test_fd_lora(arch):
+    """LoRA factors of every target linear (the base is frozen), with the
+    readout adapter on the llama form."""
+    _fd_check(tiny_case(arch, alpha=0.5, lora_rank=2, lora_alpha=3.0,
+                        adapter_rank=2 if arch == "llama" else 0))
 
 
 def test_fd_no_padding_one_layer():

@@ -331,3 +331,66 @@ def test_p11_adapter_gradient_at_zero_input(arch):
     dh = r0["dh_out"].reshape(B * S, d)
     want = 0.5 * c["P"][f"L{L}.ad_w2"].T @ (dh.T @ h)
     assert rel_err(r["grads"][f"L{L}.ad_w1"], want) < 1e-12
+
+
+def _lora_run(c, P):
+    return oracle.chunk_grads_ref(c["cfg"], P, c["h_in"], c["labels"], c["head_w"], c["hn_w"],
+                                  c["hn_b"], c["seq_lens"], c["pos_ids"])
+
+
+@pytest.mark.parametrize("arch", ["llama", "gpt2"])
+def test_p12_lora_with_zero_B_is_the_base_model(arch):
+    """Eq. (6) LoRA with B = 0: the base model exactly, and dA = 0 (the A
+    factors act only through B)."""
+    c = tiny_case(arch, alpha=0.5, lora_rank=2)
+    P = {k: (np.zeros_like(v) if k.endswith("_lb") else v) for k, v in c["P"].items()}
+    base_cfg = oracle.OracleConfig.from_shape(c["shape"].with_(lora_rank=0), alpha=0.5)
+    base = {k: v for k, v in P.items() if not (k.endswith("_la") or k.endswith("_lb"))}
+    r = _lora_run(c, P)
+    r0 = oracle.chunk_grads_ref(base_cfg, base, c["h_in"], c["labels"], c["head_w"], c["hn_w"],
+                                c["hn_b"], c["seq_lens"], c["pos_ids"])
+    assert r["loss"] == r0["loss"]
+    np.testing.assert_array_equal(r["dh_out"], r0["dh_out"])
+    assert set(r["grads"]) == set(c["trainable"])
+    for k in c["trainable"]:
+        if k.endswith("_la"):
+            assert not np.any(r["grads"][k]), k
+
+
+@pytest.mark.parametrize("arch", ["llama", "gpt2"])
+def test_p12_lora_equals_merged_weight_update(arch):
+    """x W^T + s (x A^T) B^T = x (W + s B A)^T, so the LoRA loss equals the
+    full chunk's with W' = W + s B A, and the chain rule through W' gives
+    dB = s dW' A^T, dA = s B^T dW' from the full chunk's gradient dW'."""
+    c = tiny_case(arch, alpha=0.5, lora_rank=2, lora_alpha=3.0)
+    s = c["cfg"].lora_scale
+    r = _lora_run(c, c["P"])
+    merged, pairs = {}, []
+    for k, v in c["P"].items():
+        if k.endswith("_la") or k.endswith("_lb"):
+            continue
+        a, b = c["P"].get(k + "_la"), c["P"].get(k + "_lb")
+        merged[k] = v + s * b @ a if a is not None else v
+        if a is not None:
+            pairs.append((k, a, b))
+    full_cfg = oracle.OracleConfig.from_shape(c["shape"].with_(lora_rank=0), alpha=0.5)
+    rf = oracle.chunk_grads_ref(full_cfg, merged, c["h_in"], c["labels"], c["head_w"], c["hn_w"],
+                                c["hn_b"], c["seq_lens"], c["pos_ids"])
+    assert abs(r["loss"] - rf["loss"]) < 1e-12 * max(1.0, abs(rf["loss"]))
+    assert len(pairs) == (7 if arch == "llama" else 4) * c["shape"].n_layers
+    for k, a, b in pairs:
+        dW = rf["grads"][k]
+        assert rel_err(r["grads"][k + "_lb"], s * dW @ a.T) < 1e-10, k
+        assert rel_err(r["grads"][k + "_la"], s * b.T @ dW) < 1e-10, k
+
+
+def test_p12_lora_update_moves_only_the_factors():
+    c = tiny_case("llama", alpha=0.5, lora_rank=2)
+    mb = dict(h_in=c["h_in"], labels=c["labels"], seq_lens=c["seq_lens"], pos_ids=c["pos_ids"])
+    out = oracle.chunk_update_ref(c["cfg"], c["P"], init_opt_state(), [mb], c["head_w"], c["hn_w"],
+                                  c["hn_b"])
+    for k, v in c["P"].items():
+        if k in c["trainable"]:
+            assert np.any(out["params"][k] != v), k
+        else:
+            np.testing.assert_array_equal(out["params"][k], v, err_msg=k)

@@ -5,7 +5,7 @@ benchmark.  It holds shapes, seeded random draws and the next-token label
 shift only -- none of the method's arithmetic (no norm, attention, head,
 loss or optimizer code lives here).
 """
-from .configs import CONFIGS, ChunkShape, get_config, param_specs  # noqa: F401
+from .configs import CONFIGS, LORA_TARGETS, ChunkShape, base_specs, get_config, param_specs  # noqa: F401
 from .gen import (  # noqa: F401
     bf16_round_trip_input,
     embed_tokens,

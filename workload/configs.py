@@ -25,6 +25,8 @@ class ChunkShape:
     n_chunks: int        # chunks the whole model is split into
     norm_eps: float = 1e-5
     adapter_rank: int = 0  # readout adapter width r (0 = static head only)
+    lora_rank: int = 0     # LoRA rank (0 = the whole chunk is trained)
+    lora_alpha: float = 16.0  # LoRA scale s = lora_alpha / lora_rank
 
     @property
     def tokens(self):
@@ -48,13 +50,12 @@ def get_config(name, **overrides):
     return cfg.with_(**overrides) if overrides else cfg
 
 
-def param_specs(cfg):
-    """Trainable tensors of one chunk, in order: list of (key, shape, kind).
+def base_specs(cfg):
+    """The chunk's layer tensors, in order: list of (key, shape, kind).
 
     key is "L{layer}.{name}"; kind is one of "norm_w", "norm_b", "weight",
-    "bias", "adapter_out" (the readout adapter's output projection, a weight
-    initialised to zero so the adapter starts as the identity).  Linear
-    weights are [out, in] (y = x W^T, as in Eq. (2)).
+    "bias".  Linear weights are [out, in] (y = x W^T, as in Eq. (2)).  With
+    LoRA these are the frozen base of the chunk.
     """
     d, hd = cfg.d_model, cfg.head_dim
     dq, dkv, ff = cfg.n_heads * hd, cfg.n_kv_heads * hd, cfg.d_ff
@@ -90,6 +91,41 @@ def param_specs(cfg):
             ]
         else:
             raise ValueError(cfg.arch)
+    return out
+
+
+LORA_TARGETS = {"llama": ("wq", "wk", "wv", "wo", "wg", "wu", "wd"),
+                "gpt2": ("wqkv", "wo", "wfc", "wproj")}
+
+
+def param_specs(cfg):
+    """The chunk's trainable tensors, in order: list of (key, shape, kind).
+
+    Without LoRA: base_specs.  With LoRA (Eq. (6), rank r): per layer the
+    factors A [r, in] ("{name}_la", kind "lora_a") and B [out, r]
+    ("{name}_lb", kind "lora_b", zero-initialised so training starts from
+    the base model) of every linear in LORA_TARGETS, with the A factors of
+    q/k/v and of g/u adjacent.  Then, with adapter_rank r > 0, the readout
+    adapter as a pseudo-layer after the chunk's layers: ad_w1 [r, d] and
+    ad_w2 [d, r] (kind "adapter_out", zero-initialised: identity adapter).
+    """
+    d = cfg.d_model
+    if not cfg.lora_rank:
+        out = base_specs(cfg)
+    else:
+        shapes = {k[len("L0."):]: s for k, s, _ in base_specs(cfg.with_(n_layers=1))}
+        r = cfg.lora_rank
+        if cfg.arch == "llama":
+            order = [("wq", "a"), ("wk", "a"), ("wv", "a"), ("wq", "b"), ("wk", "b"), ("wv", "b"),
+                     ("wo", "a"), ("wo", "b"), ("wg", "a"), ("wu", "a"), ("wg", "b"), ("wu", "b"),
+                     ("wd", "a"), ("wd", "b")]
+        else:
+            order = [(n, f) for n in LORA_TARGETS["gpt2"] for f in ("a", "b")]
+        out = []
+        for l in range(cfg.n_layers):
+            for name, f in order:
+                o, i = shapes[name]
+                out.append((f"L{l}.{name}_l{f}", (r, i) if f == "a" else (o, r), "lora_" + f))
     if cfg.adapter_rank:
         # readout adapter h' = h + gelu(h W1^T) W2^T before the frozen head,
         # listed as one extra pseudo-layer after the chunk's layers

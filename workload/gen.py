@@ -64,9 +64,11 @@ def bf16_round_trip_input(x):
 def init_params(specs, seed=0, std=0.02, perturb=False, stress=False):
     """N(0, std) linears; norm weights 1 and biases 0.
 
-    perturb=True draws norm weights 1 + N(0, 0.1), biases N(0, 0.02) and a
-    non-zero readout-adapter output projection so every term of the update
-    is exercised (unperturbed, that projection is zero: identity adapter);
+    LoRA factors: A ~ N(0, std), B = 0 (the chunk starts as its base).
+    perturb=True draws norm weights 1 + N(0, 0.1), biases N(0, 0.02), and a
+    non-zero readout-adapter output projection and LoRA B, so every term of
+    the update is exercised (unperturbed, those are zero: identity adapter,
+    base model);
     stress=True widens the output projections (wo, wd, wproj) to
     N(0, 0.2 * sqrt(64 / fan_in)), i.e. 0.2 at fan-in 64, so their
     contribution keeps the same scale at every width.
@@ -78,10 +80,14 @@ def init_params(specs, seed=0, std=0.02, perturb=False, stress=False):
         if kind == "weight":
             s = 0.2 * np.sqrt(64.0 / shape[1]) if (stress and name in ("wo", "wd", "wproj")) else std
             out[key] = (rng.standard_normal(shape) * s).astype(np.float32)
-        elif kind == "adapter_out":
-            # zero (identity adapter) unless perturbed, so parity exercises it
-            out[key] = (rng.standard_normal(shape) * (0.2 * np.sqrt(64.0 / shape[1]) if stress else std)
-                        if perturb else np.zeros(shape)).astype(np.float32)
+        elif kind == "lora_a":
+            out[key] = (rng.standard_normal(shape) * std).astype(np.float32)
+        elif kind in ("adapter_out", "lora_b"):
+            # zero (identity adapter / base model) unless perturbed, so
+            # parity exercises it
+            sd = 0.2 * np.sqrt(64.0 / shape[1]) if (stress and kind == "adapter_out") else std
+            out[key] = (rng.standard_normal(shape) * sd if perturb
+                        else np.zeros(shape)).astype(np.float32)
         elif kind == "norm_w":
             out[key] = (1.0 + (rng.standard_normal(shape) * 0.1 if perturb else 0.0)) * np.ones(shape, np.float32)
             out[key] = out[key].astype(np.float32)
