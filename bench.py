@@ -30,17 +30,32 @@ def algorithmic_flops(shp, T, S, alpha):
     6 * P_lin * T for the chunk linears (forward, dgrad, wgrad); causal
     attention 2 * d_q * (S + 1) per token forward and twice that backward;
     head: readout of h_out, readout of h_in (alpha < 1), and the dgrad into
-    h_out, 2 * d * V per token each (the head is frozen: no wgrad)."""
+    h_out, 2 * d * V per token each (the head is frozen: no wgrad).
+    With LoRA rank r the base linears are frozen: 4 * P_lin * T (no wgrad,
+    and no data gradient of layer 0's QKV projection, which feeds only the
+    detached input), plus per linear (in, out) 6 * r * (in + out) per token
+    (x A^T and its B^T product forward; dy B, its A product, dA, dB
+    backward; layer 0's QKV dx product excepted)."""
     d, hd, ff = shp.d_model, shp.head_dim, shp.d_ff
     dq, dkv = shp.n_heads * hd, shp.n_kv_heads * hd
     if shp.arch == "llama":
         p_lin = d * (dq + 2 * dkv) + dq * d + 3 * d * ff
+        lins = [(d, dq), (d, dkv), (d, dkv), (dq, d), (d, ff), (d, ff), (ff, d)]
     else:
         p_lin = d * (dq + 2 * dkv) + dq * d + 2 * d * ff
-    lin = 6.0 * p_lin * T * shp.n_layers
+        lins = [(d, dq + 2 * dkv), (dq, d), (d, ff), (ff, d)]
+    lr = getattr(shp, "lora_rank", 0)
+    if lr:
+        nq = 3 if shp.arch == "llama" else 1
+        lin = 4.0 * p_lin * T * shp.n_layers - 2.0 * T * d * (dq + 2 * dkv)
+        lora = 6.0 * lr * T * shp.n_layers * sum(i + o for i, o in lins) - 2.0 * T * nq * lr * d
+    else:
+        lin = 6.0 * p_lin * T * shp.n_layers
     attn = 3.0 * 2.0 * dq * (S + 1) * T * shp.n_layers
     head = (3.0 if alpha < 1.0 else 2.0) * 2.0 * d * shp.vocab * T
     parts = dict(linear=lin, attention=attn, head=head)
+    if lr:
+        parts["lora"] = lora
     r = getattr(shp, "adapter_rank", 0)
     if r:  # readout adapter: 2 GEMMs forward, 4 backward (dU, dh, dW2, dW1)
         parts["adapter"] = 6.0 * 2.0 * d * r * T
@@ -225,6 +240,9 @@ def main():
     ap.add_argument("--alpha", type=float, default=0.5)
     ap.add_argument("--adapter-rank", type=int, default=0,
                     help="readout adapter width r (0 = static head)")
+    ap.add_argument("--lora-rank", type=int, default=0,
+                    help="LoRA rank r (0 = the whole chunk is trained)")
+    ap.add_argument("--lora-alpha", type=float, default=16.0, help="LoRA scale s = alpha / r")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-json", default=None, help="write the per-kernel profile here")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -256,22 +274,27 @@ def main():
     from paper_2608_07974_amd import zl
     from paper_2608_07974_amd.chunk import TorchChunk, config_from_shape, current_stream
 
-    shp = workload.get_config(args.config, adapter_rank=args.adapter_rank)
+    shp = workload.get_config(args.config, adapter_rank=args.adapter_rank,
+                              lora_rank=args.lora_rank, lora_alpha=args.lora_alpha)
     B, S = shp.batch, shp.seq
     T = B * S
     dev = torch.device("cuda:0")
     torch.manual_seed(0)
     cfg = config_from_shape(shp, alpha=args.alpha)
     ch = TorchChunk(cfg, device=dev)
-    # random-init weights of the architecture, on device: N(0, 0.02) linears,
-    # norm weights 1, biases 0; frozen head N(0, 0.02), head norm 1 / 0
-    ch.master.normal_(0.0, 0.02)
-    for t in ch.layout:
-        v = ch.view(ch.master, f"L{t['layer']}.{t['name']}")
-        if t["name"].startswith("ln") and t["name"].endswith("_w"):
-            v.fill_(1.0)
-        elif len(t["shape"]) == 1:
-            v.zero_()
+    # random-init weights of the architecture, on device: N(0, 0.02) linears
+    # (and LoRA factors), norm weights 1, biases 0; frozen head N(0, 0.02),
+    # head norm 1 / 0
+    for buf, layout in ((ch.master, ch.layout), (ch.base_master, ch.base_layout)):
+        if buf is None:
+            continue
+        buf.normal_(0.0, 0.02)
+        for t in layout:
+            v = buf[t["offset"]: t["offset"] + t["numel"]]
+            if t["name"].startswith("ln") and t["name"].endswith("_w"):
+                v.fill_(1.0)
+            elif len(t["shape"]) == 1:
+                v.zero_()
     ch.head_w.normal_(0.0, 0.02)
     zl.zl_refresh_shadow(ch.handle, current_stream())
     tokens = workload.zipf_tokens(B, S, shp.vocab, seed=1) if shp.vocab > 256 else \
@@ -358,7 +381,7 @@ def main():
                                if shp.name == "8b" else shp.name,
                    "global_batch": B, "seq_len": S, "tokens_per_step": T,
                    "alpha": args.alpha, "optimizer": "adamw", "parallelism": "none (1 GPU)",
-                   "adapter_rank": shp.adapter_rank},
+                   "adapter_rank": shp.adapter_rank, "lora_rank": shp.lora_rank},
         "mfma_util_pct": round(mfma_pct, 2),
         "device": dict(zl.zl_device_info(0), peak_bf16_tflops_used=PEAK_BF16_TFLOPS),
         "algorithmic_tflop_per_step": round(flops / 1e12, 2),

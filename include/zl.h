@@ -85,6 +85,18 @@ typedef struct zl_config {
                         frozen norm and head; the consistency target from
                         h_in uses the static head.  W1 and W2 are trainable
                         (W2 = 0 makes the adapter the identity).             */
+  int lora_rank;     /* LoRA rank r (Sec. II.A: Delta w_l = B_l A_l on the
+                        frozen w_l, trained by Eq. (6)); 0 = the whole chunk
+                        is trainable.  Else a multiple of 8 up to 256: every
+                        linear (llama wq wk wv wo wg wu wd, gpt2 wqkv wo wfc
+                        wproj) computes y = x W^T (+ b) + s (x A^T) B^T with
+                        s = lora_alpha / r; W, norms and biases are frozen and
+                        read from base_master / base_shadow; the trainable set
+                        is the factors A [r, in], B [out, r] (and the readout
+                        adapter).  A smaller rank q runs as r = 8 with rows
+                        q.. of A and columns q.. of B zero (they stay zero
+                        under SGD and AdamW) and lora_alpha scaled by 8 / q. */
+  float lora_alpha;  /* s = lora_alpha / lora_rank; > 0 when lora_rank > 0  */
 } zl_config;
 
 /* One trainable tensor inside the flat parameter buffers (zl_param_layout).
@@ -93,10 +105,20 @@ typedef struct zl_config {
  *          ln2_w[d], wg[ff,d], wu[ff,d], wd[d,ff]
  *   gpt2:  ln1_w[d], ln1_b[d], wqkv[(hq+2hkv)*hd,d], bqkv[..], wo[d,hq*hd],
  *          bo[d], ln2_w[d], ln2_b[d], wfc[ff,d], bfc[ff], wproj[d,ff], bproj[d]
+ * With lora_rank r > 0 these are the frozen base tensors, laid out in the
+ * base buffers as zl_param_layout of the same config with lora_rank = 0 and
+ * adapter_rank = 0, and the trainable tensors are, per layer, the factors
+ *   llama: wq_la[r,d], wk_la[r,d], wv_la[r,d], wq_lb[hq*hd,r],
+ *          wk_lb[hkv*hd,r], wv_lb[hkv*hd,r], wo_la[r,hq*hd], wo_lb[d,r],
+ *          wg_la[r,d], wu_la[r,d], wg_lb[ff,r], wu_lb[ff,r], wd_la[r,ff],
+ *          wd_lb[d,r]
+ *   gpt2:  wqkv_la[r,d], wqkv_lb[(hq+2hkv)*hd,r], wo_la, wo_lb, wfc_la,
+ *          wfc_lb, wproj_la, wproj_lb
  * With adapter_rank r > 0 two more tensors follow the last layer, listed
  * with layer index n_layers: ad_w1[r,d], ad_w2[d,r].
  * Linear weights are row-major [out, in] (y = x W^T, as in Eq. (2)).  Offsets
- * are in elements and multiples of 64; wq/wk/wv (and wg/wu) are adjacent. */
+ * are in elements and multiples of 64; wq/wk/wv (and wg/wu) are adjacent,
+ * and so are their LoRA A factors and their B factors. */
 typedef struct zl_tensor_desc {
   char name[16];
   int layer;
@@ -119,6 +141,13 @@ typedef struct zl_buffers {
   const float* head_norm_w; /* frozen final-norm weight [d_model]            */
   const float* head_norm_b; /* frozen final-norm bias [d_model] (gpt2), else
                                NULL                                          */
+  const float* base_master; /* lora_rank > 0: the frozen base tensors (fp32),
+                               n_base elements laid out as zl_param_layout of
+                               the config with lora_rank = adapter_rank = 0;
+                               else NULL                                     */
+  void* base_shadow;        /* lora_rank > 0 and ZL_BF16: bf16 copy of
+                               base_master, written by zl_refresh_shadow;
+                               else NULL                                     */
 } zl_buffers;
 
 typedef struct zl_chunk zl_chunk;
@@ -141,8 +170,9 @@ zl_status zl_chunk_create(const zl_config* cfg, const zl_buffers* bufs,
                           void* workspace, size_t ws_bytes, zl_chunk** out);
 void zl_chunk_destroy(zl_chunk* chunk);
 
-/* Writes the bf16 shadow from the fp32 master (round to nearest even).
- * Call after initialising or loading master in ZL_BF16 mode; a no-op for
+/* Writes the bf16 shadow from the fp32 master (round to nearest even), and
+ * with lora_rank > 0 also base_shadow from base_master.  Call after
+ * initialising or loading master (or the base) in ZL_BF16 mode; a no-op for
  * ZL_F32. */
 zl_status zl_refresh_shadow(zl_chunk* chunk, void* stream);
 

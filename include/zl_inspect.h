@@ -38,12 +38,15 @@ typedef struct zl_view {
  * Pointers are device pointers into the workspace; do not write them. */
 zl_status zl_inspect(const zl_chunk* chunk, const char* name, int layer, zl_view* out);
 
-/* C[m, n] = sum_k A(m, k) B(n, k), fp32 output with row stride ldc, where
- * A(m, k) = a_kmajor ? A[m*lda + k] : A[k*lda + m] and likewise for B; the
- * GEMM kernel used for every linear of the chunk (Eq. (1)) and the head
- * (Eq. (2)).  dtype ZL_BF16 (MFMA) or ZL_F32 (SIMT). */
+/* C[m, n] = sum_k A(m, k) B(n, k) + sum_{k < K2} A2(m, k) B2(n, k), fp32
+ * output with row stride ldc, where A(m, k) = a_kmajor ? A[m*lda + k] :
+ * A[k*lda + m] and likewise for B, A2 (lda2) and B2 (ldb2) in the layouts of
+ * A and B; the GEMM kernel used for every linear of the chunk (Eq. (1)), the
+ * second segment carrying the LoRA term (K2 = 0: none, A2 and B2 unused),
+ * and the head (Eq. (2)).  dtype ZL_BF16 (MFMA) or ZL_F32 (SIMT). */
 zl_status zl_kernel_gemm(int M, int N, int K, const void* A, int64_t lda, int a_kmajor,
-                         const void* B, int64_t ldb, int b_kmajor, float* C, int64_t ldc,
+                         const void* B, int64_t ldb, int b_kmajor, int K2, const void* A2,
+                         int64_t lda2, const void* B2, int64_t ldb2, float* C, int64_t ldc,
                          int dtype, void* stream);
 
 /* Causal GQA attention forward (backward = 0: o, lse) or backward

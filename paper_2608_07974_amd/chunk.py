@@ -31,12 +31,15 @@ def config_from_shape(shp, alpha=0.5, consis="reverse", optimizer="adamw", lr=1e
         consis=zl.ZL_KL_REVERSE if consis == "reverse" else zl.ZL_KL_FORWARD,
         optimizer=zl.ZL_ADAMW if optimizer == "adamw" else zl.ZL_SGD, lr=lr, beta1=0.9,
         beta2=0.999, eps=1e-8, weight_decay=wd, max_batch=max_batch or shp.batch,
-        max_seq=max_seq or shp.seq, adapter_rank=getattr(shp, "adapter_rank", 0))
+        max_seq=max_seq or shp.seq, adapter_rank=getattr(shp, "adapter_rank", 0),
+        lora_rank=getattr(shp, "lora_rank", 0), lora_alpha=getattr(shp, "lora_alpha", 16.0))
 
 
 class TorchChunk:
     """`head`: optional (head_w, head_norm_w, head_norm_b) device tensors to
-    share with other chunks (the frozen head is read-only)."""
+    share with other chunks (the frozen head is read-only).  With LoRA
+    (cfg.lora_rank > 0) the frozen base tensors sit in base_master /
+    base_shadow and master holds the trainable factors (and adapter)."""
 
     def __init__(self, cfg, device="cuda", head=None):
         zl.load()
@@ -60,15 +63,24 @@ class TorchChunk:
             self.head_norm_w = torch.ones(d, dtype=torch.float32, device=dev)
             self.head_norm_b = (torch.zeros(d, dtype=torch.float32, device=dev)
                                 if cfg.arch == zl.ZL_ARCH_GPT2 else None)
+        self.base_master = self.base_shadow = None
+        self.base_layout = []
+        if cfg.lora_rank:
+            nb, self.base_layout = zl.zl_param_layout(zl.base_config(cfg))
+            self.base_master = torch.zeros(nb, dtype=torch.float32, device=dev)
+            if cfg.dtype == zl.ZL_BF16:
+                self.base_shadow = torch.zeros(nb, dtype=torch.bfloat16, device=dev)
         self.ws_bytes = zl.zl_workspace_size(cfg)
         self._ws = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=dev)
         self.ws_ptr = (self._ws.data_ptr() + 255) // 256 * 256
         self.loss = torch.zeros(1, dtype=torch.float32, device=dev)
         bufs = zl.zl_buffers(_ptr(self.master), _ptr(self.shadow), _ptr(self.grad),
                              _ptr(self.adam_m), _ptr(self.adam_v), _ptr(self.head_w),
-                             _ptr(self.head_norm_w), _ptr(self.head_norm_b))
+                             _ptr(self.head_norm_w), _ptr(self.head_norm_b),
+                             _ptr(self.base_master), _ptr(self.base_shadow))
         self.handle = zl.zl_chunk_create(cfg, bufs, self.ws_ptr, self.ws_bytes)
         self.by_key = {f"L{t['layer']}.{t['name']}": t for t in self.layout}
+        self.base_by_key = {f"L{t['layer']}.{t['name']}": t for t in self.base_layout}
 
     def close(self):
         if self.handle:
@@ -87,8 +99,17 @@ class TorchChunk:
         return buf[t["offset"]: t["offset"] + t["numel"]].view(*t["shape"])
 
     def load_params(self, params):
+        """Trainable tensors by key into master; with LoRA, frozen base
+        tensors (keys of the base layout) into base_master."""
         for key, val in params.items():
-            self.view(self.master, key).copy_(torch.as_tensor(np.asarray(val, np.float32)))
+            src = torch.as_tensor(np.asarray(val, np.float32))
+            if key in self.by_key:
+                self.view(self.master, key).copy_(src)
+            elif key in self.base_by_key:
+                t = self.base_by_key[key]
+                self.base_master[t["offset"]: t["offset"] + t["numel"]].view(*t["shape"]).copy_(src)
+            else:
+                raise KeyError(key)
         zl.zl_refresh_shadow(self.handle, current_stream())
 
     def load_head(self, head_w, head_norm_w, head_norm_b=None):

@@ -44,6 +44,9 @@ template <> struct Elem<bf16_t> {
 //   A(m, k) = a_kmajor ? A[m * lda + k] : A[k * lda + m]
 //   B(n, k) = b_kmajor ? B[n * ldb + k] : B[k * ldb + n]
 // Elements of A with k >= ka and of B with k >= kb read as zero (ragged K).
+// Optional second K segment (K2 > 0): C[m, n] += sum_{k < K2} A2(m, k) B2(n, k)
+// with A2, B2 in the layouts of A and B (row strides lda2, ldb2); it carries
+// a low-rank term into the same accumulators.
 // Contiguous dimensions must be multiples of 8 elements and 16-byte aligned.
 struct GemmDesc {
   int M, N, K;
@@ -54,6 +57,11 @@ struct GemmDesc {
   const void* B;
   int64_t ldb;
   bool b_kmajor;
+  int K2;
+  const void* A2;
+  int64_t lda2;
+  const void* B2;
+  int64_t ldb2;
 };
 
 enum EpiKind {
@@ -81,7 +89,7 @@ struct EpiArgs {
   const void* aux;      // EPI_SWIGLU_BWD / EPI_GELU_BWD input (act dtype)
   int64_t ldaux;
   int ff;               // EPI_SWIGLU_BWD column offset of u / du
-  float scale;          // EPI_GRAD
+  float scale;          // EPI_GRAD, EPI_STORE (out = scale * acc + bias)
   int accumulate;       // EPI_GRAD
   const int32_t* pos;   // EPI_ROPE: position of row m
   const float2* rope;   // EPI_ROPE: (cos, sin) table [max_pos, hd/2]
@@ -140,6 +148,12 @@ hipError_t launch_rope_table(float2* table, int max_pos, int half, double theta,
 // [0, (hq + hkv) * hd)), forward (sign = +1) or transpose (sign = -1).
 hipError_t launch_rope(void* qkv, int64_t ld, int dtype, const int32_t* pos, const float2* table,
                        int max_pos, int T, int nheads_qk, int hd, int sign, hipStream_t s);
+// Block-diagonal [rows, nblk * r] (act dtype, row stride nblk * r) from the
+// stacked blocks src [rows, r]: rows [0, b1) form block 0, [b1, b2) block 1,
+// [b2, rows) block 2 (nblk <= 3); row n of block j keeps src row n in
+// columns j r .. j r + r - 1 and zeros elsewhere.
+hipError_t launch_blockdiag(const void* src, void* dst, int dtype, int rows, int r, int nblk,
+                            int b1, int b2, hipStream_t s);
 hipError_t launch_swiglu_fwd(const void* gu, int64_t ldgu, void* a, int64_t lda, int dtype,
                              int T, int ff, hipStream_t s);
 

@@ -45,7 +45,7 @@ __device__ inline void epilogue(const EpiArgs& e, int M, int N, int m, int n, fl
   const size_t mo = (size_t)m;
   switch (e.kind) {
     case EPI_STORE: {
-      float v = acc + (e.bias ? e.bias[n] : 0.f);
+      float v = e.scale * acc + (e.bias ? e.bias[n] : 0.f);
       st_act(e.out, e.out_dtype, mo * e.ldo + n, v);
       break;
     }
@@ -346,6 +346,28 @@ gemm_mfma_kernel(GemmDesc g, EpiArgs e) {
     }
     __syncthreads();
   }
+  // second K segment (same layouts), one tile at a time
+  for (int k0 = 0; k0 < g.K2; k0 += BKT) {
+    sa.load(reinterpret_cast<const bf16_t*>(g.A2), g.lda2, m0, g.M, k0, g.K2);
+    sb.load(reinterpret_cast<const bf16_t*>(g.B2), g.ldb2, n0, g.N, k0, g.K2);
+    sa.store(As);
+    sb.store(Bs);
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < NS; ++q) {
+      bf16x8_t af[FM], bfr[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) af[i] = *reinterpret_cast<const bf16x8_t*>(As + offA[q] + i * 32 * BKT);
+#pragma unroll
+      for (int j = 0; j < FN; ++j) bfr[j] = *reinterpret_cast<const bf16x8_t*>(Bs + offB[q] + j * 32 * BKT);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    }
+    __syncthreads();
+  }
 
   store_tile<BM, BN, WM, WN>(acc, smem, g, e, m0, n0, wave, lane);
 }
@@ -633,6 +655,36 @@ gemm_dma_kernel(GemmDesc g, EpiArgs e) {
   }
   dma_wait();  // the zero-fill copies past K must land before LDS is reused
   __syncthreads();
+  if (g.K2 > 0) {
+    // second K segment (same layouts): one BK-deep tile at a time through
+    // stage 0, copied and multiplied without overlap (K2 is a few tiles)
+    const i32x4_t ra2 = buffer_rsrc(reinterpret_cast<const bf16_t*>(g.A2) +
+                                    (AK ? (int64_t)m0 * g.lda2 : (int64_t)m0));
+    const i32x4_t rb2 = buffer_rsrc(reinterpret_cast<const bf16_t*>(g.B2) +
+                                    (BKM ? (int64_t)n0 * g.ldb2 : (int64_t)n0));
+    da.init(wave, lane, g.lda2, min(g.M - m0, BM));
+    db.init(wave, lane, g.ldb2, min(g.N - n0, BN));
+    const bf16_t* as = reinterpret_cast<const bf16_t*>(smem);
+    for (int k0 = 0; k0 < g.K2; k0 += BK) {
+      da.issue(lds0, wave, k0, g.K2, ra2);
+      db.issue(lds0 + ABYTES, wave, k0, g.K2, rb2);
+      dma_wait();
+      __syncthreads();
+#pragma unroll
+      for (int q = 0; q < NS; ++q) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i) af[0][i] = fa.read(as, q, i);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) bfr[0][j] = fb.read(as + BM * BK, q, j);
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[0][i], bfr[0][j], acc[i][j], 0, 0, 0);
+      }
+      __syncthreads();
+    }
+  }
   store_tile<BM, BN, WM, WN>(acc, smem, g, e, m0, n0, wave, lane);
 }
 
@@ -644,16 +696,20 @@ __global__ void __launch_bounds__(256) gemm_simt_kernel(GemmDesc g, EpiArgs e) {
   __shared__ float Bs[BK][BN + 4];
   const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-  const float* A = reinterpret_cast<const float*>(g.A);
-  const float* B = reinterpret_cast<const float*>(g.B);
   float acc[4][4] = {};
-  for (int k0 = 0; k0 < g.K; k0 += BK) {
+  // segment 0: (A, B) over K; segment 1: (A2, B2) over K2
+  for (int seg = 0; seg < 2; ++seg) {
+  const float* A = reinterpret_cast<const float*>(seg ? g.A2 : g.A);
+  const float* B = reinterpret_cast<const float*>(seg ? g.B2 : g.B);
+  const int64_t lda = seg ? g.lda2 : g.lda, ldb = seg ? g.ldb2 : g.ldb;
+  const int K = seg ? g.K2 : g.K, ka = seg ? g.K2 : g.ka, kb = seg ? g.K2 : g.kb;
+  for (int k0 = 0; k0 < K; k0 += BK) {
     for (int idx = threadIdx.x; idx < BM * BK; idx += 256) {
       int r, k;
       if (AK) { r = idx / BK; k = idx % BK; } else { r = idx % BM; k = idx / BM; }
       const int gr = m0 + r, gk = k0 + k;
       float v = 0.f;
-      if (gr < g.M && gk < g.ka) v = AK ? A[(int64_t)gr * g.lda + gk] : A[(int64_t)gk * g.lda + gr];
+      if (gr < g.M && gk < ka) v = AK ? A[(int64_t)gr * lda + gk] : A[(int64_t)gk * lda + gr];
       As[k][r] = v;
     }
     for (int idx = threadIdx.x; idx < BN * BK; idx += 256) {
@@ -661,7 +717,7 @@ __global__ void __launch_bounds__(256) gemm_simt_kernel(GemmDesc g, EpiArgs e) {
       if (BKM) { r = idx / BK; k = idx % BK; } else { r = idx % BN; k = idx / BN; }
       const int gr = n0 + r, gk = k0 + k;
       float v = 0.f;
-      if (gr < g.N && gk < g.kb) v = BKM ? B[(int64_t)gr * g.ldb + gk] : B[(int64_t)gk * g.ldb + gr];
+      if (gr < g.N && gk < kb) v = BKM ? B[(int64_t)gr * ldb + gk] : B[(int64_t)gk * ldb + gr];
       Bs[k][r] = v;
     }
     __syncthreads();
@@ -678,6 +734,7 @@ __global__ void __launch_bounds__(256) gemm_simt_kernel(GemmDesc g, EpiArgs e) {
         for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
     }
     __syncthreads();
+  }
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -782,7 +839,9 @@ static hipError_t run_layout(const GemmDesc& g, const EpiArgs& e, int dtype, hip
     const bool large = big >= 240 || e.kind == EPI_ROPE;
     const int R = large ? 256 : 128;
     const bool dma = dma_operand_ok(g.A, g.lda, AK, g.M, g.ka, R) &&
-                     dma_operand_ok(g.B, g.ldb, BKM, g.N, g.kb, R);
+                     dma_operand_ok(g.B, g.ldb, BKM, g.N, g.kb, R) &&
+                     (g.K2 <= 0 || (dma_operand_ok(g.A2, g.lda2, AK, g.M, g.K2, R) &&
+                                    dma_operand_ok(g.B2, g.ldb2, BKM, g.N, g.K2, R)));
     if (dma) {
       if (large) { err = run_dma<256, 256, GEMM_WM, GEMM_WN, GEMM_BK, GEMM_NST, AK, BKM>(g, e, s); which = 3; }
       else { err = run_dma<128, 128, 2, 2, GEMM_BK, GEMM_NST, AK, BKM>(g, e, s); which = 4; }
@@ -811,6 +870,7 @@ hipError_t launch_gemm(const GemmDesc& g, const EpiArgs& e, int dtype, hipStream
                        const char** kname) {
   if (kname) *kname = "gemm_empty";
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
+  if (g.K2 < 0 || (g.K2 > 0 && (!g.A2 || !g.B2))) return hipErrorInvalidValue;
   if (e.kind == EPI_ROPE && (dtype != BF16 || e.hd > 128 || 128 % e.hd != 0 || !e.pos || !e.rope))
     return hipErrorInvalidValue;
   if (g.a_kmajor && g.b_kmajor) return run_layout<true, true>(g, e, dtype, s, kname);

@@ -415,4 +415,32 @@ hipError_t launch_swiglu_fwd(const void* gu, int64_t ldgu, void* a, int64_t lda,
   return hipGetLastError();
 }
 
+
+// Block-diagonal expansion of stacked low-rank factors (one thread per output
+// element; the matrix is small: rows x nblk r).
+__global__ void blockdiag_kernel(const void* __restrict__ src, void* __restrict__ dst, int dt,
+                                 int rows, int r, int nblk, int b1, int b2) {
+  const int64_t w = (int64_t)nblk * r, n = (int64_t)rows * w;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t row = i / w;
+    const int col = (int)(i % w);
+    const int blk = row < b1 ? 0 : (row < b2 ? 1 : 2);
+    stf(dst, dt, i, col / r == blk ? ldf(src, dt, row * r + col % r) : 0.f);
+  }
+}
+
+hipError_t launch_blockdiag(const void* src, void* dst, int dtype, int rows, int r, int nblk,
+                            int b1, int b2, hipStream_t s) {
+  if (nblk < 1 || nblk > 3 || r < 1 || rows < 0 || b1 < 0 || b2 < b1 || b2 > rows)
+    return hipErrorInvalidValue;
+  const int64_t n = (int64_t)rows * nblk * r;
+  if (n == 0) return hipSuccess;
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(blockdiag_kernel, dim3((unsigned)blocks), dim3(256), 0, s, src, dst, dtype,
+                     rows, r, nblk, b1, b2);
+  return hipGetLastError();
+}
+
 }  // namespace zl

@@ -57,6 +57,9 @@ struct LayerOff {
 struct Dims {
   int arch, L, d, hq, hkv, hd, ff, V, dq, dkv, nqkv, nup;
   int ar;  // readout adapter width (0 = none)
+  int lr;  // LoRA rank (0 = full training)
+  int nqa, nua;  // rows of the stacked A factors of the QKV and up projections
+  float ls;      // LoRA scale lora_alpha / lr
   bool llama;
 };
 
@@ -76,6 +79,10 @@ Dims dims_of(const zl_config& c) {
   m.nqkv = m.dq + 2 * m.dkv;
   m.nup = m.llama ? 2 * m.ff : m.ff;
   m.ar = c.adapter_rank;
+  m.lr = c.lora_rank;
+  m.nqa = m.llama ? 3 * m.lr : m.lr;
+  m.nua = m.llama ? 2 * m.lr : m.lr;
+  m.ls = m.lr ? c.lora_alpha / (float)m.lr : 0.f;
   return m;
 }
 
@@ -122,20 +129,34 @@ zl_status check_config(const zl_config* c) {
     return fail(ZL_ERR_UNSUPPORTED, "max_batch * max_seq above 2^24 tokens");
   if (c->adapter_rank < 0 || c->adapter_rank % 16 || c->adapter_rank > 8192)
     return fail(ZL_ERR_INVALID_ARG, "adapter_rank must be 0 or a multiple of 16 up to 8192");
+  if (c->lora_rank < 0 || c->lora_rank % 8 || c->lora_rank > 256)
+    return fail(ZL_ERR_INVALID_ARG, "lora_rank must be 0 or a multiple of 8 up to 256");
+  if (c->lora_rank && !(c->lora_alpha > 0.f && isfinite(c->lora_alpha)))
+    return fail(ZL_ERR_INVALID_ARG, "lora_alpha must be finite and > 0");
   return ZL_OK;
 }
 
-struct Layout {
-  std::vector<zl_tensor_desc> descs;
-  std::vector<LayerOff> lay;
-  size_t ad_w1 = 0, ad_w2 = 0;  // readout adapter (adapter_rank > 0)
-  size_t n_params = 0;
+// LoRA factor offsets of one layer.  A factors of projections that share an
+// input (q/k/v, gate/up) are adjacent, i.e. one stacked [nblk * r, in]
+// matrix; so are their B factors ([sum of outs, r]).
+struct LoraOff {
+  size_t qkv_a, qkv_b, o_a, o_b, up_a, up_b, down_a, down_b;
 };
 
-void build_layout(const zl_config& c, Layout& out) {
-  const Dims m = dims_of(c);
+struct Layout {
+  std::vector<zl_tensor_desc> descs;  // trainable tensors
+  std::vector<LayerOff> lay;  // layer tensors: trainable buffers, or the base buffers with LoRA
+  std::vector<LoraOff> lora;  // lora_rank > 0
+  size_t ad_w1 = 0, ad_w2 = 0;  // readout adapter (adapter_rank > 0)
+  size_t n_params = 0;  // trainable elements
+  size_t n_base = 0;    // base buffer elements (lora_rank > 0)
+};
+
+// Appends tensors to a flat buffer, each offset a multiple of ALIGN_ELEMS.
+struct Packer {
+  std::vector<zl_tensor_desc>* descs;
   size_t off = 0;
-  auto add = [&](const char* name, int layer, int64_t r, int64_t cols, int ndim) -> size_t {
+  size_t add(const char* name, int layer, int64_t r, int64_t cols, int ndim) {
     zl_tensor_desc t;
     memset(&t, 0, sizeof(t));
     strncpy(t.name, name, sizeof(t.name) - 1);
@@ -145,45 +166,96 @@ void build_layout(const zl_config& c, Layout& out) {
     t.shape[1] = cols;
     t.offset = off;
     t.numel = (size_t)r * cols;
-    out.descs.push_back(t);
+    if (descs) descs->push_back(t);
     const size_t at = off;
     off = round_up(off + t.numel, ALIGN_ELEMS);
     return at;
-  };
-  out.lay.resize(m.L);
+  }
+};
+
+void layer_tensors(const Dims& m, Packer& pk, std::vector<LayerOff>& lay) {
+  lay.resize(m.L);
   for (int l = 0; l < m.L; ++l) {
-    LayerOff& o = out.lay[l];
+    LayerOff& o = lay[l];
     memset(&o, 0, sizeof(o));
     if (m.llama) {
-      o.ln1_w = add("ln1_w", l, m.d, 1, 1);
-      o.w_qkv = add("wq", l, m.dq, m.d, 2);
-      add("wk", l, m.dkv, m.d, 2);
-      add("wv", l, m.dkv, m.d, 2);
-      o.w_o = add("wo", l, m.d, m.dq, 2);
-      o.ln2_w = add("ln2_w", l, m.d, 1, 1);
-      o.w_up = add("wg", l, m.ff, m.d, 2);
-      add("wu", l, m.ff, m.d, 2);
-      o.w_down = add("wd", l, m.d, m.ff, 2);
+      o.ln1_w = pk.add("ln1_w", l, m.d, 1, 1);
+      o.w_qkv = pk.add("wq", l, m.dq, m.d, 2);
+      pk.add("wk", l, m.dkv, m.d, 2);
+      pk.add("wv", l, m.dkv, m.d, 2);
+      o.w_o = pk.add("wo", l, m.d, m.dq, 2);
+      o.ln2_w = pk.add("ln2_w", l, m.d, 1, 1);
+      o.w_up = pk.add("wg", l, m.ff, m.d, 2);
+      pk.add("wu", l, m.ff, m.d, 2);
+      o.w_down = pk.add("wd", l, m.d, m.ff, 2);
     } else {
-      o.ln1_w = add("ln1_w", l, m.d, 1, 1);
-      o.ln1_b = add("ln1_b", l, m.d, 1, 1);
-      o.w_qkv = add("wqkv", l, m.nqkv, m.d, 2);
-      o.b_qkv = add("bqkv", l, m.nqkv, 1, 1);
-      o.w_o = add("wo", l, m.d, m.dq, 2);
-      o.b_o = add("bo", l, m.d, 1, 1);
-      o.ln2_w = add("ln2_w", l, m.d, 1, 1);
-      o.ln2_b = add("ln2_b", l, m.d, 1, 1);
-      o.w_up = add("wfc", l, m.ff, m.d, 2);
-      o.b_up = add("bfc", l, m.ff, 1, 1);
-      o.w_down = add("wproj", l, m.d, m.ff, 2);
-      o.b_down = add("bproj", l, m.d, 1, 1);
+      o.ln1_w = pk.add("ln1_w", l, m.d, 1, 1);
+      o.ln1_b = pk.add("ln1_b", l, m.d, 1, 1);
+      o.w_qkv = pk.add("wqkv", l, m.nqkv, m.d, 2);
+      o.b_qkv = pk.add("bqkv", l, m.nqkv, 1, 1);
+      o.w_o = pk.add("wo", l, m.d, m.dq, 2);
+      o.b_o = pk.add("bo", l, m.d, 1, 1);
+      o.ln2_w = pk.add("ln2_w", l, m.d, 1, 1);
+      o.ln2_b = pk.add("ln2_b", l, m.d, 1, 1);
+      o.w_up = pk.add("wfc", l, m.ff, m.d, 2);
+      o.b_up = pk.add("bfc", l, m.ff, 1, 1);
+      o.w_down = pk.add("wproj", l, m.d, m.ff, 2);
+      o.b_down = pk.add("bproj", l, m.d, 1, 1);
     }
   }
-  if (m.ar) {
-    out.ad_w1 = add("ad_w1", m.L, m.ar, m.d, 2);
-    out.ad_w2 = add("ad_w2", m.L, m.d, m.ar, 2);
+}
+
+// Every factor's element count is a multiple of 64 (r and the widths are
+// multiples of 8, d and ff of 64), so stacked factors are contiguous.
+void lora_tensors(const Dims& m, Packer& pk, std::vector<LoraOff>& lora) {
+  const int r = m.lr;
+  lora.resize(m.L);
+  for (int l = 0; l < m.L; ++l) {
+    LoraOff& o = lora[l];
+    if (m.llama) {
+      o.qkv_a = pk.add("wq_la", l, r, m.d, 2);
+      pk.add("wk_la", l, r, m.d, 2);
+      pk.add("wv_la", l, r, m.d, 2);
+      o.qkv_b = pk.add("wq_lb", l, m.dq, r, 2);
+      pk.add("wk_lb", l, m.dkv, r, 2);
+      pk.add("wv_lb", l, m.dkv, r, 2);
+      o.o_a = pk.add("wo_la", l, r, m.dq, 2);
+      o.o_b = pk.add("wo_lb", l, m.d, r, 2);
+      o.up_a = pk.add("wg_la", l, r, m.d, 2);
+      pk.add("wu_la", l, r, m.d, 2);
+      o.up_b = pk.add("wg_lb", l, m.ff, r, 2);
+      pk.add("wu_lb", l, m.ff, r, 2);
+      o.down_a = pk.add("wd_la", l, r, m.ff, 2);
+      o.down_b = pk.add("wd_lb", l, m.d, r, 2);
+    } else {
+      o.qkv_a = pk.add("wqkv_la", l, r, m.d, 2);
+      o.qkv_b = pk.add("wqkv_lb", l, m.nqkv, r, 2);
+      o.o_a = pk.add("wo_la", l, r, m.dq, 2);
+      o.o_b = pk.add("wo_lb", l, m.d, r, 2);
+      o.up_a = pk.add("wfc_la", l, r, m.d, 2);
+      o.up_b = pk.add("wfc_lb", l, m.ff, r, 2);
+      o.down_a = pk.add("wproj_la", l, r, m.ff, 2);
+      o.down_b = pk.add("wproj_lb", l, m.d, r, 2);
+    }
   }
-  out.n_params = off;
+}
+
+void build_layout(const zl_config& c, Layout& out) {
+  const Dims m = dims_of(c);
+  Packer pk{&out.descs};
+  if (m.lr) {
+    Packer base{nullptr};
+    layer_tensors(m, base, out.lay);
+    out.n_base = base.off;
+    lora_tensors(m, pk, out.lora);
+  } else {
+    layer_tensors(m, pk, out.lay);
+  }
+  if (m.ar) {
+    out.ad_w1 = pk.add("ad_w1", m.L, m.ar, m.d, 2);
+    out.ad_w2 = pk.add("ad_w2", m.L, m.d, m.ar, 2);
+  }
+  out.n_params = pk.off;
 }
 
 // Workspace plan: byte offsets of every region, 256-byte aligned.
@@ -198,6 +270,10 @@ struct Plan {
   // readout adapter: act copy of h_out, pre-activation, activation, h',
   // dL/dh' (fp32 and act), dL/dU
   size_t AXO, AU, AG, AHP, ADHP, ADHPA, ADU;
+  // LoRA: s x A^T of each projection per layer (act), the block-diagonal
+  // B factors of the projection being computed (act), and s (dy B) (act)
+  std::vector<size_t> LXQ, LXO, LXU, LXD;
+  size_t LBD, LE;
   size_t part_elems;
 };
 
@@ -268,6 +344,17 @@ void build_plan(const zl_config& c, Plan& p) {
   p.ADHP = take(ar ? T * m.d * 4 : 0);
   p.ADHPA = take(ar ? T * m.d * act : 0);
   p.ADU = take(T * ar * act);
+  const size_t lr = (size_t)m.lr;
+  p.LXQ.resize(m.L); p.LXO.resize(m.L); p.LXU.resize(m.L); p.LXD.resize(m.L);
+  for (int l = 0; l < m.L; ++l) {
+    p.LXQ[l] = take(T * m.nqa * act);
+    p.LXO[l] = take(T * lr * act);
+    p.LXU[l] = take(T * m.nua * act);
+    p.LXD[l] = take(T * lr * act);
+  }
+  const size_t bd_q = (size_t)m.nqkv * m.nqa, bd_u = (size_t)m.nup * m.nua;
+  p.LBD = take(lr && m.llama ? (bd_q > bd_u ? bd_q : bd_u) * act : 0);
+  p.LE = take(T * m.nqa * act);
   p.total = off;
 }
 
@@ -308,11 +395,18 @@ struct zl_chunk {
   }
 
   template <typename P> P* at(size_t off) const { return reinterpret_cast<P*>(ws + off); }
-  const void* W(size_t off) const {  // a weight matrix as the kernels consume it
+  // Layer tensors live in the trainable buffers, or in the frozen base
+  // buffers with LoRA; the adapter and LoRA factors in the trainable ones.
+  const void* W(size_t off) const {  // a layer weight matrix as the kernels consume it
+    if (act == BF16)
+      return reinterpret_cast<const bf16_t*>(m.lr ? buf.base_shadow : buf.shadow) + off;
+    return V32(off);
+  }
+  const float* V32(size_t off) const { return (m.lr ? buf.base_master : buf.master) + off; }
+  const void* WT(size_t off) const {  // a trainable matrix (adapter, LoRA factor)
     if (act == BF16) return reinterpret_cast<const bf16_t*>(buf.shadow) + off;
     return buf.master + off;
   }
-  const float* V32(size_t off) const { return buf.master + off; }
   float* G(size_t off) const { return buf.grad + off; }
   size_t asz() const { return act == BF16 ? 2 : 4; }
   void* A(size_t base_off, size_t elem_off) const { return ws + base_off + elem_off * asz(); }
@@ -327,6 +421,7 @@ static GemmDesc gdesc(int M, int N, int K, const void* A, int64_t lda, bool ak, 
   g.M = M; g.N = N; g.K = K; g.ka = K; g.kb = K;
   g.A = A; g.lda = lda; g.a_kmajor = ak;
   g.B = B; g.ldb = ldb; g.b_kmajor = bk;
+  g.K2 = 0; g.A2 = nullptr; g.lda2 = 0; g.B2 = nullptr; g.ldb2 = 0;
   return g;
 }
 
@@ -343,7 +438,7 @@ static hipError_t run_gemm(zl_chunk* c, hipStream_t s, const GemmDesc& g, const 
   const int pi = c->prof_start(s);
   const char* kn = "gemm";
   hipError_t err = launch_gemm(g, e, c->act, s, &kn);
-  c->prof_stop(pi, s, kn, 2.0 * g.M * g.N * (k_alg < 0 ? g.K : k_alg), 0.0);
+  c->prof_stop(pi, s, kn, 2.0 * g.M * g.N * ((k_alg < 0 ? g.K : k_alg) + g.K2), 0.0);
   return err;
 }
 
@@ -418,9 +513,14 @@ zl_status zl_chunk_create(const zl_config* cfg, const zl_buffers* bufs, void* wo
     return fail(ZL_ERR_INVALID_ARG, "head_w and head_norm_w required");
   if (cfg->arch == ZL_ARCH_GPT2 && !bufs->head_norm_b)
     return fail(ZL_ERR_INVALID_ARG, "gpt2 needs head_norm_b");
+  if (cfg->lora_rank && !bufs->base_master)
+    return fail(ZL_ERR_INVALID_ARG, "LoRA mode needs base_master");
+  if (cfg->lora_rank && cfg->dtype == ZL_BF16 && !bufs->base_shadow)
+    return fail(ZL_ERR_INVALID_ARG, "LoRA in bf16 mode needs base_shadow");
   const uintptr_t al = (uintptr_t)bufs->master | (uintptr_t)bufs->grad |
                        (uintptr_t)bufs->head_w | (uintptr_t)(bufs->shadow) |
-                       (uintptr_t)bufs->adam_m | (uintptr_t)bufs->adam_v;
+                       (uintptr_t)bufs->adam_m | (uintptr_t)bufs->adam_v |
+                       (uintptr_t)bufs->base_master | (uintptr_t)bufs->base_shadow;
   if (al % 16) return fail(ZL_ERR_INVALID_ARG, "buffers must be 16-byte aligned");
   Plan p;
   build_plan(*cfg, p);
@@ -467,6 +567,9 @@ zl_status zl_refresh_shadow(zl_chunk* c, void* stream) {
   if (c->act != BF16) return ZL_OK;
   ZL_HIP(launch_shadow(c->buf.master, reinterpret_cast<bf16_t*>(c->buf.shadow),
                        c->layout.n_params, S_(stream)));
+  if (c->m.lr)
+    ZL_HIP(launch_shadow(c->buf.base_master, reinterpret_cast<bf16_t*>(c->buf.base_shadow),
+                         c->layout.n_base, S_(stream)));
   return ZL_OK;
 }
 
@@ -537,8 +640,36 @@ zl_status zl_chunk_forward(zl_chunk* c, const void* h_in, const int32_t* seq_len
   ZL_RUN("copy_inputs", 0, B * 8, launch_copy_i32(seq_lens, sl, B, 1, 0, S, s));
   ZL_RUN("copy_inputs", 0, (double)T * 8, launch_copy_i32(pos_ids, pos, T, 1, 1, S, s));
   ZL_RUN("cast", 0, (double)T * m.d * (4 + c->asz()), launch_cast(h_in, act, c->at<float>(p.X[0]), F32, (size_t)T * m.d, s));
+  // LoRA (Delta w_l = B_l A_l of Sec. II.A on the frozen w_l): for the
+  // projections reading x, xa = s x A^T over their stacked A factors
+  // [na, in]; the projection's GEMM then takes xa and its B factors as a
+  // second K segment, y = x W^T + xa B^T, in the same accumulators (before
+  // bias, RoPE, activation or residual).  Projections sharing x (q/k/v,
+  // gate/up) each see only their own block of xa: their B factors are
+  // expanded block-diagonally to [out, na].
+  const int r = m.lr;
+  auto lora_fwd = [&](const void* x, int in, size_t a_off, int na, void* xa, size_t b_off,
+                      int nblk, const int* widths, int out, GemmDesc& g) -> hipError_t {
+    EpiArgs ea = epi(EPI_STORE, xa, na, act);
+    ea.scale = m.ls;
+    hipError_t err = run_gemm(c, s, gdesc(T, na, in, x, in, true, c->WT(a_off), in, true), ea);
+    const void* b2 = c->WT(b_off);
+    if (err == hipSuccess && nblk > 1) {
+      void* bd = c->ws + p.LBD;
+      const int b1 = widths[0], bnd2 = nblk > 2 ? widths[0] + widths[1] : out;
+      const int pi = c->prof_start(s);
+      err = launch_blockdiag(b2, bd, act, out, r, nblk, b1, bnd2, s);
+      c->prof_stop(pi, s, "lora_blockdiag", 0, (double)out * (r + na) * c->asz());
+      b2 = bd;
+    }
+    g.K2 = na; g.A2 = xa; g.lda2 = na; g.B2 = b2; g.ldb2 = na;
+    return err;
+  };
+  const int w_qkv[3] = {m.dq, m.dkv, m.dkv}, w_up[2] = {m.ff, m.ff};
+  const int n_qkv = m.llama ? 3 : 1, n_up = m.llama ? 2 : 1;
   for (int l = 0; l < m.L; ++l) {
     const LayerOff& o = c->layout.lay[l];
+    const LoraOff* lo = r ? &c->layout.lora[l] : nullptr;
     float* X = c->at<float>(p.X[l]);
     float* X2 = c->at<float>(p.X2[l]);
     void* N1 = c->ws + p.N1[l];
@@ -559,7 +690,9 @@ zl_status zl_chunk_forward(zl_chunk* c, const void* h_in, const int32_t* seq_len
         e.pos = pos; e.rope = c->at<float2>(p.rope); e.max_pos = c->cfg.max_seq;
         e.hd = m.hd; e.n_rot = (m.hq + m.hkv) * m.hd;
       }
-      ZL_HIP(run_gemm(c, s, gdesc(T, m.nqkv, m.d, N1, m.d, true, c->W(o.w_qkv), m.d, true), e));
+      GemmDesc g = gdesc(T, m.nqkv, m.d, N1, m.d, true, c->W(o.w_qkv), m.d, true);
+      if (r) ZL_HIP(lora_fwd(N1, m.d, lo->qkv_a, m.nqa, c->ws + p.LXQ[l], lo->qkv_b, n_qkv, w_qkv, m.nqkv, g));
+      ZL_HIP(run_gemm(c, s, g, e));
     }
     if (m.llama && !rope_in_gemm)
       ZL_RUN("rope", 0, 2.0 * T * (m.hq + m.hkv) * m.hd * c->asz(),
@@ -581,26 +714,34 @@ zl_status zl_chunk_forward(zl_chunk* c, const void* h_in, const int32_t* seq_len
       EpiArgs e = epi(EPI_RESID, X2, m.d, F32);
       e.resid = X; e.ldr = m.d;
       e.bias = ln ? c->V32(o.b_o) : nullptr;
-      ZL_HIP(run_gemm(c, s, gdesc(T, m.d, m.dq, O, m.dq, true, c->W(o.w_o), m.dq, true), e));
+      GemmDesc g = gdesc(T, m.d, m.dq, O, m.dq, true, c->W(o.w_o), m.dq, true);
+      if (r) ZL_HIP(lora_fwd(O, m.dq, lo->o_a, r, c->ws + p.LXO[l], lo->o_b, 1, nullptr, m.d, g));
+      ZL_HIP(run_gemm(c, s, g, e));
     }
     ZL_RUN("norm_fwd", 0, (double)T * m.d * (4 + c->asz()), launch_norm_fwd(ln, X2, m.d, c->V32(o.ln2_w), ln ? c->V32(o.ln2_b) : nullptr, N2, m.d,
                            act, ln ? c->at<float>(p.MU2[l]) : nullptr, c->at<float>(p.RS2[l]),
                            T, m.d, eps, s));
     if (m.llama) {
       EpiArgs e = epi(EPI_STORE, UP, m.nup, act);
-      ZL_HIP(run_gemm(c, s, gdesc(T, m.nup, m.d, N2, m.d, true, c->W(o.w_up), m.d, true), e));
+      GemmDesc g = gdesc(T, m.nup, m.d, N2, m.d, true, c->W(o.w_up), m.d, true);
+      if (r) ZL_HIP(lora_fwd(N2, m.d, lo->up_a, m.nua, c->ws + p.LXU[l], lo->up_b, n_up, w_up, m.nup, g));
+      ZL_HIP(run_gemm(c, s, g, e));
       ZL_RUN("swiglu_fwd", 0, 3.0 * T * m.ff * c->asz(), launch_swiglu_fwd(UP, m.nup, ACT, m.ff, act, T, m.ff, s));
     } else {
       EpiArgs e = epi(EPI_GELU, ACT, m.ff, act);
       e.out2 = UP; e.ldo2 = m.nup;
       e.bias = c->V32(o.b_up);
-      ZL_HIP(run_gemm(c, s, gdesc(T, m.ff, m.d, N2, m.d, true, c->W(o.w_up), m.d, true), e));
+      GemmDesc g = gdesc(T, m.ff, m.d, N2, m.d, true, c->W(o.w_up), m.d, true);
+      if (r) ZL_HIP(lora_fwd(N2, m.d, lo->up_a, m.nua, c->ws + p.LXU[l], lo->up_b, 1, nullptr, m.ff, g));
+      ZL_HIP(run_gemm(c, s, g, e));
     }
     {
       EpiArgs e = epi(EPI_RESID, c->at<float>(p.X[l + 1]), m.d, F32);
       e.resid = X2; e.ldr = m.d;
       e.bias = ln ? c->V32(o.b_down) : nullptr;
-      ZL_HIP(run_gemm(c, s, gdesc(T, m.d, m.ff, ACT, m.ff, true, c->W(o.w_down), m.ff, true), e));
+      GemmDesc g = gdesc(T, m.d, m.ff, ACT, m.ff, true, c->W(o.w_down), m.ff, true);
+      if (r) ZL_HIP(lora_fwd(ACT, m.ff, lo->down_a, r, c->ws + p.LXD[l], lo->down_b, 1, nullptr, m.d, g));
+      ZL_HIP(run_gemm(c, s, g, e));
     }
   }
   ZL_RUN("cast", 0, (double)T * m.d * (4 + c->asz()), launch_cast(c->at<float>(p.X[m.L]), F32, h_out, act, (size_t)T * m.d, s));
@@ -640,13 +781,13 @@ zl_status zl_local_objective(zl_chunk* c, const int32_t* labels, float* loss_out
       EpiArgs e = epi(EPI_GELU, c->ws + p.AG, m.ar, act);
       e.out2 = c->ws + p.AU;
       e.ldo2 = m.ar;
-      ZL_HIP(run_gemm(c, s, gdesc(T, m.ar, m.d, xo, m.d, true, c->W(c->layout.ad_w1), m.d, true), e));
+      ZL_HIP(run_gemm(c, s, gdesc(T, m.ar, m.d, xo, m.d, true, c->WT(c->layout.ad_w1), m.d, true), e));
     }
     {
       EpiArgs e = epi(EPI_RESID, c->at<float>(p.AHP), m.d, F32);
       e.resid = hout;
       e.ldr = m.d;
-      ZL_HIP(run_gemm(c, s, gdesc(T, m.d, m.ar, c->ws + p.AG, m.ar, true, c->W(c->layout.ad_w2), m.ar,
+      ZL_HIP(run_gemm(c, s, gdesc(T, m.d, m.ar, c->ws + p.AG, m.ar, true, c->WT(c->layout.ad_w2), m.ar,
                                true), e));
     }
     hout = c->at<float>(p.AHP);
@@ -689,14 +830,14 @@ zl_status zl_local_objective(zl_chunk* c, const int32_t* labels, float* loss_out
       EpiArgs e = epi(EPI_GELU_BWD, c->ws + p.ADU, m.ar, act);
       e.aux = c->ws + p.AU;
       e.ldaux = m.ar;
-      ZL_HIP(run_gemm(c, s, gdesc(T, m.ar, m.d, c->ws + p.ADHPA, m.d, true, c->W(c->layout.ad_w2),
+      ZL_HIP(run_gemm(c, s, gdesc(T, m.ar, m.d, c->ws + p.ADHPA, m.d, true, c->WT(c->layout.ad_w2),
                                m.ar, false), e));
     }
     {
       EpiArgs e = epi(EPI_RESID, c->at<float>(p.DX), m.d, F32);
       e.resid = c->at<float>(p.ADHP);
       e.ldr = m.d;
-      ZL_HIP(run_gemm(c, s, gdesc(T, m.d, m.ar, c->ws + p.ADU, m.ar, true, c->W(c->layout.ad_w1), m.d,
+      ZL_HIP(run_gemm(c, s, gdesc(T, m.d, m.ar, c->ws + p.ADU, m.ar, true, c->WT(c->layout.ad_w1), m.d,
                                false), e));
     }
     ZL_RUN("cast", 0, (double)T * m.d * (4 + c->asz()),
@@ -748,6 +889,48 @@ zl_status zl_chunk_backward(zl_chunk* c, float grad_scale, int accumulate, void*
     return e;
   };
 
+  // LoRA backward of projections y_j = x W_j^T + xa_j B_j^T (xa = s x A^T),
+  // j over the column blocks of dy [T, out]: E_j = s dy_j B_j into LE
+  // [T, na]; the data gradient dy W + E A takes (E, A) as its GEMM's second
+  // K segment (when dx is needed); then dA = E^T x and dB_j = dy_j^T xa_j.
+  // The frozen W_j get no gradient.
+  const int r = m.lr;
+  const size_t asz = c->asz();
+  void* LE = c->ws + p.LE;
+  auto lora_bwd_dx = [&](const void* dy, int out, size_t a_off, int na, size_t b_off,
+                         const int* widths, int nblk, int in, bool need_dx,
+                         GemmDesc& g) -> hipError_t {
+    hipError_t err = hipSuccess;
+    int col = 0;
+    size_t boff = b_off;
+    for (int j = 0; j < nblk && err == hipSuccess; ++j) {
+      EpiArgs ee = epi(EPI_STORE, static_cast<char*>(LE) + (size_t)j * r * asz, na, act);
+      ee.scale = m.ls;
+      err = run_gemm(c, s, gdesc(T, r, widths[j], static_cast<const char*>(dy) + (size_t)col * asz,
+                                 out, true, c->WT(boff), r, false), ee);
+      col += widths[j];
+      boff += (size_t)widths[j] * r;
+    }
+    if (need_dx) { g.K2 = na; g.A2 = LE; g.lda2 = na; g.B2 = c->WT(a_off); g.ldb2 = in; }
+    return err;
+  };
+  auto lora_bwd_w = [&](const void* dy, int out, const void* x, int in, size_t a_off, int na,
+                        const void* xa, size_t b_off, const int* widths, int nblk) -> hipError_t {
+    hipError_t err = wgrad(na, in, LE, na, x, in, a_off);
+    int col = 0;
+    size_t boff = b_off;
+    for (int j = 0; j < nblk && err == hipSuccess; ++j) {
+      err = wgrad(widths[j], r, static_cast<const char*>(dy) + (size_t)col * asz, out,
+                  static_cast<const char*>(xa) + (size_t)j * r * asz, na, boff);
+      col += widths[j];
+      boff += (size_t)widths[j] * r;
+    }
+    return err;
+  };
+  const int w_qkv[3] = {m.dq, m.dkv, m.dkv}, w_qkv1[1] = {m.nqkv};
+  const int w_up[2] = {m.ff, m.ff}, w_up1[1] = {m.ff}, w_d[1] = {m.d};
+  const int n_qkv = m.llama ? 3 : 1, n_up = m.llama ? 2 : 1;
+
   if (m.ar) {  // readout adapter weights: dW2 = dh'^T A, dW1 = dU^T h_out
     ZL_HIP(wgrad(m.d, m.ar, c->ws + p.ADHPA, m.d, c->ws + p.AG, m.ar, c->layout.ad_w2));
     const void* xo = act == BF16 ? (const void*)(c->ws + p.AXO) : (const void*)c->at<float>(p.X[m.L]);
@@ -755,38 +938,65 @@ zl_status zl_chunk_backward(zl_chunk* c, float grad_scale, int accumulate, void*
   }
   for (int l = m.L - 1; l >= 0; --l) {
     const LayerOff& o = c->layout.lay[l];
+    const LoraOff* lo = r ? &c->layout.lora[l] : nullptr;
     bool rope_fused = false;
     // down projection
     {
       EpiArgs e = epi(m.llama ? EPI_SWIGLU_BWD : EPI_GELU_BWD, DUP, m.nup, act);
       e.aux = c->ws + p.UP[l]; e.ldaux = m.nup; e.ff = m.ff;
-      ZL_HIP(run_gemm(c, s, gdesc(T, m.ff, m.d, DXA, m.d, true, c->W(o.w_down), m.ff, false), e));
+      GemmDesc g = gdesc(T, m.ff, m.d, DXA, m.d, true, c->W(o.w_down), m.ff, false);
+      if (r) ZL_HIP(lora_bwd_dx(DXA, m.d, lo->down_a, r, lo->down_b, w_d, 1, m.ff, true, g));
+      ZL_HIP(run_gemm(c, s, g, e));
     }
-    ZL_HIP(wgrad(m.d, m.ff, DXA, m.d, c->ws + p.ACT[l], m.ff, o.w_down));
-    if (ln) ZL_HIP(bias_grad(DX, F32, m.d, o.b_down));
+    if (r) {
+      ZL_HIP(lora_bwd_w(DXA, m.d, c->ws + p.ACT[l], m.ff, lo->down_a, r, c->ws + p.LXD[l],
+                        lo->down_b, w_d, 1));
+    } else {
+      ZL_HIP(wgrad(m.d, m.ff, DXA, m.d, c->ws + p.ACT[l], m.ff, o.w_down));
+      if (ln) ZL_HIP(bias_grad(DX, F32, m.d, o.b_down));
+    }
     // up projection (gate|up or fc)
     {
       EpiArgs e = epi(EPI_STORE, DN, m.d, F32);
-      ZL_HIP(run_gemm(c, s, gdesc(T, m.d, m.nup, DUP, m.nup, true, c->W(o.w_up), m.d, false), e));
+      GemmDesc g = gdesc(T, m.d, m.nup, DUP, m.nup, true, c->W(o.w_up), m.d, false);
+      if (r)
+        ZL_HIP(lora_bwd_dx(DUP, m.nup, lo->up_a, m.nua, lo->up_b, m.llama ? w_up : w_up1, n_up,
+                           m.d, true, g));
+      ZL_HIP(run_gemm(c, s, g, e));
     }
-    ZL_HIP(wgrad(m.nup, m.d, DUP, m.nup, c->ws + p.N2[l], m.d, o.w_up));
-    if (ln) ZL_HIP(bias_grad(DUP, act, m.nup, o.b_up));
+    if (r) {
+      ZL_HIP(lora_bwd_w(DUP, m.nup, c->ws + p.N2[l], m.d, lo->up_a, m.nua, c->ws + p.LXU[l],
+                        lo->up_b, m.llama ? w_up : w_up1, n_up));
+    } else {
+      ZL_HIP(wgrad(m.nup, m.d, DUP, m.nup, c->ws + p.N2[l], m.d, o.w_up));
+      if (ln) ZL_HIP(bias_grad(DUP, act, m.nup, o.b_up));
+    }
     // norm 2
     {
       int nblk = 0;
       ZL_RUN("norm_bwd", 0, (double)T * m.d * (16 + c->asz()), launch_norm_bwd(ln, DN, c->at<float>(p.X2[l]), c->V32(o.ln2_w),
                              ln ? c->at<float>(p.MU2[l]) : nullptr, c->at<float>(p.RS2[l]), DX, DX,
-                             DXA, act, PART, ln ? PART + half_part : nullptr, T, m.d, s, &nblk));
-      ZL_RUN("reduce_rows", 0, 0, launch_reduce_rows(PART, nblk, m.d, c->G(o.ln2_w), grad_scale, acc, s));
-      if (ln) ZL_RUN("reduce_rows", 0, 0, launch_reduce_rows(PART + half_part, nblk, m.d, c->G(o.ln2_b), grad_scale, acc, s));
+                             DXA, act, r ? nullptr : PART, ln && !r ? PART + half_part : nullptr,
+                             T, m.d, s, &nblk));
+      if (!r) {
+        ZL_RUN("reduce_rows", 0, 0, launch_reduce_rows(PART, nblk, m.d, c->G(o.ln2_w), grad_scale, acc, s));
+        if (ln) ZL_RUN("reduce_rows", 0, 0, launch_reduce_rows(PART + half_part, nblk, m.d, c->G(o.ln2_b), grad_scale, acc, s));
+      }
     }
     // output projection
     {
       EpiArgs e = epi(EPI_STORE, DO, m.dq, act);
-      ZL_HIP(run_gemm(c, s, gdesc(T, m.dq, m.d, DXA, m.d, true, c->W(o.w_o), m.dq, false), e));
+      GemmDesc g = gdesc(T, m.dq, m.d, DXA, m.d, true, c->W(o.w_o), m.dq, false);
+      if (r) ZL_HIP(lora_bwd_dx(DXA, m.d, lo->o_a, r, lo->o_b, w_d, 1, m.dq, true, g));
+      ZL_HIP(run_gemm(c, s, g, e));
     }
-    ZL_HIP(wgrad(m.d, m.dq, DXA, m.d, c->ws + p.O[l], m.dq, o.w_o));
-    if (ln) ZL_HIP(bias_grad(DX, F32, m.d, o.b_o));
+    if (r) {
+      ZL_HIP(lora_bwd_w(DXA, m.d, c->ws + p.O[l], m.dq, lo->o_a, r, c->ws + p.LXO[l], lo->o_b,
+                        w_d, 1));
+    } else {
+      ZL_HIP(wgrad(m.d, m.dq, DXA, m.d, c->ws + p.O[l], m.dq, o.w_o));
+      if (ln) ZL_HIP(bias_grad(DX, F32, m.d, o.b_o));
+    }
     // attention
     {
       AttnDesc a;
@@ -812,23 +1022,37 @@ zl_status zl_chunk_backward(zl_chunk* c, float grad_scale, int accumulate, void*
       ZL_RUN("rope", 0, 2.0 * T * (m.hq + m.hkv) * m.hd * c->asz(),
              launch_rope(DQKV, m.nqkv, act, c->at<int32_t>(p.pos), c->at<float2>(p.rope),
                          c->cfg.max_seq, T, m.hq + m.hkv, m.hd, -1, s));
-    // QKV projection
+    // QKV projection.  With LoRA nothing below layer 0's QKV GEMMs is
+    // trained, so its data gradient (feeding only norm-1 weight gradients
+    // and h_in, which is detached) is skipped.
+    const bool need_dn = !r || l > 0;
     {
       EpiArgs e = epi(EPI_STORE, DN, m.d, F32);
-      ZL_HIP(run_gemm(c, s, gdesc(T, m.d, m.nqkv, DQKV, m.nqkv, true, c->W(o.w_qkv), m.d, false), e));
+      GemmDesc g = gdesc(T, m.d, m.nqkv, DQKV, m.nqkv, true, c->W(o.w_qkv), m.d, false);
+      if (r)
+        ZL_HIP(lora_bwd_dx(DQKV, m.nqkv, lo->qkv_a, m.nqa, lo->qkv_b, m.llama ? w_qkv : w_qkv1,
+                           n_qkv, m.d, need_dn, g));
+      if (need_dn) ZL_HIP(run_gemm(c, s, g, e));
     }
-    ZL_HIP(wgrad(m.nqkv, m.d, DQKV, m.nqkv, c->ws + p.N1[l], m.d, o.w_qkv));
-    if (ln) ZL_HIP(bias_grad(DQKV, act, m.nqkv, o.b_qkv));
+    if (r) {
+      ZL_HIP(lora_bwd_w(DQKV, m.nqkv, c->ws + p.N1[l], m.d, lo->qkv_a, m.nqa, c->ws + p.LXQ[l],
+                        lo->qkv_b, m.llama ? w_qkv : w_qkv1, n_qkv));
+    } else {
+      ZL_HIP(wgrad(m.nqkv, m.d, DQKV, m.nqkv, c->ws + p.N1[l], m.d, o.w_qkv));
+      if (ln) ZL_HIP(bias_grad(DQKV, act, m.nqkv, o.b_qkv));
+    }
     // norm 1; layer 0 forms no gradient into h_in
-    {
+    if (need_dn) {
       int nblk = 0;
       float* dx = l > 0 ? DX : nullptr;
       ZL_RUN("norm_bwd", 0, (double)T * m.d * (16 + c->asz()), launch_norm_bwd(ln, DN, c->at<float>(p.X[l]), c->V32(o.ln1_w),
                              ln ? c->at<float>(p.MU1[l]) : nullptr, c->at<float>(p.RS1[l]), dx, dx,
-                             l > 0 ? DXA : nullptr, act, PART, ln ? PART + half_part : nullptr, T,
-                             m.d, s, &nblk));
-      ZL_RUN("reduce_rows", 0, 0, launch_reduce_rows(PART, nblk, m.d, c->G(o.ln1_w), grad_scale, acc, s));
-      if (ln) ZL_RUN("reduce_rows", 0, 0, launch_reduce_rows(PART + half_part, nblk, m.d, c->G(o.ln1_b), grad_scale, acc, s));
+                             l > 0 ? DXA : nullptr, act, r ? nullptr : PART,
+                             ln && !r ? PART + half_part : nullptr, T, m.d, s, &nblk));
+      if (!r) {
+        ZL_RUN("reduce_rows", 0, 0, launch_reduce_rows(PART, nblk, m.d, c->G(o.ln1_w), grad_scale, acc, s));
+        if (ln) ZL_RUN("reduce_rows", 0, 0, launch_reduce_rows(PART + half_part, nblk, m.d, c->G(o.ln1_b), grad_scale, acc, s));
+      }
     }
   }
   c->state = ST_IDLE;
@@ -971,16 +1195,22 @@ zl_status zl_device_info(int device, int* cu_count, int* clock_khz, char* arch, 
 }
 
 zl_status zl_kernel_gemm(int M, int N, int K, const void* A, int64_t lda, int a_kmajor,
-                         const void* B, int64_t ldb, int b_kmajor, float* C, int64_t ldc,
+                         const void* B, int64_t ldb, int b_kmajor, int K2, const void* A2,
+                         int64_t lda2, const void* B2, int64_t ldb2, float* C, int64_t ldc,
                          int dtype, void* stream) {
-  if (M < 0 || N < 0 || K < 0 || !A || !B || !C) return fail(ZL_ERR_INVALID_ARG, "bad gemm args");
+  if (M < 0 || N < 0 || K < 0 || K2 < 0 || !A || !B || !C || (K2 > 0 && (!A2 || !B2)))
+    return fail(ZL_ERR_INVALID_ARG, "bad gemm args");
   if (dtype != ZL_F32 && dtype != ZL_BF16) return fail(ZL_ERR_INVALID_ARG, "bad dtype");
   if (dtype == ZL_BF16) {
     const int64_t ca = a_kmajor ? K : M, cb = b_kmajor ? K : N;
     if (ca % 8 || cb % 8 || lda % 8 || ldb % 8 || ((uintptr_t)A | (uintptr_t)B) % 16)
       return fail(ZL_ERR_INVALID_ARG, "bf16 gemm needs 8-element contiguous dims and alignment");
+    const int64_t ca2 = a_kmajor ? K2 : M, cb2 = b_kmajor ? K2 : N;
+    if (K2 > 0 && (ca2 % 8 || cb2 % 8 || lda2 % 8 || ldb2 % 8 || ((uintptr_t)A2 | (uintptr_t)B2) % 16))
+      return fail(ZL_ERR_INVALID_ARG, "bf16 gemm needs 8-element contiguous dims and alignment");
   }
   GemmDesc g = gdesc(M, N, K, A, lda, a_kmajor != 0, B, ldb, b_kmajor != 0);
+  if (K2 > 0) { g.K2 = K2; g.A2 = A2; g.lda2 = lda2; g.B2 = B2; g.ldb2 = ldb2; }
   EpiArgs e = epi(EPI_STORE, C, ldc, F32);
   ZL_HIP(launch_gemm(g, e, dtype == ZL_BF16 ? BF16 : F32, S_(stream)));
   return ZL_OK;

@@ -45,7 +45,8 @@ class zl_config(ctypes.Structure):
                 ("optimizer", ctypes.c_int), ("lr", ctypes.c_float), ("beta1", ctypes.c_float),
                 ("beta2", ctypes.c_float), ("eps", ctypes.c_float),
                 ("weight_decay", ctypes.c_float), ("max_batch", ctypes.c_int),
-                ("max_seq", ctypes.c_int), ("adapter_rank", ctypes.c_int)]
+                ("max_seq", ctypes.c_int), ("adapter_rank", ctypes.c_int),
+                ("lora_rank", ctypes.c_int), ("lora_alpha", ctypes.c_float)]
 
 
 class zl_tensor_desc(ctypes.Structure):
@@ -58,7 +59,8 @@ class zl_buffers(ctypes.Structure):
     _fields_ = [("master", ctypes.c_void_p), ("shadow", ctypes.c_void_p),
                 ("grad", ctypes.c_void_p), ("adam_m", ctypes.c_void_p),
                 ("adam_v", ctypes.c_void_p), ("head_w", ctypes.c_void_p),
-                ("head_norm_w", ctypes.c_void_p), ("head_norm_b", ctypes.c_void_p)]
+                ("head_norm_w", ctypes.c_void_p), ("head_norm_b", ctypes.c_void_p),
+                ("base_master", ctypes.c_void_p), ("base_shadow", ctypes.c_void_p)]
 
 
 class zl_view(ctypes.Structure):
@@ -112,7 +114,7 @@ def load(path=None):
         "zl_status_string": [c],
         "zl_last_error": [],
         "zl_inspect": [vp, ctypes.c_char_p, c, P(zl_view)],
-        "zl_kernel_gemm": [c, c, c, vp, i64, c, vp, i64, c, vp, i64, c, vp],
+        "zl_kernel_gemm": [c, c, c, vp, i64, c, vp, i64, c, c, vp, i64, vp, i64, vp, i64, c, vp],
         "zl_kernel_attention": [c, c, c, c, c, vp, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, vp,
                                 c, c, vp],
         "zl_profile_begin": [vp, c],
@@ -156,10 +158,21 @@ def _check(st, name):
 def make_config(arch, n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ff, vocab, *,
                 norm_eps=1e-5, rope_theta=1e4, dtype=ZL_F32, alpha=0.5, consis=ZL_KL_REVERSE,
                 optimizer=ZL_ADAMW, lr=1e-4, beta1=0.9, beta2=0.999, eps=1e-8,
-                weight_decay=0.01, max_batch=1, max_seq=1, adapter_rank=0):
+                weight_decay=0.01, max_batch=1, max_seq=1, adapter_rank=0, lora_rank=0,
+                lora_alpha=16.0):
     return zl_config(arch, n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ff, vocab,
                      norm_eps, rope_theta, dtype, alpha, consis, optimizer, lr, beta1, beta2,
-                     eps, weight_decay, max_batch, max_seq, adapter_rank)
+                     eps, weight_decay, max_batch, max_seq, adapter_rank, lora_rank, lora_alpha)
+
+
+def base_config(cfg):
+    """The config whose zl_param_layout lays out the frozen base buffers of
+    a LoRA chunk (lora_rank = adapter_rank = 0)."""
+    b = zl_config()
+    ctypes.pointer(b)[0] = cfg
+    b.lora_rank = 0
+    b.adapter_rank = 0
+    return b
 
 
 def zl_param_layout(cfg):
@@ -239,9 +252,10 @@ def zl_inspect(h, name, layer=0):
     return dict(ptr=v.ptr, rows=v.rows, cols=v.cols, ld=v.ld, dtype=v.dtype)
 
 
-def zl_kernel_gemm(M, N, K, A, lda, a_kmajor, B, ldb, b_kmajor, C, ldc, dtype, stream=0):
-    _check(load().zl_kernel_gemm(M, N, K, A, lda, int(a_kmajor), B, ldb, int(b_kmajor), C, ldc,
-                                 dtype, stream), "zl_kernel_gemm")
+def zl_kernel_gemm(M, N, K, A, lda, a_kmajor, B, ldb, b_kmajor, C, ldc, dtype, stream=0,
+                   K2=0, A2=None, lda2=0, B2=None, ldb2=0):
+    _check(load().zl_kernel_gemm(M, N, K, A, lda, int(a_kmajor), B, ldb, int(b_kmajor), K2, A2,
+                                 lda2, B2, ldb2, C, ldc, dtype, stream), "zl_kernel_gemm")
 
 
 def zl_kernel_attention(B, S, Hq, Hkv, hd, q, k, v, ld_qkv, seq_lens, o, lse, dout, dq, dk, dv,

@@ -31,6 +31,9 @@ def make_inputs(shp, seed=0, stress=True, seq_lens=None, drop=0):
     """Seeded parameters and batch; parity cases perturb norms/biases and use
     the stress scale so the consistency term is exercised."""
     params = workload.init_params(workload.param_specs(shp), seed=seed, perturb=True, stress=stress)
+    if getattr(shp, "lora_rank", 0):  # the frozen base of a LoRA chunk
+        params.update(workload.init_params(workload.base_specs(shp), seed=seed + 50, perturb=True,
+                                           stress=stress))
     batch = workload.make_batch(shp, stress=stress, seq_lens=seq_lens, perturb_head=True)
     if drop:
         rng = np.random.default_rng(seed + 7)

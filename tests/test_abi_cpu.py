@@ -71,6 +71,55 @@ def test_layout_matches_workload_specs(adapter_rank):
                                              rope_theta=5e5))[0] >= 1_744_896_000
 
 
+@pytest.mark.parametrize("adapter_rank", [0, 16])
+def test_lora_layout_matches_workload_specs(adapter_rank):
+    """With LoRA the trainable layout is the factors (and adapter) in
+    param_specs order; the base buffers follow the full layout of the config
+    without LoRA and adapter; stacked factors are adjacent."""
+    import workload
+    for name, r in (("tiny", 8), ("gpt2", 16), ("8b", 8)):
+        shp = workload.get_config(name, adapter_rank=adapter_rank, lora_rank=r)
+        arch = zl.ZL_ARCH_LLAMA if shp.arch == "llama" else zl.ZL_ARCH_GPT2
+        cfg = zl.make_config(arch, shp.n_layers, shp.d_model, shp.n_heads, shp.n_kv_heads,
+                             shp.head_dim, shp.d_ff, shp.vocab, rope_theta=max(shp.rope_theta, 2.0),
+                             max_batch=1, max_seq=8, adapter_rank=adapter_rank, lora_rank=r)
+        n, lay = zl.zl_param_layout(cfg)
+        specs = workload.param_specs(shp)
+        assert [f"L{t['layer']}.{t['name']}" for t in lay] == [k for k, _, _ in specs]
+        for t, (_, shape, _) in zip(lay, specs):
+            assert tuple(t["shape"]) == tuple(shape) and t["offset"] % 64 == 0
+        assert n >= max(t["offset"] + t["numel"] for t in lay)
+        nb, base = zl.zl_param_layout(zl.base_config(cfg))
+        assert [f"L{t['layer']}.{t['name']}" for t in base] == \
+            [k for k, _, _ in workload.base_specs(shp)]
+        if name == "8b":
+            assert n * 100 < nb
+        by = {(t["layer"], t["name"]): t for t in lay}
+        groups = ([("wq_la", "wk_la", "wv_la"), ("wq_lb", "wk_lb", "wv_lb"), ("wg_la", "wu_la"),
+                   ("wg_lb", "wu_lb")] if shp.arch == "llama" else [])
+        for l in range(shp.n_layers):
+            for g in groups:
+                for a, b in zip(g, g[1:]):
+                    assert by[(l, b)]["offset"] == by[(l, a)]["offset"] + by[(l, a)]["numel"]
+
+
+@pytest.mark.parametrize("rank,lalpha", [(-8, 16.0), (4, 16.0), (12, 16.0), (264, 16.0),
+                                         (8, 0.0), (8, float("nan"))])
+def test_lora_rank_validated(rank, lalpha):
+    b = ctypes.c_size_t()
+    cfg = _cfg(lora_rank=rank, lora_alpha=lalpha)
+    assert zl.load().zl_workspace_size(ctypes.byref(cfg), ctypes.byref(b)) == zl.ZL_ERR_INVALID_ARG
+
+
+def test_lora_create_needs_base_buffers():
+    for dtype, bufs in ((zl.ZL_F32, zl.zl_buffers(4096, 0, 8192, 12288, 16384, 20480, 24576, 0)),
+                        (zl.ZL_BF16, zl.zl_buffers(4096, 32768, 8192, 12288, 16384, 20480, 24576, 0,
+                                                   28672, 0))):
+        with pytest.raises(zl.ZlError) as ei:
+            zl.zl_chunk_create(_cfg(lora_rank=8, dtype=dtype), bufs, 256, 1 << 40)
+        assert ei.value.status == zl.ZL_ERR_INVALID_ARG and "base" in str(ei.value)
+
+
 @pytest.mark.parametrize("rank", [-16, 8, 24])
 def test_adapter_rank_validated(rank):
     import ctypes

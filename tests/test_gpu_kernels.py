@@ -61,6 +61,71 @@ def test_gemm_layouts(dtype, layout, M, N, K):
     assert rel_err(got, ref) < 2e-6
 
 
+def _gemm_operands(rng, layout, M, N, K, tdt):
+    a_k = layout in ("nt", "nn")
+    b_k = layout == "nt"
+    A = rng.standard_normal((M, K) if a_k else (K, M)).astype(np.float32)
+    B = rng.standard_normal((N, K) if b_k else (K, N)).astype(np.float32)
+    return (torch.tensor(A, device=_dev()).to(tdt), torch.tensor(B, device=_dev()).to(tdt), a_k, b_k)
+
+
+def _gemm_ref(At, Bt, a_k, b_k):
+    a64 = At.double().cpu().numpy()
+    b64 = Bt.double().cpu().numpy()
+    return (a64 if a_k else a64.T) @ (b64 if b_k else b64.T).T
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("layout", ["nt", "nn", "tn"])
+@pytest.mark.parametrize("M,N,K,K2", [(304, 520, 200, 8), (4096, 3848, 264, 48),
+                                      (512, 768, 4096, 16), (136, 64, 8, 200)])
+def test_gemm_second_segment(dtype, layout, M, N, K, K2):
+    """C = A B^T + A2 B2^T with the second pair in the layouts of the first
+    (the low-rank term of a LoRA projection), ragged in every dimension."""
+    zl = _zl()
+    if dtype == "f32" and M * N * (K + K2) > 1e9:
+        pytest.skip("fp32 SIMT path is sized for small problems")
+    rng = np.random.default_rng(M + N + K + K2)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    At, Bt, a_k, b_k = _gemm_operands(rng, layout, M, N, K, tdt)
+    A2, B2, _, _ = _gemm_operands(rng, layout, M, N, K2, tdt)
+    C = torch.full((M, N), float("nan"), dtype=torch.float32, device=_dev())
+    torch.cuda.synchronize()
+    zl.zl_kernel_gemm(M, N, K, At.data_ptr(), At.shape[1], a_k, Bt.data_ptr(), Bt.shape[1], b_k,
+                      C.data_ptr(), N, zl.ZL_BF16 if dtype == "bf16" else zl.ZL_F32, _stream(),
+                      K2=K2, A2=A2.data_ptr(), lda2=A2.shape[1], B2=B2.data_ptr(), ldb2=B2.shape[1])
+    torch.cuda.synchronize()
+    ref = _gemm_ref(At, Bt, a_k, b_k) + _gemm_ref(A2, B2, a_k, b_k)
+    got = C.cpu().double().numpy()
+    assert np.all(np.isfinite(got))
+    assert rel_err(got, ref) < 2e-6
+
+
+def test_gemm_register_staged_path_with_second_segment():
+    """Both operands MN-major with A's row stride 16384 and K = 66000: A's
+    tile offsets pass 2^31 bytes, so the direct-to-LDS kernel is not used and
+    the register-staged MFMA kernel computes C = A B^T + A2 B2^T."""
+    zl = _zl()
+    M, N, K, K2, lda = 256, 256, 66000, 16, 16384
+    rng = np.random.default_rng(5)
+    A = torch.zeros((K, lda), dtype=torch.bfloat16, device=_dev())
+    A[:, :M] = torch.tensor(rng.standard_normal((K, M)).astype(np.float32), device=_dev()).to(torch.bfloat16)
+    Bt = torch.tensor(rng.standard_normal((K, N)).astype(np.float32), device=_dev()).to(torch.bfloat16)
+    A2 = torch.tensor(rng.standard_normal((K2, M)).astype(np.float32), device=_dev()).to(torch.bfloat16)
+    B2 = torch.tensor(rng.standard_normal((K2, N)).astype(np.float32), device=_dev()).to(torch.bfloat16)
+    C = torch.full((M, N), float("nan"), dtype=torch.float32, device=_dev())
+    torch.cuda.synchronize()
+    zl.zl_kernel_gemm(M, N, K, A.data_ptr(), lda, False, Bt.data_ptr(), N, False, C.data_ptr(), N,
+                      zl.ZL_BF16, _stream(), K2=K2, A2=A2.data_ptr(), lda2=M, B2=B2.data_ptr(),
+                      ldb2=N)
+    torch.cuda.synchronize()
+    ref = _gemm_ref(A[:, :M], Bt, False, False) + _gemm_ref(A2, B2, False, False)
+    del A
+    got = C.cpu().double().numpy()
+    assert np.all(np.isfinite(got))
+    assert rel_err(got, ref) < 2e-6
+
+
 def _attn_inputs(B, S, Hq, Hkv, hd, lens, seed):
     rng = np.random.default_rng(seed)
     q = rng.standard_normal((B, S, Hq, hd)).astype(np.float32)

@@ -46,6 +46,11 @@ def _run_device(shp, params, batch, steps=1, **kw):
         ch.step()
         out["masters"].append(ch.tensors(ch.master))
     out["h_in_after"] = d["h_in"].double().cpu().numpy()
+    if ch.base_master is not None:  # LoRA: the frozen base is never written
+        torch.cuda.synchronize()
+        for k, t in ch.base_by_key.items():
+            got = ch.base_master[t["offset"]: t["offset"] + t["numel"]].cpu().numpy()
+            np.testing.assert_array_equal(got, np.asarray(params[k], np.float32).reshape(-1), err_msg=k)
     ch.close()
     return out
 
@@ -80,7 +85,7 @@ def _compare(shp, dev, ref, tol, lr, optimizer, gate_adam_delta=True):
         for k in ref["grads"][s]:
             report[f"g{s}:{k}"] = rel_err(dev["grads"][s][k], ref["grads"][s][k])
     for s in range(1, len(dev["masters"])):
-        for k in ref["masters"][s]:
+        for k in dev["masters"][s]:  # the trainable tensors (LoRA: not the frozen base)
             report[f"p{s}:{k}"] = rel_err(dev["masters"][s][k], ref["masters"][s][k])
             dd = dev["masters"][s][k] - dev["masters"][s - 1][k]
             rd = ref["masters"][s][k] - ref["masters"][s - 1][k]
@@ -269,3 +274,70 @@ def test_readout_adapter_with_zero_output_is_the_static_head(dtype):
     for k in g0:
         np.testing.assert_array_equal(g0[k], g1[k], err_msg=k)
     assert not np.any(g1[f"L{L}.ad_w1"])
+
+
+# ------------------------------------------------------------------- LoRA
+# Eq. (6) on the LoRA factors of Sec. II.A: every linear is
+# x W^T + s (x A^T) B^T with W, norms and biases frozen.
+@pytest.mark.parametrize("alpha", [0.5, 1.0])
+def test_tiny_fp32_lora(alpha):
+    _case(TINY.with_(lora_rank=8, lora_alpha=24.0), alpha=alpha, seq_lens=[32, 17, 1, 9], drop=5)
+
+
+def test_tiny_fp32_lora_with_adapter_three_steps():
+    _case(TINY.with_(lora_rank=8, adapter_rank=16), steps=3, lr=1e-3)
+
+
+def test_tiny_gqa_fp32_lora_sgd():
+    _case(TINY.with_(n_kv_heads=2, name="tiny-gqa", lora_rank=16), optimizer="sgd", lr=0.05,
+          alpha=0.7, consis="forward")
+
+
+def test_tiny_gpt2_fp32_lora():
+    shp = workload.configs.ChunkShape("tiny-gpt2", "gpt2", 2, 64, 4, 4, 16, 256, 97, 4, 24, "f32",
+                                      0.0, 2, lora_rank=16)
+    _case(shp, alpha=0.5, seq_lens=[24, 20, 3, 24])
+
+
+def test_gpt2_bf16_lora():
+    _case(GPT2.with_(batch=2, seq=128, lora_rank=8), seq_lens=[128, 90], drop=10)
+
+
+def test_llama1b_bf16_one_layer_lora():
+    _case(workload.get_config("1b").with_(n_layers=1, batch=1, seq=512, lora_rank=16))
+
+
+def test_llama8b_bf16_two_layers_lora():
+    _case(workload.get_config("8b").with_(n_layers=2, batch=1, seq=256, lora_rank=8))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_lora_with_zero_B_is_the_base_chunk(dtype):
+    """B = 0: the chunk computes its base model, so the loss and dL/dh_out
+    equal those of the full chunk with the same weights bit for bit, and
+    dA = s (dy B)^T x is exactly 0."""
+    shp = TINY.with_(dtype=dtype)
+    shp_l = shp.with_(lora_rank=8)
+    params, batch = make_inputs(shp_l, seed=0)
+    params = {k: (np.zeros_like(v) if k.endswith("_lb") else v) for k, v in params.items()}
+    full = {k: params[k] for k, _, _ in workload.base_specs(shp)}
+    out = []
+    for s, p in ((shp, full), (shp_l, params)):
+        ch = device_chunk(s, p, batch)
+        d = to_dev(batch, dtype)
+        h = ch.forward(d["h_in"], d["seq_lens"], d["pos_ids"])
+        ch.objective(d["labels"])
+        dh = ch.inspect("dh_out")
+        ch.backward(1.0, 0)
+        torch.cuda.synchronize()
+        out.append((float(ch.loss.item()), h.double().cpu().numpy(), dh, ch.tensors(ch.grad)))
+        ch.close()
+    (l0, h0, dh0, _), (l1, h1, dh1, g1) = out
+    assert l0 == l1
+    np.testing.assert_array_equal(h0, h1)
+    np.testing.assert_array_equal(dh0, dh1)
+    for k, g in g1.items():
+        if k.endswith("_la"):
+            assert not np.any(g), k
+        else:
+            assert np.all(np.isfinite(g)) and np.any(g), k
