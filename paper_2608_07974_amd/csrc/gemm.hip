@@ -12,6 +12,10 @@
 
 #include "common.h"
 
+#ifndef GEMM_IL  // main-loop schedule of the direct-to-LDS kernel
+#define GEMM_IL 1
+#endif
+
 namespace zl {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
@@ -88,6 +92,120 @@ __device__ inline void epilogue(const EpiArgs& e, int M, int N, int m, int n, fl
   }
 }
 
+// Four consecutive columns n .. n+3 of row m.  The vector path (vec: every
+// operand 16-byte aligned, every row stride a multiple of 4, checked once
+// per block) loads and stores 4 elements at once with the same arithmetic
+// as epilogue(); the column tail and unaligned operands take the scalar
+// path.
+__device__ inline float4 ld4f(const float* p) { return *reinterpret_cast<const float4*>(p); }
+__device__ inline void ld4_act(const void* p, int dt, size_t i, float (&v)[4]) {
+  if (dt == BF16) {
+    const uint2 u = *reinterpret_cast<const uint2*>(static_cast<const bf16_t*>(p) + i);
+    v[0] = bf16_to_f32((bf16_t)(u.x & 0xffff)); v[1] = bf16_to_f32((bf16_t)(u.x >> 16));
+    v[2] = bf16_to_f32((bf16_t)(u.y & 0xffff)); v[3] = bf16_to_f32((bf16_t)(u.y >> 16));
+  } else {
+    const float4 f = ld4f(static_cast<const float*>(p) + i);
+    v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
+  }
+}
+__device__ inline void st4_act(void* p, int dt, size_t i, const float (&v)[4]) {
+  if (dt == BF16) {
+    uint2 u;
+    u.x = (uint32_t)f32_to_bf16(v[0]) | ((uint32_t)f32_to_bf16(v[1]) << 16);
+    u.y = (uint32_t)f32_to_bf16(v[2]) | ((uint32_t)f32_to_bf16(v[3]) << 16);
+    *reinterpret_cast<uint2*>(static_cast<bf16_t*>(p) + i) = u;
+  } else {
+    *reinterpret_cast<float4*>(static_cast<float*>(p) + i) = make_float4(v[0], v[1], v[2], v[3]);
+  }
+}
+
+__device__ inline bool epi_vec_ok(const EpiArgs& e) {
+  const uintptr_t p = (uintptr_t)e.out | (uintptr_t)e.bias | (uintptr_t)e.resid |
+                      (uintptr_t)e.out2 | (uintptr_t)e.aux;
+  const int64_t l = e.ldo | e.ldr | e.ldo2 | e.ldaux | (int64_t)e.ff;
+  return (p & 15) == 0 && (l & 3) == 0;
+}
+
+__device__ inline void epilogue4(const EpiArgs& e, int M, int N, int m, int n, const float (&a)[4],
+                                 bool vec) {
+  if (m >= M) return;
+  if (!vec || n + 4 > N) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) epilogue(e, M, N, m, n + i, a[i]);
+    return;
+  }
+  const size_t mo = (size_t)m;
+  float v[4], b[4] = {0.f, 0.f, 0.f, 0.f};
+  if (e.bias && (e.kind == EPI_STORE || e.kind == EPI_RESID || e.kind == EPI_GELU)) {
+    const float4 f = ld4f(e.bias + n);
+    b[0] = f.x; b[1] = f.y; b[2] = f.z; b[3] = f.w;
+  }
+  switch (e.kind) {
+    case EPI_STORE:
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = e.scale * a[i] + b[i];
+      st4_act(e.out, e.out_dtype, mo * e.ldo + n, v);
+      break;
+    case EPI_RESID: {
+      const float4 r = ld4f(e.resid + mo * e.ldr + n);
+      v[0] = r.x + a[0] + b[0]; v[1] = r.y + a[1] + b[1];
+      v[2] = r.z + a[2] + b[2]; v[3] = r.w + a[3] + b[3];
+      st4_act(e.out, F32, mo * e.ldo + n, v);
+      break;
+    }
+    case EPI_GELU: {
+      float h[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        h[i] = a[i] + b[i];
+        if (e.out_dtype == BF16) h[i] = bf16_to_f32(f32_to_bf16(h[i]));  // as stored
+        v[i] = gelu_f(h[i]);
+      }
+      st4_act(e.out2, e.out_dtype, mo * e.ldo2 + n, h);
+      st4_act(e.out, e.out_dtype, mo * e.ldo + n, v);
+      break;
+    }
+    case EPI_GRAD: {
+      float* o = static_cast<float*>(e.out) + mo * e.ldo + n;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = e.scale * a[i];
+      if (e.accumulate) {
+        const float4 f = ld4f(o);
+        v[0] = f.x + v[0]; v[1] = f.y + v[1]; v[2] = f.z + v[2]; v[3] = f.w + v[3];
+      }
+      st4_act(o, F32, 0, v);
+      break;
+    }
+    case EPI_SWIGLU_BWD: {
+      float g[4], u[4], w[4];
+      ld4_act(e.aux, e.out_dtype, mo * e.ldaux + n, g);
+      ld4_act(e.aux, e.out_dtype, mo * e.ldaux + n + e.ff, u);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float sg = 1.f / (1.f + __expf(-g[i]));
+        const float silu = g[i] * sg;
+        const float dsilu = sg * (1.f + g[i] * (1.f - sg));
+        v[i] = a[i] * u[i] * dsilu;
+        w[i] = a[i] * silu;
+      }
+      st4_act(e.out, e.out_dtype, mo * e.ldo + n, v);
+      st4_act(e.out, e.out_dtype, mo * e.ldo + n + e.ff, w);
+      break;
+    }
+    case EPI_GELU_BWD: {
+      float h[4];
+      ld4_act(e.aux, e.out_dtype, mo * e.ldaux + n, h);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = a[i] * gelu_grad_f(h[i]);
+      st4_act(e.out, e.out_dtype, mo * e.ldo + n, v);
+      break;
+    }
+    case EPI_ROPE:  // rotation already applied by the staged epilogue
+      st4_act(e.out, e.out_dtype, mo * e.ldo + n, a);
+      break;
+  }
+}
+
 // ------------------------------------------------------------- tile order
 // Grouped (GROUP_M row panels) order, then remapped so that the blocks the
 // dispatcher places on one XCD (round-robin over 8) take a contiguous range
@@ -126,6 +244,7 @@ __device__ inline void store_tile(const f32x16_t (&acc)[BM / WM / 32][BN / WN / 
   constexpr int LDW = TN + 4;
   static_assert(WM * WN * 32 * LDW * 4 <= 160 * 1024, "epilogue tile exceeds LDS");
   float* ep = reinterpret_cast<float*>(smem) + wave * 32 * LDW;
+  const bool vec = epi_vec_ok(e);
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
 #pragma unroll
@@ -135,29 +254,38 @@ __device__ inline void store_tile(const f32x16_t (&acc)[BM / WM / 32][BN / WN / 
         ep[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * LDW + j * 32 + (lane & 31)] = acc[i][j][r];
     __syncthreads();
     const int mb = m0 + wm * TM + i * 32, nb = n0 + wn * TN;
+    // 4 consecutive columns per lane: a row of TN columns takes TN / 4 lanes
+    constexpr int QPR = TN / 4;
     if (e.kind == EPI_ROPE) {
-      // wave tiles are head-aligned (nb % hd == 0, TN % hd == 0), so the
-      // partner column j +- hd/2 of a head lives in the same staged row
+      // wave tiles are head-aligned (nb % hd == 0, TN % hd == 0) and half =
+      // hd / 2 is a multiple of 4, so the partner columns j +- hd/2 of a
+      // 4-column group are again 4 consecutive columns of the staged row
       const int half = e.hd >> 1;
-      for (int t = lane; t < 32 * TN; t += 64) {
-        const int row = t / TN, col = t % TN;
+      for (int t = lane; t < 32 * QPR; t += 64) {
+        const int row = t / QPR, col = (t % QPR) * 4;
         const int n = nb + col, m = mb + row;
-        float v = ep[row * LDW + col];
+        const float4 x = *reinterpret_cast<const float4*>(&ep[row * LDW + col]);
+        float v[4] = {x.x, x.y, x.z, x.w};
         if (n < e.n_rot && m < g.M) {
           const int j = n % e.hd;
           const bool lo = j < half;
-          const float pv = ep[row * LDW + (lo ? col + half : col - half)];
+          const float4 y = *reinterpret_cast<const float4*>(&ep[row * LDW + (lo ? col + half : col - half)]);
+          const float pv[4] = {y.x, y.y, y.z, y.w};
           int p = e.pos[m];
           p = p < 0 ? 0 : (p >= e.max_pos ? e.max_pos - 1 : p);
-          const float2 cs = e.rope[(int64_t)p * half + (lo ? j : j - half)];
-          v = lo ? v * cs.x - pv * cs.y : v * cs.x + pv * cs.y;
+          const float2* cs = e.rope + (int64_t)p * half + (lo ? j : j - half);
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+            v[k] = lo ? v[k] * cs[k].x - pv[k] * cs[k].y : v[k] * cs[k].x + pv[k] * cs[k].y;
         }
-        epilogue(e, g.M, g.N, m, n, v);
+        epilogue4(e, g.M, g.N, m, n, v, vec);
       }
     } else {
-      for (int t = lane; t < 32 * TN; t += 64) {
-        const int row = t / TN, col = t % TN;
-        epilogue(e, g.M, g.N, mb + row, nb + col, ep[row * LDW + col]);
+      for (int t = lane; t < 32 * QPR; t += 64) {
+        const int row = t / QPR, col = (t % QPR) * 4;
+        const float4 x = *reinterpret_cast<const float4*>(&ep[row * LDW + col]);
+        const float v[4] = {x.x, x.y, x.z, x.w};
+        epilogue4(e, g.M, g.N, mb + row, nb + col, v, vec);
       }
     }
     __syncthreads();
@@ -611,6 +739,45 @@ gemm_dma_kernel(GemmDesc g, EpiArgs e) {
     const int rn = rd + 1 == NST ? 0 : rd + 1;
     const bf16_t* as = reinterpret_cast<const bf16_t*>(smem + rd * STAGE);
     const bf16_t* an = reinterpret_cast<const bf16_t*>(smem + rn * STAGE);
+#if GEMM_IL
+    // Fine interleave: after each MFMA of slice q, the next slice's fragment
+    // reads and this tile's share of the copy are issued in fixed places, so
+    // the matrix pipe of a single wave per SIMD is never left waiting on an
+    // issue burst.
+    static_assert(!RA && !RB, "interleaved schedule uses direct-to-LDS copies");
+#pragma unroll
+    for (int q = 0; q < NS; ++q) {
+      const int cb = q & 1, nb = cb ^ 1;
+      const bf16_t* src = q + 1 < NS ? as : an;
+      const int qs = q + 1 < NS ? q + 1 : 0;
+      if (q + 1 == NS) {
+        wait_vmcnt<(NST - 2) * PER_TILE>();  // this wave's share of tile kt+1
+        __syncthreads();                      // everyone's share; tile kt fully read
+      }
+      constexpr int NMF = FM * FN, NRD = FM + FN, TOT = TA::ITEMS + TB::ITEMS;
+      const int lo = q < DS ? q * TOT / DS : 0, hi = q < DS ? (q + 1) * TOT / DS : 0;
+      const int span = hi > lo ? hi - lo : 1;
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int t = 0; t < NMF; ++t) {
+        acc[t / FN][t % FN] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            af[cb][t / FN], bfr[cb][t % FN], acc[t / FN][t % FN], 0, 0, 0);
+#pragma unroll
+        for (int r = 0; r < NRD; ++r) {
+          if (r * NMF / NRD != t) continue;
+          if (r < FM) af[nb][r] = fa.read(src, qs, r);
+          else bfr[nb][r - FM] = fb.read(src + BM * BK, qs, r - FM);
+        }
+#pragma unroll
+        for (int u = 0; u < TOT; ++u) {
+          if (u < lo || u >= hi || (u - lo) * NMF / span != t) continue;
+          if (u < TA::ITEMS) da.issue_one(u, dst, wave, k0n, g.ka, ra);
+          else db.issue_one(u - TA::ITEMS, dst + ABYTES, wave, k0n, g.kb, rb);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+#else
 #pragma unroll
     for (int q = 0; q < NS; ++q) {
       const int cb = q & 1, nb = cb ^ 1;
@@ -650,6 +817,7 @@ gemm_dma_kernel(GemmDesc g, EpiArgs e) {
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cb][i], bfr[cb][j], acc[i][j], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
+#endif
     rd = rn;
     wr = wr + 1 == NST ? 0 : wr + 1;
   }
@@ -789,6 +957,7 @@ static const char* layout_tag(bool ak, bool bk) {
 #ifndef GEMM_RB
 #define GEMM_RB false
 #endif
+
 
 template <int BM, int BN, int WM, int WN, int BK, int NST, bool AK, bool BKM>
 static hipError_t run_dma(const GemmDesc& g, const EpiArgs& e, hipStream_t s) {
