@@ -129,8 +129,9 @@ hipError_t launch_head_norm_bwd(bool layernorm, const float* dy, int64_t lddy, c
                                 const float* w, const float* mean, const float* rstd,
                                 int rstd_stride, float* dx, void* dx_act, int act_dtype,
                                 int row0, int rows, int d, hipStream_t s);
-// out[j] = (accumulate ? out[j] : 0) + scale * sum_b part[b, j]
-hipError_t launch_reduce_rows(const float* part, int nblk, int d, float* out, float scale,
+// out[j] = (accumulate ? out[j] : 0) + scale * sum_b part[b, j]; part is
+// scratch (a first stage may overwrite some of its rows).
+hipError_t launch_reduce_rows(float* part, int nblk, int d, float* out, float scale,
                               int accumulate, hipStream_t s);
 // Column sums of an act-dtype matrix [T, n] into partials [nblk, n].
 hipError_t launch_colsum_partial(const void* x, int64_t ldx, int dtype, int T, int n,

@@ -13,7 +13,7 @@
 #include "common.h"
 
 #ifndef GEMM_IL  // main-loop schedule of the direct-to-LDS kernel
-#define GEMM_IL 1
+#define GEMM_IL 2
 #endif
 
 namespace zl {
@@ -709,13 +709,16 @@ gemm_dma_kernel(GemmDesc g, EpiArgs e) {
 
   const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>(smem);
   const int nk = (g.K + BK - 1) / BK;
-  // prologue: tiles 0 .. NST-2 (tiles past K are zero-filled, never used)
+  // prologue: tiles 0 .. NST-2, or 0 .. NST-1 when each tile's copy is
+  // issued as soon as its stage is released (tiles past K are zero-filled,
+  // never used)
+  constexpr int PRO = GEMM_IL == 2 ? NST : NST - 1;
 #pragma unroll
-  for (int t = 0; t < NST - 1; ++t) {
+  for (int t = 0; t < PRO; ++t) {
     da.issue(lds0 + t * STAGE, wave, t * BK, g.ka, ra);
     db.issue(lds0 + t * STAGE + ABYTES, wave, t * BK, g.kb, rb);
   }
-  wait_vmcnt<(NST - 2) * PER_TILE>();
+  wait_vmcnt<(PRO - 1) * PER_TILE>();
   __syncthreads();
   // Fragments are double-buffered in registers: the LDS reads of the next
   // k16 slice are issued before the MFMAs of the current one (scheduling
@@ -755,7 +758,15 @@ gemm_dma_kernel(GemmDesc g, EpiArgs e) {
         __syncthreads();                      // everyone's share; tile kt fully read
       }
       constexpr int NMF = FM * FN, NRD = FM + FN, TOT = TA::ITEMS + TB::ITEMS;
-      const int lo = q < DS ? q * TOT / DS : 0, hi = q < DS ? (q + 1) * TOT / DS : 0;
+      // GEMM_IL == 2: tile kt + NST goes into stage rd right after the
+      // barrier that releases it (last slice); else tile kt + NST - 1 into
+      // stage wr over the first DS slices
+      const bool early = GEMM_IL == 2;
+      const bool dslice = early ? q + 1 == NS : q < DS;
+      const int lo = !dslice ? 0 : early ? 0 : q * TOT / DS;
+      const int hi = !dslice ? 0 : early ? TOT : (q + 1) * TOT / DS;
+      const uint32_t ddst = early ? lds0 + rd * STAGE : dst;
+      const int dk0 = early ? (kt + NST) * BK : k0n;
       const int span = hi > lo ? hi - lo : 1;
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -771,8 +782,8 @@ gemm_dma_kernel(GemmDesc g, EpiArgs e) {
 #pragma unroll
         for (int u = 0; u < TOT; ++u) {
           if (u < lo || u >= hi || (u - lo) * NMF / span != t) continue;
-          if (u < TA::ITEMS) da.issue_one(u, dst, wave, k0n, g.ka, ra);
-          else db.issue_one(u - TA::ITEMS, dst + ABYTES, wave, k0n, g.kb, rb);
+          if (u < TA::ITEMS) da.issue_one(u, ddst, wave, dk0, g.ka, ra);
+          else db.issue_one(u - TA::ITEMS, ddst + ABYTES, wave, dk0, g.kb, rb);
         }
         __builtin_amdgcn_sched_barrier(0);
       }
@@ -942,6 +953,12 @@ static const char* layout_tag(bool ak, bool bk) {
 #ifndef GEMM_NST
 #define GEMM_NST 2
 #endif
+#ifndef GEMM_BK_MN
+#define GEMM_BK_MN 32
+#endif
+#ifndef GEMM_NST_MN
+#define GEMM_NST_MN 3
+#endif
 #ifndef GEMM_DS
 #define GEMM_DS 1
 #endif
@@ -1012,8 +1029,11 @@ static hipError_t run_layout(const GemmDesc& g, const EpiArgs& e, int dtype, hip
                      (g.K2 <= 0 || (dma_operand_ok(g.A2, g.lda2, AK, g.M, g.K2, R) &&
                                     dma_operand_ok(g.B2, g.ldb2, BKM, g.N, g.K2, R)));
     if (dma) {
-      if (large) { err = run_dma<256, 256, GEMM_WM, GEMM_WN, GEMM_BK, GEMM_NST, AK, BKM>(g, e, s); which = 3; }
-      else { err = run_dma<128, 128, 2, 2, GEMM_BK, GEMM_NST, AK, BKM>(g, e, s); which = 4; }
+      // an M-contiguous A (weight gradients) runs best with shallower,
+      // deeper-pipelined k tiles
+      constexpr int BKL = AK ? GEMM_BK : GEMM_BK_MN, NSTL = AK ? GEMM_NST : GEMM_NST_MN;
+      if (large) { err = run_dma<256, 256, GEMM_WM, GEMM_WN, BKL, NSTL, AK, BKM>(g, e, s); which = 3; }
+      else { err = run_dma<128, 128, 2, 2, BKL, NSTL, AK, BKM>(g, e, s); which = 4; }
     } else if (large) {
       if constexpr (AK && BKM) err = run_mfma<256, 256, 4, 2, AK, BKM>(g, e, s);
       else err = run_mfma<256, 256, 2, 2, AK, BKM>(g, e, s);

@@ -61,6 +61,22 @@ __device__ inline Soft soft_add(Soft a, float x, float w) {
   return {a.m, a.s + p, a.e + p * w};
 }
 
+// Four values at once: one rescale to their maximum, then four exponentials.
+__device__ inline Soft soft_add4(Soft a, const float (&x)[4], const float (&w)[4]) {
+  const float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+  if (mx > a.m) {
+    const float f = __expf(a.m - mx);
+    a = {mx, a.s * f, a.e * f};
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const float p = __expf(x[k] - a.m);
+    a.s += p;
+    a.e += p * w[k];
+  }
+  return a;
+}
+
 __device__ inline Soft block_soft(Soft v, Soft* red) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
@@ -75,6 +91,19 @@ __device__ inline Soft block_soft(Soft v, Soft* red) {
   return r;
 }
 
+// Rows are 16-byte aligned (ldz and lddz multiples of 8); 4 columns per
+// thread and step, the last partial group of a row element by element.
+__device__ inline void st_dz4(const ObjDesc& o, int64_t i, const float (&g)[4]) {
+  if (o.dz_dtype == BF16) {
+    uint2 u;
+    u.x = (uint32_t)f32_to_bf16(g[0]) | ((uint32_t)f32_to_bf16(g[1]) << 16);
+    u.y = (uint32_t)f32_to_bf16(g[2]) | ((uint32_t)f32_to_bf16(g[3]) << 16);
+    *reinterpret_cast<uint2*>((bf16_t*)o.dz + i) = u;
+  } else {
+    *reinterpret_cast<float4*>((float*)o.dz + i) = make_float4(g[0], g[1], g[2], g[3]);
+  }
+}
+
 __global__ void __launch_bounds__(OT) objective_rows_kernel(ObjDesc o) {
   __shared__ Soft red[OT / 64];
   const int i = blockIdx.x;
@@ -86,21 +115,35 @@ __global__ void __launch_bounds__(OT) objective_rows_kernel(ObjDesc o) {
   const float inv = nomega > 0.f ? 1.f / nomega : 0.f;
   const bool rev = o.consis == 0;
   const int64_t orow = (int64_t)i * o.lddz;
+  const int V4 = o.V & ~3;  // columns handled 4 at a time
 
   if (!in_omega) {
-    for (int v = threadIdx.x; v < o.Vpad; v += OT) {
-      if (o.dz_dtype == BF16) ((bf16_t*)o.dz)[orow + v] = 0;
-      else ((float*)o.dz)[orow + v] = 0.f;
-    }
+    const float zero[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int v = threadIdx.x * 4; v < o.Vpad; v += OT * 4) st_dz4(o, orow + v, zero);
     if (threadIdx.x == 0) o.row_loss[i] = 0.f;
     return;
   }
 
   Soft sp = {-INFINITY, 0.f, 0.f}, sq = {-INFINITY, 0.f, 0.f};
-  for (int v = threadIdx.x; v < o.V; v += OT) {
+  for (int v = threadIdx.x * 4; v < V4; v += OT * 4) {
+    const float4 a4 = *reinterpret_cast<const float4*>(z + v);
+    const float a[4] = {a4.x, a4.y, a4.z, a4.w};
+    float b[4] = {0.f, 0.f, 0.f, 0.f};
+    if (zp) {
+      const float4 b4 = *reinterpret_cast<const float4*>(zp + v);
+      b[0] = b4.x; b[1] = b4.y; b[2] = b4.z; b[3] = b4.w;
+    }
+    const float ab[4] = {a[0] - b[0], a[1] - b[1], a[2] - b[2], a[3] - b[3]};
+    sp = soft_add4(sp, a, ab);  // e accumulates sum p (z - z') unnormalised
+    if (zp) {
+      const float ba[4] = {-ab[0], -ab[1], -ab[2], -ab[3]};
+      sq = soft_add4(sq, b, ba);
+    }
+  }
+  for (int v = V4 + threadIdx.x; v < o.V; v += OT) {
     const float a = z[v];
     const float b = zp ? zp[v] : 0.f;
-    sp = soft_add(sp, a, a - b);   // e accumulates sum p (z - z') unnormalised
+    sp = soft_add(sp, a, a - b);
     if (zp) sq = soft_add(sq, b, b - a);
   }
   sp = block_soft(sp, red);
@@ -119,21 +162,30 @@ __global__ void __launch_bounds__(OT) objective_rows_kernel(ObjDesc o) {
   const float a = o.alpha;
   if (threadIdx.x == 0) o.row_loss[i] = a * ce + (zp ? (1.f - a) * kl : 0.f);
 
-  for (int v = threadIdx.x; v < o.Vpad; v += OT) {
-    float g = 0.f;
-    if (v < o.V) {
-      const float zv = z[v];
-      const float p = __expf(zv - lse);
-      g = a * (p - (v == y ? 1.f : 0.f));
-      if (zp) {
-        const float zpv = zp[v];
-        if (rev) g += (1.f - a) * p * (zv - zpv - E);
-        else g += (1.f - a) * (p - __expf(zpv - lse2));
-      }
-      g *= inv;
+  // dL/dz of one column
+  auto grad = [&](int v, float zv, float zpv) {
+    const float p = __expf(zv - lse);
+    float g = a * (p - (v == y ? 1.f : 0.f));
+    if (zp) {
+      if (rev) g += (1.f - a) * p * (zv - zpv - E);
+      else g += (1.f - a) * (p - __expf(zpv - lse2));
     }
-    if (o.dz_dtype == BF16) ((bf16_t*)o.dz)[orow + v] = f32_to_bf16(g);
-    else ((float*)o.dz)[orow + v] = g;
+    return g * inv;
+  };
+  for (int v = threadIdx.x * 4; v < o.Vpad; v += OT * 4) {
+    float g[4] = {0.f, 0.f, 0.f, 0.f};
+    if (v < V4) {
+      const float4 a4 = *reinterpret_cast<const float4*>(z + v);
+      float4 b4 = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (zp) b4 = *reinterpret_cast<const float4*>(zp + v);
+      g[0] = grad(v, a4.x, b4.x); g[1] = grad(v + 1, a4.y, b4.y);
+      g[2] = grad(v + 2, a4.z, b4.z); g[3] = grad(v + 3, a4.w, b4.w);
+    } else {
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        if (v + k < o.V) g[k] = grad(v + k, z[v + k], zp ? zp[v + k] : 0.f);
+    }
+    st_dz4(o, orow + v, g);
   }
 }
 

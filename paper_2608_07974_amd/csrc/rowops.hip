@@ -103,42 +103,44 @@ hipError_t launch_head_norm(bool layernorm, const float* xa, const float* xb, in
 //   rms: dx = rstd * (g - xhat * mean(g * xhat))
 //   ln:  dx = rstd * (g - mean(g) - xhat * mean(g * xhat))
 // The weight-gradient partials sum(dy * xhat) (and sum(dy)) over the wave's
-// rows accumulate in a wave-private LDS slice and are written as one row of
-// part_w / part_b per wave: deterministic, no atomics.
-constexpr int NB_WAVES = 1024;  // waves (partial rows) of a norm backward launch
-
+// rows accumulate in registers (lane l owns columns 256 k + 4 l .. +3, CM
+// chunks) and are written as one row of part_w / part_b per wave:
+// deterministic, no atomics, no LDS, so many waves stay resident.
 int norm_bwd_blocks(int T) {
-  const int waves = T < NB_WAVES ? (T > 0 ? T : 1) : NB_WAVES;
-  return waves;  // number of partial rows
+  // about four rows per wave, at least 1024 waves when there are rows for them
+  int waves = T / 4;
+  if (waves < 1024) waves = T < 1024 ? T : 1024;
+  return waves > 0 ? waves : 1;  // number of partial rows
 }
 
+template <int CM, bool LN>
 __global__ void __launch_bounds__(RT)
-norm_bwd_kernel(int layernorm, const float* __restrict__ dy, int64_t lddy,
-                const float* __restrict__ x, const float* __restrict__ w,
-                const float* __restrict__ mean, const float* __restrict__ rstd, int rstride,
-                const float* dres, float* dx, void* dx_act, int adt,
-                float* __restrict__ part_w, float* __restrict__ part_b, int T, int d, int rpw,
-                int nwaves, int row_out0) {
-  extern __shared__ float accs[];
+norm_bwd_kernel(const float* __restrict__ dy, int64_t lddy, const float* __restrict__ x,
+                const float* __restrict__ w, const float* __restrict__ mean,
+                const float* __restrict__ rstd, int rstride, const float* dres, float* dx,
+                void* dx_act, int adt, float* __restrict__ part_w, float* __restrict__ part_b,
+                int T, int d, int rpw, int nwaves, int row_out0) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int gw = blockIdx.x * (RT / 64) + wave;
   const bool want_part = part_w != nullptr;
-  float* aw = accs + (size_t)wave * (layernorm ? 2 : 1) * d;
-  float* ab = aw + d;
-  if (want_part)
-    for (int c = lane * 4; c < d; c += 256) {
-      *reinterpret_cast<float4*>(aw + c) = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (layernorm) *reinterpret_cast<float4*>(ab + c) = make_float4(0.f, 0.f, 0.f, 0.f);
-    }
+  float4 aw[CM], ab[CM];
+#pragma unroll
+  for (int k = 0; k < CM; ++k) {
+    aw[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+    ab[k] = aw[k];
+  }
   const int r0 = gw * rpw, r1 = min(T, r0 + rpw);
   for (int r = (gw < nwaves ? r0 : T); r < r1; ++r) {
     const float rs = rstd[(int64_t)r * rstride];
-    const float mu = layernorm ? mean[(int64_t)r * rstride] : 0.f;
+    const float mu = LN ? mean[(int64_t)r * rstride] : 0.f;
     const int ro = row_out0 + r;
     const float* dyr = dy + (int64_t)r * lddy;
     const float* xr = x + (int64_t)ro * d;
     float sg = 0.f, sgx = 0.f;
-    for (int c = lane * 4; c < d; c += 256) {
+#pragma unroll
+    for (int k = 0; k < CM; ++k) {
+      const int c = k * 256 + lane * 4;
+      if (c >= d) continue;
       const float4 a = *reinterpret_cast<const float4*>(dyr + c);
       const float4 v = *reinterpret_cast<const float4*>(xr + c);
       const float4 g = *reinterpret_cast<const float4*>(w + c);
@@ -147,29 +149,26 @@ norm_bwd_kernel(int layernorm, const float* __restrict__ dy, int64_t lddy,
       sg += (g0 + g1) + (g2 + g3);
       sgx += (g0 * h0 + g1 * h1) + (g2 * h2 + g3 * h3);
       if (want_part) {
-        float4 t = *reinterpret_cast<float4*>(aw + c);
-        t.x += a.x * h0; t.y += a.y * h1; t.z += a.z * h2; t.w += a.w * h3;
-        *reinterpret_cast<float4*>(aw + c) = t;
-        if (layernorm) {
-          float4 u = *reinterpret_cast<float4*>(ab + c);
-          u.x += a.x; u.y += a.y; u.z += a.z; u.w += a.w;
-          *reinterpret_cast<float4*>(ab + c) = u;
-        }
+        aw[k].x += a.x * h0; aw[k].y += a.y * h1; aw[k].z += a.z * h2; aw[k].w += a.w * h3;
+        if (LN) { ab[k].x += a.x; ab[k].y += a.y; ab[k].z += a.z; ab[k].w += a.w; }
       }
     }
     if (!dx) continue;
-    const float mg = layernorm ? wave_sum(sg) / d : 0.f;
+    const float mg = LN ? wave_sum(sg) / d : 0.f;
     const float mgx = wave_sum(sgx) / d;
-    for (int c = lane * 4; c < d; c += 256) {
+#pragma unroll
+    for (int k = 0; k < CM; ++k) {
+      const int c = k * 256 + lane * 4;
+      if (c >= d) continue;
       const float4 a = *reinterpret_cast<const float4*>(dyr + c);
       const float4 v = *reinterpret_cast<const float4*>(xr + c);
       const float4 g = *reinterpret_cast<const float4*>(w + c);
       float o[4];
       const float av[4] = {a.x, a.y, a.z, a.w}, vv[4] = {v.x, v.y, v.z, v.w}, gv[4] = {g.x, g.y, g.z, g.w};
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const float h = (vv[k] - mu) * rs;
-        o[k] = rs * (av[k] * gv[k] - mg - h * mgx);
+      for (int q = 0; q < 4; ++q) {
+        const float h = (vv[q] - mu) * rs;
+        o[q] = rs * (av[q] * gv[q] - mg - h * mgx);
       }
       const int64_t off = (int64_t)ro * d + c;
       if (dres) {
@@ -186,12 +185,25 @@ norm_bwd_kernel(int layernorm, const float* __restrict__ dy, int64_t lddy,
       }
     }
   }
-  if (want_part && gw < nwaves)
-    for (int c = lane * 4; c < d; c += 256) {
-      *reinterpret_cast<float4*>(part_w + (int64_t)gw * d + c) = *reinterpret_cast<float4*>(aw + c);
-      if (layernorm && part_b)
-        *reinterpret_cast<float4*>(part_b + (int64_t)gw * d + c) = *reinterpret_cast<float4*>(ab + c);
+  if (want_part && gw < nwaves) {
+#pragma unroll
+    for (int k = 0; k < CM; ++k) {
+      const int c = k * 256 + lane * 4;
+      if (c >= d) continue;
+      *reinterpret_cast<float4*>(part_w + (int64_t)gw * d + c) = aw[k];
+      if (LN && part_b) *reinterpret_cast<float4*>(part_b + (int64_t)gw * d + c) = ab[k];
     }
+  }
+}
+
+template <int CM, bool LN>
+static void norm_bwd_go(int blocks, hipStream_t s, const float* dy, int64_t lddy, const float* x,
+                        const float* w, const float* mean, const float* rstd, int rstride,
+                        const float* dres, float* dx, void* dx_act, int adt, float* part_w,
+                        float* part_b, int T, int d, int rpw, int nw, int row_out0) {
+  hipLaunchKernelGGL((norm_bwd_kernel<CM, LN>), dim3(blocks), dim3(RT), 0, s, dy, lddy, x, w,
+                     mean, rstd, rstride, dres, dx, dx_act, adt, part_w, part_b, T, d, rpw, nw,
+                     row_out0);
 }
 
 static hipError_t norm_bwd_launch(bool layernorm, const float* dy, int64_t lddy, const float* x,
@@ -202,17 +214,28 @@ static hipError_t norm_bwd_launch(bool layernorm, const float* dy, int64_t lddy,
   const int nw = norm_bwd_blocks(T);
   const int rpw = (T + nw - 1) / nw;
   if (nblk_out) *nblk_out = nw;
-  const size_t lds = part_w ? (size_t)(RT / 64) * (layernorm ? 2 : 1) * d * sizeof(float) : 0;
-  static bool attr = false;
-  if (!attr) {
-    hipError_t e = hipFuncSetAttribute((const void*)norm_bwd_kernel,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    if (e != hipSuccess) return e;
-    attr = true;
+  if (d <= 0 || d % 4 || d > 8192) return hipErrorInvalidValue;
+  const int blocks = (nw + 3) / 4;
+#define ZL_NB(CM, LN)                                                                       \
+  norm_bwd_go<CM, LN>(blocks, s, dy, lddy, x, w, mean, rstd, rstride, dres, dx, dx_act, adt, \
+                      part_w, part_b, T, d, rpw, nw, row_out0)
+  const int cm = (d + 255) / 256;
+  if (layernorm) {
+    if (cm <= 1) ZL_NB(1, true);
+    else if (cm <= 2) ZL_NB(2, true);
+    else if (cm <= 4) ZL_NB(4, true);
+    else if (cm <= 8) ZL_NB(8, true);
+    else if (cm <= 16) ZL_NB(16, true);
+    else ZL_NB(32, true);
+  } else {
+    if (cm <= 1) ZL_NB(1, false);
+    else if (cm <= 2) ZL_NB(2, false);
+    else if (cm <= 4) ZL_NB(4, false);
+    else if (cm <= 8) ZL_NB(8, false);
+    else if (cm <= 16) ZL_NB(16, false);
+    else ZL_NB(32, false);
   }
-  hipLaunchKernelGGL(norm_bwd_kernel, dim3((nw + 3) / 4), dim3(RT), lds, s, (int)layernorm, dy,
-                     lddy, x, w, mean, rstd, rstride, dres, dx, dx_act, adt, part_w, part_b, T, d,
-                     rpw, nw, row_out0);
+#undef ZL_NB
   return hipGetLastError();
 }
 
@@ -237,37 +260,57 @@ hipError_t launch_head_norm_bwd(bool layernorm, const float* dy, int64_t lddy, c
 // out[j] = (accumulate ? out[j] : 0) + scale * sum_b part[b, j]; a block
 // covers 64 columns with 4 row groups, each summing with 4 independent
 // accumulators; the 4 group sums combine in a fixed order (deterministic).
-__global__ void __launch_bounds__(256) reduce_rows_kernel(const float* __restrict__ part, int nblk,
-                                                          int d, float* __restrict__ out,
-                                                          float scale, int accumulate) {
+// Rows b < nblk of part at part + b * rstride.  Block (x, y) sums rows
+// [y gs, min(nblk, (y + 1) gs)) of columns 64 x .. 64 x + 63 in a fixed
+// order; the last stage (final) writes out, an earlier one leaves its sum in
+// place of the group's first row (read by the next stage), so the result is
+// deterministic for a given nblk.
+__global__ void __launch_bounds__(256) reduce_rows_kernel(float* part, int nblk, int64_t rstride,
+                                                          int d, int gs, float* __restrict__ out,
+                                                          float scale, int accumulate, int final) {
   __shared__ float red[4][64];
   const int j = blockIdx.x * 64 + (threadIdx.x & 63);
   const int grp = threadIdx.x >> 6;
+  const int b0 = blockIdx.y * gs, b1 = min(nblk, b0 + gs);
   float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
   if (j < d) {
-    int b = grp;
-    for (; b + 12 < nblk; b += 16) {
-      a0 += part[(int64_t)b * d + j];
-      a1 += part[(int64_t)(b + 4) * d + j];
-      a2 += part[(int64_t)(b + 8) * d + j];
-      a3 += part[(int64_t)(b + 12) * d + j];
+    int b = b0 + grp;
+    for (; b + 12 < b1; b += 16) {
+      a0 += part[(int64_t)b * rstride + j];
+      a1 += part[(int64_t)(b + 4) * rstride + j];
+      a2 += part[(int64_t)(b + 8) * rstride + j];
+      a3 += part[(int64_t)(b + 12) * rstride + j];
     }
-    for (; b < nblk; b += 4) a0 += part[(int64_t)b * d + j];
+    for (; b < b1; b += 4) a0 += part[(int64_t)b * rstride + j];
   }
   red[grp][threadIdx.x & 63] = (a0 + a1) + (a2 + a3);
   __syncthreads();
   if (grp == 0 && j < d) {
     const float t = ((red[0][threadIdx.x] + red[1][threadIdx.x]) + red[2][threadIdx.x]) + red[3][threadIdx.x];
-    const float v = scale * t;
-    out[j] = accumulate ? out[j] + v : v;
+    if (final) {
+      const float v = scale * t;
+      out[j] = accumulate ? out[j] + v : v;
+    } else {
+      part[(int64_t)b0 * rstride + j] = t;
+    }
   }
 }
 
-hipError_t launch_reduce_rows(const float* part, int nblk, int d, float* out, float scale,
+hipError_t launch_reduce_rows(float* part, int nblk, int d, float* out, float scale,
                               int accumulate, hipStream_t s) {
   if (d <= 0) return hipSuccess;
-  hipLaunchKernelGGL(reduce_rows_kernel, dim3((d + 63) / 64), dim3(256), 0, s, part, nblk, d, out,
-                     scale, accumulate);
+  const int cb = (d + 63) / 64;
+  int64_t stride = d;
+  if (nblk > 256) {  // first stage: groups of 64 rows, many blocks
+    constexpr int GS = 64;
+    const int ng = (nblk + GS - 1) / GS;
+    hipLaunchKernelGGL(reduce_rows_kernel, dim3(cb, ng), dim3(256), 0, s, part, nblk, stride, d,
+                       GS, out, scale, accumulate, 0);
+    nblk = ng;
+    stride *= GS;
+  }
+  hipLaunchKernelGGL(reduce_rows_kernel, dim3(cb, 1), dim3(256), 0, s, part, nblk, stride, d, nblk,
+                     out, scale, accumulate, 1);
   return hipGetLastError();
 }
 
@@ -391,30 +434,60 @@ hipError_t launch_rope(void* qkv, int64_t ld, int dtype, const int32_t* pos, con
   return hipGetLastError();
 }
 
+// 8 consecutive elements per thread (16-byte bf16 / 2 x 16-byte fp32
+// accesses); rows on the grid's y dimension (grid-stride beyond 65535).
+__device__ inline void ld8(const void* p, int dt, int64_t i, float (&v)[8]) {
+  if (dt == BF16) {
+    const uint4 u = *reinterpret_cast<const uint4*>((const bf16_t*)p + i);
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      v[2 * k] = bf16_to_f32((bf16_t)(w[k] & 0xffff));
+      v[2 * k + 1] = bf16_to_f32((bf16_t)(w[k] >> 16));
+    }
+  } else {
+    const float4 a = *reinterpret_cast<const float4*>((const float*)p + i);
+    const float4 b = *reinterpret_cast<const float4*>((const float*)p + i + 4);
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+  }
+}
+__device__ inline void st8(void* p, int dt, int64_t i, const float (&v)[8]) {
+  if (dt == BF16) {
+    uint32_t w[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      w[k] = (uint32_t)f32_to_bf16(v[2 * k]) | ((uint32_t)f32_to_bf16(v[2 * k + 1]) << 16);
+    *reinterpret_cast<uint4*>((bf16_t*)p + i) = make_uint4(w[0], w[1], w[2], w[3]);
+  } else {
+    *reinterpret_cast<float4*>((float*)p + i) = make_float4(v[0], v[1], v[2], v[3]);
+    *reinterpret_cast<float4*>((float*)p + i + 4) = make_float4(v[4], v[5], v[6], v[7]);
+  }
+}
+
 __global__ void swiglu_fwd_kernel(const void* __restrict__ gu, int64_t ldgu,
                                   void* __restrict__ a, int64_t lda, int dt, int T, int ff) {
-  const int64_t n = (int64_t)T * ff;
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t t = i / ff;
-    const int j = (int)(i % ff);
-    const float g = ldf(gu, dt, t * ldgu + j);
-    const float u = ldf(gu, dt, t * ldgu + ff + j);
-    stf(a, dt, t * lda + j, g / (1.f + __expf(-g)) * u);
+  const int j = (blockIdx.x * blockDim.x + threadIdx.x) * 8;
+  if (j >= ff) return;
+  for (int t = blockIdx.y; t < T; t += gridDim.y) {
+    float g[8], u[8], o[8];
+    ld8(gu, dt, (int64_t)t * ldgu + j, g);
+    ld8(gu, dt, (int64_t)t * ldgu + ff + j, u);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) o[k] = g[k] / (1.f + __expf(-g[k])) * u[k];
+    st8(a, dt, (int64_t)t * lda + j, o);
   }
 }
 
 hipError_t launch_swiglu_fwd(const void* gu, int64_t ldgu, void* a, int64_t lda, int dtype,
                              int T, int ff, hipStream_t s) {
-  const int64_t n = (int64_t)T * ff;
-  if (n <= 0) return hipSuccess;
-  int64_t blocks = (n + 255) / 256;
-  if (blocks > 65536) blocks = 65536;
-  hipLaunchKernelGGL(swiglu_fwd_kernel, dim3((unsigned)blocks), dim3(256), 0, s, gu, ldgu, a,
-                     lda, dtype, T, ff);
+  if (T <= 0 || ff <= 0) return hipSuccess;
+  if (ff % 8 || ldgu % 8 || lda % 8) return hipErrorInvalidValue;
+  const int bx = (ff / 8 + 255) / 256;
+  const int by = T < 65535 ? T : 65535;
+  hipLaunchKernelGGL(swiglu_fwd_kernel, dim3(bx, by), dim3(256), 0, s, gu, ldgu, a, lda, dtype,
+                     T, ff);
   return hipGetLastError();
 }
-
 
 // Block-diagonal expansion of stacked low-rank factors (one thread per output
 // element; the matrix is small: rows x nblk r).
