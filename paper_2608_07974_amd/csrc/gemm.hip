@@ -92,30 +92,44 @@ __device__ inline void epilogue(const EpiArgs& e, int M, int N, int m, int n, fl
   }
 }
 
-// Four consecutive columns n .. n+3 of row m.  The vector path (vec: every
-// operand 16-byte aligned, every row stride a multiple of 4, checked once
-// per block) loads and stores 4 elements at once with the same arithmetic
-// as epilogue(); the column tail and unaligned operands take the scalar
-// path.
-__device__ inline float4 ld4f(const float* p) { return *reinterpret_cast<const float4*>(p); }
-__device__ inline void ld4_act(const void* p, int dt, size_t i, float (&v)[4]) {
-  if (dt == BF16) {
-    const uint2 u = *reinterpret_cast<const uint2*>(static_cast<const bf16_t*>(p) + i);
-    v[0] = bf16_to_f32((bf16_t)(u.x & 0xffff)); v[1] = bf16_to_f32((bf16_t)(u.x >> 16));
-    v[2] = bf16_to_f32((bf16_t)(u.y & 0xffff)); v[3] = bf16_to_f32((bf16_t)(u.y >> 16));
-  } else {
-    const float4 f = ld4f(static_cast<const float*>(p) + i);
-    v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
+// EW consecutive columns n .. n+EW-1 of row m.  The vector path (vec: every
+// operand 16-byte aligned, every row stride a multiple of 8, checked once
+// per block) loads and stores them at once (16-byte accesses for bf16) with
+// the same arithmetic as epilogue(); the column tail and unaligned operands
+// take the scalar path.
+constexpr int EW = 8;
+__device__ inline void ldv_f32(const float* p, float (&v)[EW]) {
+#pragma unroll
+  for (int k = 0; k < EW; k += 4) {
+    const float4 f = *reinterpret_cast<const float4*>(p + k);
+    v[k] = f.x; v[k + 1] = f.y; v[k + 2] = f.z; v[k + 3] = f.w;
   }
 }
-__device__ inline void st4_act(void* p, int dt, size_t i, const float (&v)[4]) {
+__device__ inline void ldv_act(const void* p, int dt, size_t i, float (&v)[EW]) {
   if (dt == BF16) {
-    uint2 u;
-    u.x = (uint32_t)f32_to_bf16(v[0]) | ((uint32_t)f32_to_bf16(v[1]) << 16);
-    u.y = (uint32_t)f32_to_bf16(v[2]) | ((uint32_t)f32_to_bf16(v[3]) << 16);
-    *reinterpret_cast<uint2*>(static_cast<bf16_t*>(p) + i) = u;
+    const uint4 u = *reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(p) + i);
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      v[2 * k] = bf16_to_f32((bf16_t)(w[k] & 0xffff));
+      v[2 * k + 1] = bf16_to_f32((bf16_t)(w[k] >> 16));
+    }
   } else {
-    *reinterpret_cast<float4*>(static_cast<float*>(p) + i) = make_float4(v[0], v[1], v[2], v[3]);
+    ldv_f32(static_cast<const float*>(p) + i, v);
+  }
+}
+__device__ inline void stv_act(void* p, int dt, size_t i, const float (&v)[EW]) {
+  if (dt == BF16) {
+    uint32_t w[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      w[k] = (uint32_t)f32_to_bf16(v[2 * k]) | ((uint32_t)f32_to_bf16(v[2 * k + 1]) << 16);
+    *reinterpret_cast<uint4*>(static_cast<bf16_t*>(p) + i) = make_uint4(w[0], w[1], w[2], w[3]);
+  } else {
+    float* q = static_cast<float*>(p) + i;
+#pragma unroll
+    for (int k = 0; k < EW; k += 4)
+      *reinterpret_cast<float4*>(q + k) = make_float4(v[k], v[k + 1], v[k + 2], v[k + 3]);
   }
 }
 
@@ -123,85 +137,88 @@ __device__ inline bool epi_vec_ok(const EpiArgs& e) {
   const uintptr_t p = (uintptr_t)e.out | (uintptr_t)e.bias | (uintptr_t)e.resid |
                       (uintptr_t)e.out2 | (uintptr_t)e.aux;
   const int64_t l = e.ldo | e.ldr | e.ldo2 | e.ldaux | (int64_t)e.ff;
-  return (p & 15) == 0 && (l & 3) == 0;
+  return (p & 15) == 0 && (l & 7) == 0;
 }
 
-__device__ inline void epilogue4(const EpiArgs& e, int M, int N, int m, int n, const float (&a)[4],
-                                 bool vec) {
+__device__ inline void epilogue_v(const EpiArgs& e, int M, int N, int m, int n,
+                                  const float (&a)[EW], bool vec) {
   if (m >= M) return;
-  if (!vec || n + 4 > N) {
+  if (!vec || n + EW > N) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) epilogue(e, M, N, m, n + i, a[i]);
+    for (int i = 0; i < EW; ++i) epilogue(e, M, N, m, n + i, a[i]);
     return;
   }
   const size_t mo = (size_t)m;
-  float v[4], b[4] = {0.f, 0.f, 0.f, 0.f};
-  if (e.bias && (e.kind == EPI_STORE || e.kind == EPI_RESID || e.kind == EPI_GELU)) {
-    const float4 f = ld4f(e.bias + n);
-    b[0] = f.x; b[1] = f.y; b[2] = f.z; b[3] = f.w;
-  }
+  float v[EW], b[EW];
+#pragma unroll
+  for (int i = 0; i < EW; ++i) b[i] = 0.f;
+  if (e.bias && (e.kind == EPI_STORE || e.kind == EPI_RESID || e.kind == EPI_GELU))
+    ldv_f32(e.bias + n, b);
   switch (e.kind) {
     case EPI_STORE:
 #pragma unroll
-      for (int i = 0; i < 4; ++i) v[i] = e.scale * a[i] + b[i];
-      st4_act(e.out, e.out_dtype, mo * e.ldo + n, v);
+      for (int i = 0; i < EW; ++i) v[i] = e.scale * a[i] + b[i];
+      stv_act(e.out, e.out_dtype, mo * e.ldo + n, v);
       break;
     case EPI_RESID: {
-      const float4 r = ld4f(e.resid + mo * e.ldr + n);
-      v[0] = r.x + a[0] + b[0]; v[1] = r.y + a[1] + b[1];
-      v[2] = r.z + a[2] + b[2]; v[3] = r.w + a[3] + b[3];
-      st4_act(e.out, F32, mo * e.ldo + n, v);
+      float r[EW];
+      ldv_f32(e.resid + mo * e.ldr + n, r);
+#pragma unroll
+      for (int i = 0; i < EW; ++i) v[i] = r[i] + a[i] + b[i];
+      stv_act(e.out, F32, mo * e.ldo + n, v);
       break;
     }
     case EPI_GELU: {
-      float h[4];
+      float h[EW];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
+      for (int i = 0; i < EW; ++i) {
         h[i] = a[i] + b[i];
         if (e.out_dtype == BF16) h[i] = bf16_to_f32(f32_to_bf16(h[i]));  // as stored
         v[i] = gelu_f(h[i]);
       }
-      st4_act(e.out2, e.out_dtype, mo * e.ldo2 + n, h);
-      st4_act(e.out, e.out_dtype, mo * e.ldo + n, v);
+      stv_act(e.out2, e.out_dtype, mo * e.ldo2 + n, h);
+      stv_act(e.out, e.out_dtype, mo * e.ldo + n, v);
       break;
     }
     case EPI_GRAD: {
       float* o = static_cast<float*>(e.out) + mo * e.ldo + n;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) v[i] = e.scale * a[i];
+      for (int i = 0; i < EW; ++i) v[i] = e.scale * a[i];
       if (e.accumulate) {
-        const float4 f = ld4f(o);
-        v[0] = f.x + v[0]; v[1] = f.y + v[1]; v[2] = f.z + v[2]; v[3] = f.w + v[3];
+        float f[EW];
+        ldv_f32(o, f);
+#pragma unroll
+        for (int i = 0; i < EW; ++i) v[i] = f[i] + v[i];
       }
-      st4_act(o, F32, 0, v);
+      stv_act(o, F32, 0, v);
       break;
     }
     case EPI_SWIGLU_BWD: {
-      float g[4], u[4], w[4];
-      ld4_act(e.aux, e.out_dtype, mo * e.ldaux + n, g);
-      ld4_act(e.aux, e.out_dtype, mo * e.ldaux + n + e.ff, u);
+      float g[EW], u[EW], w[EW];
+      ldv_act(e.aux, e.out_dtype, mo * e.ldaux + n, g);
+      ldv_act(e.aux, e.out_dtype, mo * e.ldaux + n + e.ff, u);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
+      for (int i = 0; i < EW; ++i) {
         const float sg = 1.f / (1.f + __expf(-g[i]));
         const float silu = g[i] * sg;
         const float dsilu = sg * (1.f + g[i] * (1.f - sg));
         v[i] = a[i] * u[i] * dsilu;
         w[i] = a[i] * silu;
       }
-      st4_act(e.out, e.out_dtype, mo * e.ldo + n, v);
-      st4_act(e.out, e.out_dtype, mo * e.ldo + n + e.ff, w);
+      stv_act(e.out, e.out_dtype, mo * e.ldo + n, v);
+      stv_act(e.out, e.out_dtype, mo * e.ldo + n + e.ff, w);
       break;
     }
     case EPI_GELU_BWD: {
-      float h[4];
-      ld4_act(e.aux, e.out_dtype, mo * e.ldaux + n, h);
+      float h[EW];
+      ldv_act(e.aux, e.out_dtype, mo * e.ldaux + n, h);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) v[i] = a[i] * gelu_grad_f(h[i]);
-      st4_act(e.out, e.out_dtype, mo * e.ldo + n, v);
+      for (int i = 0; i < EW; ++i) v[i] = a[i] * gelu_grad_f(h[i]);
+      stv_act(e.out, e.out_dtype, mo * e.ldo + n, v);
       break;
     }
     case EPI_ROPE:  // rotation already applied by the staged epilogue
-      st4_act(e.out, e.out_dtype, mo * e.ldo + n, a);
+      stv_act(e.out, e.out_dtype, mo * e.ldo + n, a);
       break;
   }
 }
@@ -254,38 +271,52 @@ __device__ inline void store_tile(const f32x16_t (&acc)[BM / WM / 32][BN / WN / 
         ep[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * LDW + j * 32 + (lane & 31)] = acc[i][j][r];
     __syncthreads();
     const int mb = m0 + wm * TM + i * 32, nb = n0 + wn * TN;
-    // 4 consecutive columns per lane: a row of TN columns takes TN / 4 lanes
-    constexpr int QPR = TN / 4;
+    // EW consecutive columns per lane: a row of TN columns takes TN / EW lanes
+    constexpr int QPR = TN / EW;
+    static_assert(TN % EW == 0, "wave tile width must hold whole column groups");
     if (e.kind == EPI_ROPE) {
       // wave tiles are head-aligned (nb % hd == 0, TN % hd == 0) and half =
-      // hd / 2 is a multiple of 4, so the partner columns j +- hd/2 of a
-      // 4-column group are again 4 consecutive columns of the staged row
+      // hd / 2 is a multiple of EW, so the partner columns j +- hd/2 of a
+      // column group are again EW consecutive columns of the staged row
       const int half = e.hd >> 1;
       for (int t = lane; t < 32 * QPR; t += 64) {
-        const int row = t / QPR, col = (t % QPR) * 4;
+        const int row = t / QPR, col = (t % QPR) * EW;
         const int n = nb + col, m = mb + row;
-        const float4 x = *reinterpret_cast<const float4*>(&ep[row * LDW + col]);
-        float v[4] = {x.x, x.y, x.z, x.w};
+        float v[EW];
+#pragma unroll
+        for (int k = 0; k < EW; k += 4) {
+          const float4 x = *reinterpret_cast<const float4*>(&ep[row * LDW + col + k]);
+          v[k] = x.x; v[k + 1] = x.y; v[k + 2] = x.z; v[k + 3] = x.w;
+        }
         if (n < e.n_rot && m < g.M) {
           const int j = n % e.hd;
           const bool lo = j < half;
-          const float4 y = *reinterpret_cast<const float4*>(&ep[row * LDW + (lo ? col + half : col - half)]);
-          const float pv[4] = {y.x, y.y, y.z, y.w};
+          const int pc = lo ? col + half : col - half;
+          float pv[EW];
+#pragma unroll
+          for (int k = 0; k < EW; k += 4) {
+            const float4 y = *reinterpret_cast<const float4*>(&ep[row * LDW + pc + k]);
+            pv[k] = y.x; pv[k + 1] = y.y; pv[k + 2] = y.z; pv[k + 3] = y.w;
+          }
           int p = e.pos[m];
           p = p < 0 ? 0 : (p >= e.max_pos ? e.max_pos - 1 : p);
           const float2* cs = e.rope + (int64_t)p * half + (lo ? j : j - half);
 #pragma unroll
-          for (int k = 0; k < 4; ++k)
+          for (int k = 0; k < EW; ++k)
             v[k] = lo ? v[k] * cs[k].x - pv[k] * cs[k].y : v[k] * cs[k].x + pv[k] * cs[k].y;
         }
-        epilogue4(e, g.M, g.N, m, n, v, vec);
+        epilogue_v(e, g.M, g.N, m, n, v, vec);
       }
     } else {
       for (int t = lane; t < 32 * QPR; t += 64) {
-        const int row = t / QPR, col = (t % QPR) * 4;
-        const float4 x = *reinterpret_cast<const float4*>(&ep[row * LDW + col]);
-        const float v[4] = {x.x, x.y, x.z, x.w};
-        epilogue4(e, g.M, g.N, mb + row, nb + col, v, vec);
+        const int row = t / QPR, col = (t % QPR) * EW;
+        float v[EW];
+#pragma unroll
+        for (int k = 0; k < EW; k += 4) {
+          const float4 x = *reinterpret_cast<const float4*>(&ep[row * LDW + col + k]);
+          v[k] = x.x; v[k + 1] = x.y; v[k + 2] = x.z; v[k + 3] = x.w;
+        }
+        epilogue_v(e, g.M, g.N, mb + row, nb + col, v, vec);
       }
     }
     __syncthreads();
