@@ -46,7 +46,7 @@ __global__ void __launch_bounds__(256) optimizer_kernel(OptDesc o) {
 hipError_t launch_optimizer(const OptDesc& o, hipStream_t s) {
   if (o.n == 0) return hipSuccess;
   size_t blocks = (o.n / 4 + 255) / 256;
-  if (blocks > 8192) blocks = 8192;
+  if (blocks > 65536) blocks = 65536;  // a few float4 per thread, many waves in flight
   if (blocks == 0) blocks = 1;
   hipLaunchKernelGGL(optimizer_kernel, dim3((unsigned)blocks), dim3(256), 0, s, o);
   return hipGetLastError();
