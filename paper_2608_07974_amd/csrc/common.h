@@ -74,6 +74,11 @@ enum EpiKind {
   EPI_GELU_BWD = 5,    // out[m, n] = acc * gelu'(aux[m, n])
   EPI_ROPE = 6,        // EPI_STORE after rotating column pairs (j, j + hd/2) of
                        // every head in cols [0, n_rot) by pos[m] (rotate-half RoPE)
+  EPI_LOGITS = 7,      // fp32 store, plus per row m and 64-column block cb the
+                       // softmax partials stats[m * ldst + cb] = (max x,
+                       // sum exp(x - max), sum exp(x - max) (x - x'), 0) over
+                       // the block's columns < N, x' = row m ^ 1 (pair != 0)
+                       // else 0.  MFMA (bf16) paths only.
 };
 
 struct EpiArgs {
@@ -91,6 +96,9 @@ struct EpiArgs {
   int ff;               // EPI_SWIGLU_BWD column offset of u / du
   float scale;          // EPI_GRAD, EPI_STORE (out = scale * acc + bias)
   int accumulate;       // EPI_GRAD
+  float4* stats;        // EPI_LOGITS
+  int64_t ldst;
+  int pair;
   const int32_t* pos;   // EPI_ROPE: position of row m
   const float2* rope;   // EPI_ROPE: (cos, sin) table [max_pos, hd/2]
   int max_pos, hd, n_rot;
@@ -190,6 +198,9 @@ struct ObjDesc {
   const float* n_omega;   // device scalar |Omega|
   void* dz; int64_t lddz; int dz_dtype;  // [rows, Vpad]; pad columns zeroed
   float* row_loss;        // [rows]
+  const float4* stats;    // optional EPI_LOGITS partials of zc's rows (row stride ldst,
+  int64_t ldst;           // nst 64-column blocks): replace the statistics pass
+  int nst;
 };
 hipError_t launch_count_omega(const int32_t* labels, int T, int V, float* n_omega,
                               hipStream_t s);

@@ -44,7 +44,7 @@ __device__ inline void st_act(void* p, int dt, size_t i, float v) {
   else ((float*)p)[i] = v;
 }
 
-__device__ inline void epilogue(const EpiArgs& e, int M, int N, int m, int n, float acc) {
+__device__ __forceinline__ void epilogue(const EpiArgs& e, int M, int N, int m, int n, float acc) {
   if (m >= M || n >= N) return;
   const size_t mo = (size_t)m;
   switch (e.kind) {
@@ -87,6 +87,7 @@ __device__ inline void epilogue(const EpiArgs& e, int M, int N, int m, int n, fl
       break;
     }
     case EPI_ROPE:  // rotation already applied by the staged epilogue
+    case EPI_LOGITS:  // the staged epilogue adds the row statistics
       st_act(e.out, e.out_dtype, mo * e.ldo + n, acc);
       break;
   }
@@ -140,7 +141,7 @@ __device__ inline bool epi_vec_ok(const EpiArgs& e) {
   return (p & 15) == 0 && (l & 7) == 0;
 }
 
-__device__ inline void epilogue_v(const EpiArgs& e, int M, int N, int m, int n,
+__device__ __forceinline__ void epilogue_v(const EpiArgs& e, int M, int N, int m, int n,
                                   const float (&a)[EW], bool vec) {
   if (m >= M) return;
   if (!vec || n + EW > N) {
@@ -218,10 +219,14 @@ __device__ inline void epilogue_v(const EpiArgs& e, int M, int N, int m, int n,
       break;
     }
     case EPI_ROPE:  // rotation already applied by the staged epilogue
+    case EPI_LOGITS:
       stv_act(e.out, e.out_dtype, mo * e.ldo + n, a);
       break;
   }
 }
+
+// Online-softmax partials (max, sum exp(x - max), sum exp(x - max) w).
+struct SoftPart { float m, s, e; };
 
 // ------------------------------------------------------------- tile order
 // Grouped (GROUP_M row panels) order, then remapped so that the blocks the
@@ -252,7 +257,7 @@ __device__ inline void tile_coords(int nbm, int nbn, int& tm, int& tn) {
 // registers), then read back row-contiguously, which coalesces the global
 // stores of the epilogue.  Callers end their main loop with a barrier.
 template <int BM, int BN, int WM, int WN>
-__device__ inline void store_tile(const f32x16_t (&acc)[BM / WM / 32][BN / WN / 32],
+__device__ __forceinline__ void store_tile(const f32x16_t (&acc)[BM / WM / 32][BN / WN / 32],
                                   unsigned char* smem, const GemmDesc& g, const EpiArgs& e,
                                   int m0, int n0, int wave, int lane) {
   constexpr int TM = BM / WM, TN = BN / WN;
@@ -306,6 +311,45 @@ __device__ inline void store_tile(const f32x16_t (&acc)[BM / WM / 32][BN / WN / 
             v[k] = lo ? v[k] * cs[k].x - pv[k] * cs[k].y : v[k] * cs[k].x + pv[k] * cs[k].y;
         }
         epilogue_v(e, g.M, g.N, m, n, v, vec);
+      }
+    } else if (e.kind == EPI_LOGITS) {
+      // 8 lanes cover a 64-column block of one row (64 % EW == 0, TN % 64 == 0)
+      static_assert(TN % 64 == 0, "logit statistics need 64-column blocks");
+      for (int t = lane; t < 32 * QPR; t += 64) {
+        const int row = t / QPR, col = (t % QPR) * EW;
+        const int m = mb + row, n = nb + col;
+        float v[EW], w[EW];
+#pragma unroll
+        for (int k = 0; k < EW; k += 4) {
+          const float4 x = *reinterpret_cast<const float4*>(&ep[row * LDW + col + k]);
+          v[k] = x.x; v[k + 1] = x.y; v[k + 2] = x.z; v[k + 3] = x.w;
+          float4 y = make_float4(0.f, 0.f, 0.f, 0.f);
+          if (e.pair) y = *reinterpret_cast<const float4*>(&ep[(row ^ 1) * LDW + col + k]);
+          w[k] = x.x - y.x; w[k + 1] = x.y - y.y; w[k + 2] = x.z - y.z; w[k + 3] = x.w - y.w;
+        }
+        epilogue_v(e, g.M, g.N, m, n, v, vec);
+        // block maximum first (8 lanes), then one exponential per logit
+        float mx = -INFINITY;
+#pragma unroll
+        for (int k = 0; k < EW; ++k) mx = n + k < g.N ? fmaxf(mx, v[k]) : mx;
+#pragma unroll
+        for (int off = 1; off < 64 / EW; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+        SoftPart sp = {mx, 0.f, 0.f};
+        if (mx != -INFINITY) {
+#pragma unroll
+          for (int k = 0; k < EW; ++k) {
+            const float p = n + k < g.N ? __expf(v[k] - mx) : 0.f;
+            sp.s += p;
+            sp.e += p * w[k];
+          }
+        }
+#pragma unroll
+        for (int off = 1; off < 64 / EW; off <<= 1) {
+          sp.s += __shfl_xor(sp.s, off, 64);
+          sp.e += __shfl_xor(sp.e, off, 64);
+        }
+        if ((lane & (64 / EW - 1)) == 0 && m < g.M && n < g.N)
+          e.stats[(int64_t)m * e.ldst + n / 64] = make_float4(sp.m, sp.s, sp.e, 0.f);
       }
     } else {
       for (int t = lane; t < 32 * QPR; t += 64) {
@@ -1092,6 +1136,8 @@ hipError_t launch_gemm(const GemmDesc& g, const EpiArgs& e, int dtype, hipStream
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
   if (g.K2 < 0 || (g.K2 > 0 && (!g.A2 || !g.B2))) return hipErrorInvalidValue;
   if (e.kind == EPI_ROPE && (dtype != BF16 || e.hd > 128 || 128 % e.hd != 0 || !e.pos || !e.rope))
+    return hipErrorInvalidValue;
+  if (e.kind == EPI_LOGITS && (dtype != BF16 || !e.stats || e.out_dtype != F32 || (e.pair && g.M % 2)))
     return hipErrorInvalidValue;
   if (g.a_kmajor && g.b_kmajor) return run_layout<true, true>(g, e, dtype, s, kname);
   if (g.a_kmajor && !g.b_kmajor) return run_layout<true, false>(g, e, dtype, s, kname);

@@ -125,7 +125,18 @@ __global__ void __launch_bounds__(OT) objective_rows_kernel(ObjDesc o) {
   }
 
   Soft sp = {-INFINITY, 0.f, 0.f}, sq = {-INFINITY, 0.f, 0.f};
-  for (int v = threadIdx.x * 4; v < V4; v += OT * 4) {
+  if (o.stats) {  // partials of 64-column blocks from the logit GEMM's epilogue
+    const float4* st = o.stats + (int64_t)i * o.stacked * o.ldst;
+    for (int cb = threadIdx.x; cb < o.nst; cb += OT) {
+      const float4 p = st[cb];
+      sp = soft_merge(sp, {p.x, p.y, p.z});
+      if (zp) {
+        const float4 q = st[o.ldst + cb];
+        sq = soft_merge(sq, {q.x, q.y, q.z});
+      }
+    }
+  }
+  for (int v = o.stats ? V4 : threadIdx.x * 4; v < V4; v += OT * 4) {
     const float4 a4 = *reinterpret_cast<const float4*>(z + v);
     const float a[4] = {a4.x, a4.y, a4.z, a4.w};
     float b[4] = {0.f, 0.f, 0.f, 0.f};
@@ -140,7 +151,7 @@ __global__ void __launch_bounds__(OT) objective_rows_kernel(ObjDesc o) {
       sq = soft_add4(sq, b, ba);
     }
   }
-  for (int v = V4 + threadIdx.x; v < o.V; v += OT) {
+  for (int v = V4 + threadIdx.x; v < (o.stats ? 0 : o.V); v += OT) {
     const float a = z[v];
     const float b = zp ? zp[v] : 0.f;
     sp = soft_add(sp, a, a - b);

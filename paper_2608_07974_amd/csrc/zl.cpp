@@ -266,7 +266,8 @@ struct Plan {
   std::vector<size_t> X;  // L + 1
   std::vector<size_t> N1, RS1, MU1, QKV, O, LSE, X2, N2, RS2, MU2, UP, ACT;
   size_t DX, DXA, DUP, DN, DO, DQKV, DELTA, PART;
-  size_t HN, HRS, HMU, ZC, DZ, DNF, ROWLOSS, NOMEGA;
+  size_t HN, HRS, HMU, ZC, HST, DZ, DNF, ROWLOSS, NOMEGA;
+  int nst;  // 64-column blocks of a logit row (softmax partials, bf16 path)
   // readout adapter: act copy of h_out, pre-activation, activation, h',
   // dL/dh' (fp32 and act), dL/dU
   size_t AXO, AU, AG, AHP, ADHP, ADHPA, ADU;
@@ -332,6 +333,8 @@ void build_plan(const zl_config& c, Plan& p) {
   p.HRS = take(S2 * 4);
   p.HMU = take(S2 * 4);
   p.ZC = take(S2 * p.Vpad * 4);
+  p.nst = (m.V + 63) / 64;
+  p.HST = take(act == 2 ? S2 * p.nst * 16 : 0);
   p.DZ = take(R * p.Vpad * act);
   p.DNF = take(R * m.d * 4);
   p.ROWLOSS = take(T * 4);
@@ -801,7 +804,16 @@ zl_status zl_local_objective(zl_chunk* c, const int32_t* labels, float* loss_out
                             ln ? c->at<float>(p.HMU) : nullptr, c->at<float>(p.HRS), m.d,
                             c->cfg.norm_eps, s));
     {
-      EpiArgs e = epi(EPI_STORE, c->at<float>(p.ZC), p.Vpad, F32);
+      // bf16: the GEMM's epilogue also leaves per-row softmax partials of
+      // 64-column blocks (z rows paired with their z' rows), which replace
+      // the objective's statistics pass over the logits
+      const bool fused = act == BF16;
+      EpiArgs e = epi(fused ? EPI_LOGITS : EPI_STORE, c->at<float>(p.ZC), p.Vpad, F32);
+      if (fused) {
+        e.stats = c->at<float4>(p.HST);
+        e.ldst = p.nst;
+        e.pair = stk == 2;
+      }
       ZL_HIP(run_gemm(c, s, gdesc(stk * rows, m.V, m.d, c->ws + p.HN, m.d, true, c->buf.head_w, m.d,
                                true), e));
     }
@@ -812,6 +824,9 @@ zl_status zl_local_objective(zl_chunk* c, const int32_t* labels, float* loss_out
       o.alpha = c->cfg.alpha; o.consis = c->cfg.consis; o.n_omega = nomega;
       o.dz = c->ws + p.DZ; o.lddz = p.Vpad; o.dz_dtype = act;
       o.row_loss = c->at<float>(p.ROWLOSS) + r0;
+      o.stats = act == BF16 ? c->at<float4>(p.HST) : nullptr;
+      o.ldst = p.nst;
+      o.nst = p.nst;
       ZL_RUN("objective_rows", 0, (double)rows * (stk * 4.0 * m.V + c->asz() * p.Vpad), launch_objective_rows(o, s));
     }
     {
