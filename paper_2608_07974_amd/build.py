@@ -24,12 +24,35 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
          "-I", os.path.join(ROOT, "include"), "-Wno-unused-command-line-argument"]
 
 
+# Hot kernels must not use scratch memory: a spill or an argument block
+# copied to scratch costs far more than any schedule gains (checked from the
+# compiler's resource-usage remarks).
+NO_SCRATCH = {"gemm.hip": "gemm_dma_kernel", "attention_mfma.hip": "attn_"}
+
+
+def _scratch_users(stderr, pattern):
+    bad, name = [], None
+    for line in stderr.splitlines():
+        if "Function Name:" in line:
+            name = line.split("Function Name:")[1].split()[0]
+        elif "ScratchSize [bytes/lane]:" in line and name and pattern in name:
+            size = int(line.split("ScratchSize [bytes/lane]:")[1].split()[0])
+            if size:
+                bad.append((name, size))
+    return bad
+
+
 def _compile(src):
     obj = os.path.join(BUILD, src + ".o")
-    cmd = [HIPCC] + FLAGS + ["-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+    extra = ["-Rpass-analysis=kernel-resource-usage"] if src in NO_SCRATCH else []
+    cmd = [HIPCC] + FLAGS + extra + ["-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"compile failed: {src}\n{' '.join(cmd)}\n{r.stderr}")
+    if src in NO_SCRATCH:
+        bad = _scratch_users(r.stderr, NO_SCRATCH[src])
+        if bad:
+            raise RuntimeError(f"{src}: hot kernels use scratch memory: {bad}")
     return obj
 
 
