@@ -448,17 +448,35 @@ __global__ void __launch_bounds__(KV_NT) attn_dkv_mfma(AttnDesc a) {
     // some key of the wave lies after some query of the tile, or keys or
     // queries run past their ends
     const bool masked = kw0 + 15 > q0 || q0 + BT > a.S || kw0 + 16 > klim;
+    // Fragment reads run one step ahead of the MFMAs that use them: the Q /
+    // dO row fragments of the next 16-query block, and the transposed dO / Q
+    // column fragments of the next 16-wide dV / dK block (double-buffered).
+    bf16x8_t fq[2][HD / 32], fd[2][HD / 32];
+#pragma unroll
+    for (int kk = 0; kk < HD / 32; ++kk) {
+      fq[0][kk] = frag_row<HD>(qt, c, g + 4 * kk);
+      fd[0][kk] = frag_row<HD>(dt, c, g + 4 * kk);
+    }
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
       bf16x8_t pk, dsk;
 #pragma unroll
       for (int qq = 0; qq < 2; ++qq) {
-        const int qb = 2 * half + qq;
+        const int qb = 2 * half + qq, cur = qb & 1;
+        if (qb + 1 < 4) {
+#pragma unroll
+          for (int kk = 0; kk < HD / 32; ++kk) {
+            fq[cur ^ 1][kk] = frag_row<HD>(qt, (qb + 1) * 16 + c, g + 4 * kk);
+            fd[cur ^ 1][kk] = frag_row<HD>(dt, (qb + 1) * 16 + c, g + 4 * kk);
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        // two independent accumulation chains, interleaved
         f32x4_t sc = f32x4_t{0.f, 0.f, 0.f, 0.f}, dp = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kk = 0; kk < HD / 32; ++kk) {
-          sc = mfma16(frag_row<HD>(qt, qb * 16 + c, g + 4 * kk), kf[kk], sc);
-          dp = mfma16(frag_row<HD>(dt, qb * 16 + c, g + 4 * kk), vf[kk], dp);
+          sc = mfma16(fq[cur][kk], kf[kk], sc);
+          dp = mfma16(fd[cur][kk], vf[kk], dp);
         }
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -474,10 +492,19 @@ __global__ void __launch_bounds__(KV_NT) attn_dkv_mfma(AttnDesc a) {
         }
       }
       // dV += P^T dO, dK += dS^T Q over this half's 32 queries
+      bf16x8_t dcol[2], qcol[2];
+      dcol[0] = frag_col<HD>(dt, 32 * half, g, 0, c);
+      qcol[0] = frag_col<HD>(qt, 32 * half, g, 0, c);
 #pragma unroll
       for (int db = 0; db < HD / 16; ++db) {
-        dv[db] = mfma16(pk, frag_col<HD>(dt, 32 * half, g, 16 * db, c), dv[db]);
-        dk[db] = mfma16(dsk, frag_col<HD>(qt, 32 * half, g, 16 * db, c), dk[db]);
+        const int cur = db & 1;
+        if (db + 1 < HD / 16) {
+          dcol[cur ^ 1] = frag_col<HD>(dt, 32 * half, g, 16 * (db + 1), c);
+          qcol[cur ^ 1] = frag_col<HD>(qt, 32 * half, g, 16 * (db + 1), c);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        dv[db] = mfma16(pk, dcol[cur], dv[db]);
+        dk[db] = mfma16(dsk, qcol[cur], dk[db]);
       }
     }
     if (pr + 1 < npair) commit(pr + 1);
