@@ -247,16 +247,29 @@ __global__ void __launch_bounds__(FW_NT) attn_fwd_mfma(AttnDesc a) {
     if (k0 >= kend_w) continue;  // past every key this wave's queries see
     const bf16_t* kt = reinterpret_cast<const bf16_t*>(smem + (t & 1) * 2 * TB);
     const bf16_t* vt = kt + BT * HD;
+    // S^T: 8 independent accumulators per k-step; the K fragments of the
+    // next k-step are read while the current step's MFMAs run
     f32x4_t s[2][4];
+    bf16x8_t kb[2][4];
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) {
       s[0][blk] = f32x4_t{0.f, 0.f, 0.f, 0.f};
       s[1][blk] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      kb[0][blk] = frag_row<HD>(kt, blk * 16 + c, g);
+    }
 #pragma unroll
-      for (int kk = 0; kk < HD / 32; ++kk) {
-        const bf16x8_t kf = frag_row<HD>(kt, blk * 16 + c, g + 4 * kk);
-        s[0][blk] = mfma16(kf, qf[0][kk], s[0][blk]);
-        s[1][blk] = mfma16(kf, qf[1][kk], s[1][blk]);
+    for (int kk = 0; kk < HD / 32; ++kk) {
+      const int cur = kk & 1;
+      if (kk + 1 < HD / 32) {
+#pragma unroll
+        for (int blk = 0; blk < 4; ++blk)
+          kb[cur ^ 1][blk] = frag_row<HD>(kt, blk * 16 + c, g + 4 * (kk + 1));
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int blk = 0; blk < 4; ++blk) {
+        s[0][blk] = mfma16(kb[cur][blk], qf[0][kk], s[0][blk]);
+        s[1][blk] = mfma16(kb[cur][blk], qf[1][kk], s[1][blk]);
       }
     }
     // some key of the tile lies after some query of the wave, or past kend
@@ -305,14 +318,17 @@ __global__ void __launch_bounds__(FW_NT) attn_fwd_mfma(AttnDesc a) {
         }
       lsum[j] += psum;
     }
+    bf16x8_t vb[2];
+    vb[0] = frag_col<HD>(vt, 0, g, 0, c);
 #pragma unroll
-    for (int db = 0; db < HD / 16; ++db)
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-        const bf16x8_t vf = frag_col<HD>(vt, 32 * kk, g, 16 * db, c);
-        o[0][db] = mfma16(vf, pf[0][kk], o[0][db]);
-        o[1][db] = mfma16(vf, pf[1][kk], o[1][db]);
-      }
+    for (int i = 0; i < 2 * (HD / 16); ++i) {  // i = 2 db + kk
+      const int db = i >> 1, kk = i & 1, cur = i & 1;
+      if (i + 1 < 2 * (HD / 16))
+        vb[cur ^ 1] = frag_col<HD>(vt, 32 * ((i + 1) & 1), g, 16 * ((i + 1) >> 1), c);
+      __builtin_amdgcn_sched_barrier(0);
+      o[0][db] = mfma16(vb[cur], pf[0][kk], o[0][db]);
+      o[1][db] = mfma16(vb[cur], pf[1][kk], o[1][db]);
+    }
   }
   dma_wait();
 #pragma unroll
@@ -603,6 +619,11 @@ __global__ void __launch_bounds__(FW_NT) attn_dq_mfma(AttnDesc a) {
     const bf16_t* vt = kt + BT * HD;
     const bool masked = k0 + BT - 1 > qw0 || k0 + BT > kend;
     bf16x8_t dsk[2][2];
+    // K / V fragments of the next (block, k-step) are read while the
+    // current step's four independent MFMAs run
+    bf16x8_t ka[2], va[2];
+    ka[0] = frag_row<HD>(kt, c, g);
+    va[0] = frag_row<HD>(vt, c, g);
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) {
       f32x4_t st[2], dpt[2];
@@ -613,12 +634,17 @@ __global__ void __launch_bounds__(FW_NT) attn_dq_mfma(AttnDesc a) {
       }
 #pragma unroll
       for (int kk = 0; kk < HD / 32; ++kk) {
-        const bf16x8_t ka = frag_row<HD>(kt, blk * 16 + c, g + 4 * kk);
-        const bf16x8_t va = frag_row<HD>(vt, blk * 16 + c, g + 4 * kk);
+        const int i = blk * (HD / 32) + kk, cur = i & 1;
+        if (i + 1 < 4 * (HD / 32)) {
+          const int nb = (i + 1) / (HD / 32), nk = (i + 1) % (HD / 32);
+          ka[cur ^ 1] = frag_row<HD>(kt, nb * 16 + c, g + 4 * nk);
+          va[cur ^ 1] = frag_row<HD>(vt, nb * 16 + c, g + 4 * nk);
+        }
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-          st[j] = mfma16(ka, qf[j][kk], st[j]);
-          dpt[j] = mfma16(va, df[j][kk], dpt[j]);
+          st[j] = mfma16(ka[cur], qf[j][kk], st[j]);
+          dpt[j] = mfma16(va[cur], df[j][kk], dpt[j]);
         }
       }
 #pragma unroll
@@ -634,14 +660,17 @@ __global__ void __launch_bounds__(FW_NT) attn_dq_mfma(AttnDesc a) {
           dsk[j][blk >> 1][(blk & 1) * 4 + r] = (__bf16)(p * (dpt[j][r] - dl[j]));
         }
     }
+    bf16x8_t kc[2];
+    kc[0] = frag_col<HD>(kt, 0, g, 0, c);
 #pragma unroll
-    for (int db = 0; db < HD / 16; ++db)
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-        const bf16x8_t kb = frag_col<HD>(kt, 32 * kk, g, 16 * db, c);
-        dq[0][db] = mfma16(dsk[0][kk], kb, dq[0][db]);
-        dq[1][db] = mfma16(dsk[1][kk], kb, dq[1][db]);
-      }
+    for (int i = 0; i < 2 * (HD / 16); ++i) {  // i = 2 db + kk
+      const int db = i >> 1, kk = i & 1, cur = i & 1;
+      if (i + 1 < 2 * (HD / 16))
+        kc[cur ^ 1] = frag_col<HD>(kt, 32 * ((i + 1) & 1), g, 16 * ((i + 1) >> 1), c);
+      __builtin_amdgcn_sched_barrier(0);
+      dq[0][db] = mfma16(dsk[0][kk], kc[cur], dq[0][db]);
+      dq[1][db] = mfma16(dsk[1][kk], kc[cur], dq[1][db]);
+    }
   }
   dma_wait();
   bf16_t* DQ = reinterpret_cast<bf16_t*>(a.dq);
