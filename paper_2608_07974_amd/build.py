@@ -21,7 +21,10 @@ SOURCES = ["gemm.hip", "attention.hip", "attention_mfma.hip", "rowops.hip",
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-         "-I", os.path.join(ROOT, "include"), "-Wno-unused-command-line-argument"]
+         "-I", os.path.join(ROOT, "include"), "-Wno-unused-command-line-argument",
+         # a requested unroll that fails leaves register arrays indexed at run
+         # time (scratch memory): make it an error
+         "-Werror=pass-failed"]
 
 
 # Hot kernels must not use scratch memory: a spill or an argument block

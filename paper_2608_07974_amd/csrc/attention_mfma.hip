@@ -744,8 +744,10 @@ static hipError_t bwd(const AttnDesc& a, hipStream_t s) {
     once = true;
   }
   const int64_t rows = (int64_t)a.B * a.Hq * a.S;
-  hipLaunchKernelGGL(attn_delta_mfma<HD>, dim3((unsigned)((rows * 64 + 255) / 256)), dim3(256), 0,
-                     s, a);
+  if (!a.delta_ready) {
+    hipLaunchKernelGGL(attn_delta_mfma<HD>, dim3((unsigned)((rows * 64 + 255) / 256)), dim3(256), 0,
+                       s, a);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 gk((a.S + BW - 1) / BW, a.Hkv, a.B);

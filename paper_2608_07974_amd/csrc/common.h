@@ -79,6 +79,10 @@ enum EpiKind {
                        // sum exp(x - max), sum exp(x - max) (x - x'), 0) over
                        // the block's columns < N, x' = row m ^ 1 (pair != 0)
                        // else 0.  MFMA (bf16) paths only.
+  EPI_STORE_DELTA = 8, // EPI_STORE (act dtype) of dO, plus the attention
+                       // backward's delta[(b * nheads + h) * seq + s] = sum over
+                       // head h's hd columns of dO (as stored) * aux, aux = O,
+                       // row m = b * seq + s.  MFMA (bf16) paths only.
 };
 
 struct EpiArgs {
@@ -96,6 +100,8 @@ struct EpiArgs {
   int ff;               // EPI_SWIGLU_BWD column offset of u / du
   float scale;          // EPI_GRAD, EPI_STORE (out = scale * acc + bias)
   int accumulate;       // EPI_GRAD
+  float* delta;         // EPI_STORE_DELTA (also uses aux, ldaux, hd)
+  int seq, nheads;
   float4* stats;        // EPI_LOGITS
   int64_t ldst;
   int pair;
@@ -177,6 +183,7 @@ struct AttnDesc {
   // backward
   const void* dout; int64_t lddo;
   float* delta;                                  // [B, Hq, S]
+  int delta_ready;                               // delta already formed (skip its kernel)
   void* dq; void* dk; void* dv; int64_t lddq, lddk, lddv;
   float scale;
   // optional inverse RoPE of dq / dk in the backward (rope != nullptr)

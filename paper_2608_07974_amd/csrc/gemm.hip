@@ -36,10 +36,10 @@ __device__ inline float gelu_grad_f(float x) {
   return 0.5f * (1.f + t) + 0.5f * x * dt;
 }
 
-__device__ inline float ld_act(const void* p, int dt, size_t i) {
+__device__ __forceinline__ float ld_act(const void* p, int dt, size_t i) {
   return dt == BF16 ? bf16_to_f32(((const bf16_t*)p)[i]) : ((const float*)p)[i];
 }
-__device__ inline void st_act(void* p, int dt, size_t i, float v) {
+__device__ __forceinline__ void st_act(void* p, int dt, size_t i, float v) {
   if (dt == BF16) ((bf16_t*)p)[i] = f32_to_bf16(v);
   else ((float*)p)[i] = v;
 }
@@ -48,7 +48,8 @@ __device__ __forceinline__ void epilogue(const EpiArgs& e, int M, int N, int m, 
   if (m >= M || n >= N) return;
   const size_t mo = (size_t)m;
   switch (e.kind) {
-    case EPI_STORE: {
+    case EPI_STORE:
+    case EPI_STORE_DELTA: {
       float v = e.scale * acc + (e.bias ? e.bias[n] : 0.f);
       st_act(e.out, e.out_dtype, mo * e.ldo + n, v);
       break;
@@ -99,14 +100,14 @@ __device__ __forceinline__ void epilogue(const EpiArgs& e, int M, int N, int m, 
 // the same arithmetic as epilogue(); the column tail and unaligned operands
 // take the scalar path.
 constexpr int EW = 8;
-__device__ inline void ldv_f32(const float* p, float (&v)[EW]) {
+__device__ __forceinline__ void ldv_f32(const float* p, float (&v)[EW]) {
 #pragma unroll
   for (int k = 0; k < EW; k += 4) {
     const float4 f = *reinterpret_cast<const float4*>(p + k);
     v[k] = f.x; v[k + 1] = f.y; v[k + 2] = f.z; v[k + 3] = f.w;
   }
 }
-__device__ inline void ldv_act(const void* p, int dt, size_t i, float (&v)[EW]) {
+__device__ __forceinline__ void ldv_act(const void* p, int dt, size_t i, float (&v)[EW]) {
   if (dt == BF16) {
     const uint4 u = *reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(p) + i);
     const uint32_t w[4] = {u.x, u.y, u.z, u.w};
@@ -119,7 +120,7 @@ __device__ inline void ldv_act(const void* p, int dt, size_t i, float (&v)[EW]) 
     ldv_f32(static_cast<const float*>(p) + i, v);
   }
 }
-__device__ inline void stv_act(void* p, int dt, size_t i, const float (&v)[EW]) {
+__device__ __forceinline__ void stv_act(void* p, int dt, size_t i, const float (&v)[EW]) {
   if (dt == BF16) {
     uint32_t w[4];
 #pragma unroll
@@ -134,7 +135,7 @@ __device__ inline void stv_act(void* p, int dt, size_t i, const float (&v)[EW]) 
   }
 }
 
-__device__ inline bool epi_vec_ok(const EpiArgs& e) {
+__device__ __forceinline__ bool epi_vec_ok(const EpiArgs& e) {
   const uintptr_t p = (uintptr_t)e.out | (uintptr_t)e.bias | (uintptr_t)e.resid |
                       (uintptr_t)e.out2 | (uintptr_t)e.aux;
   const int64_t l = e.ldo | e.ldr | e.ldo2 | e.ldaux | (int64_t)e.ff;
@@ -153,10 +154,12 @@ __device__ __forceinline__ void epilogue_v(const EpiArgs& e, int M, int N, int m
   float v[EW], b[EW];
 #pragma unroll
   for (int i = 0; i < EW; ++i) b[i] = 0.f;
-  if (e.bias && (e.kind == EPI_STORE || e.kind == EPI_RESID || e.kind == EPI_GELU))
+  if (e.bias && (e.kind == EPI_STORE || e.kind == EPI_STORE_DELTA || e.kind == EPI_RESID ||
+                 e.kind == EPI_GELU))
     ldv_f32(e.bias + n, b);
   switch (e.kind) {
     case EPI_STORE:
+    case EPI_STORE_DELTA:
 #pragma unroll
       for (int i = 0; i < EW; ++i) v[i] = e.scale * a[i] + b[i];
       stv_act(e.out, e.out_dtype, mo * e.ldo + n, v);
@@ -267,13 +270,15 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[BM / WM / 32][B
   static_assert(WM * WN * 32 * LDW * 4 <= 160 * 1024, "epilogue tile exceeds LDS");
   float* ep = reinterpret_cast<float*>(smem) + wave * 32 * LDW;
   const bool vec = epi_vec_ok(e);
-#pragma unroll
-  for (int i = 0; i < FM; ++i) {
+  // One 32-row block per call; the calls are spelled out (not a loop) so
+  // that every acc index stays a compile-time constant however large the
+  // epilogue grows (a rolled loop would move acc to scratch memory).
+  auto chunk = [&](const f32x16_t (&ai)[FN], const int i) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < FN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r)
-        ep[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * LDW + j * 32 + (lane & 31)] = acc[i][j][r];
+        ep[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * LDW + j * 32 + (lane & 31)] = ai[j][r];
     __syncthreads();
     const int mb = m0 + wm * TM + i * 32, nb = n0 + wn * TN;
     // EW consecutive columns per lane: a row of TN columns takes TN / EW lanes
@@ -311,6 +316,37 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[BM / WM / 32][B
             v[k] = lo ? v[k] * cs[k].x - pv[k] * cs[k].y : v[k] * cs[k].x + pv[k] * cs[k].y;
         }
         epilogue_v(e, g.M, g.N, m, n, v, vec);
+      }
+    } else if (e.kind == EPI_STORE_DELTA) {
+      // the hd / EW lanes of one head's columns in a row sum dO (as stored)
+      // times O, giving the attention backward's delta of (row, head)
+      const int lph = e.hd / EW;
+      for (int t = lane; t < 32 * QPR; t += 64) {
+        const int row = t / QPR, col = (t % QPR) * EW;
+        const int m = mb + row, n = nb + col;
+        float v[EW];
+#pragma unroll
+        for (int k = 0; k < EW; k += 4) {
+          const float4 x = *reinterpret_cast<const float4*>(&ep[row * LDW + col + k]);
+          v[k] = x.x; v[k + 1] = x.y; v[k + 2] = x.z; v[k + 3] = x.w;
+        }
+        epilogue_v(e, g.M, g.N, m, n, v, vec);
+        float ds = 0.f;
+        if (m < g.M && n < g.N) {
+          float o[EW];
+          ldv_act(e.aux, e.out_dtype, (size_t)m * e.ldaux + n, o);
+#pragma unroll
+          for (int k = 0; k < EW; ++k) {
+            const float d = e.out_dtype == BF16 ? bf16_to_f32(f32_to_bf16(e.scale * v[k]))
+                                                : e.scale * v[k];
+            ds += d * o[k];
+          }
+        }
+        for (int off = 1; off < lph; off <<= 1) ds += __shfl_xor(ds, off, 64);
+        if ((lane & (lph - 1)) == 0 && m < g.M && n < g.N) {
+          const int b = m / e.seq, sq = m - b * e.seq, h = n / e.hd;
+          e.delta[((int64_t)b * e.nheads + h) * e.seq + sq] = ds;
+        }
       }
     } else if (e.kind == EPI_LOGITS) {
       // 8 lanes cover a 64-column block of one row (64 % EW == 0, TN % 64 == 0)
@@ -364,7 +400,12 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[BM / WM / 32][B
       }
     }
     __syncthreads();
-  }
+  };
+  static_assert(FM >= 1 && FM <= 4, "32-row blocks per wave tile");
+  chunk(acc[0], 0);
+  if constexpr (FM > 1) chunk(acc[1], 1);
+  if constexpr (FM > 2) chunk(acc[2], 2);
+  if constexpr (FM > 3) chunk(acc[3], 3);
 }
 
 // ------------------------------------------------------------ MFMA kernel
@@ -1096,8 +1137,8 @@ static hipError_t run_layout(const GemmDesc& g, const EpiArgs& e, int dtype, hip
     which = 0;
   } else {
     const long big = (long)((g.M + 255) / 256) * ((g.N + 255) / 256);
-    // the RoPE epilogue needs head-aligned wave tiles of 128 columns
-    const bool large = big >= 240 || e.kind == EPI_ROPE;
+    // the RoPE and delta epilogues need head-aligned wave tiles of 128 columns
+    const bool large = big >= 240 || e.kind == EPI_ROPE || e.kind == EPI_STORE_DELTA;
     const int R = large ? 256 : 128;
     const bool dma = dma_operand_ok(g.A, g.lda, AK, g.M, g.ka, R) &&
                      dma_operand_ok(g.B, g.ldb, BKM, g.N, g.kb, R) &&
@@ -1138,6 +1179,10 @@ hipError_t launch_gemm(const GemmDesc& g, const EpiArgs& e, int dtype, hipStream
   if (e.kind == EPI_ROPE && (dtype != BF16 || e.hd > 128 || 128 % e.hd != 0 || !e.pos || !e.rope))
     return hipErrorInvalidValue;
   if (e.kind == EPI_LOGITS && (dtype != BF16 || !e.stats || e.out_dtype != F32 || (e.pair && g.M % 2)))
+    return hipErrorInvalidValue;
+  if (e.kind == EPI_STORE_DELTA &&
+      (dtype != BF16 || !e.delta || !e.aux || e.hd < EW || e.hd > 128 || 128 % e.hd ||
+       e.seq < 1 || e.nheads < 1 || e.bias || (int64_t)e.nheads * e.hd != g.N || g.M % e.seq))
     return hipErrorInvalidValue;
   if (g.a_kmajor && g.b_kmajor) return run_layout<true, true>(g, e, dtype, s, kname);
   if (g.a_kmajor && !g.b_kmajor) return run_layout<true, false>(g, e, dtype, s, kname);

@@ -998,9 +998,15 @@ zl_status zl_chunk_backward(zl_chunk* c, float grad_scale, int accumulate, void*
         if (ln) ZL_RUN("reduce_rows", 0, 0, launch_reduce_rows(PART + half_part, nblk, m.d, c->G(o.ln2_b), grad_scale, acc, s));
       }
     }
-    // output projection
+    // output projection; in bf16 its epilogue also forms the attention
+    // backward's delta = rowsum(dO * O) per head
+    const bool delta_fused = act == BF16 && (m.hd == 64 || m.hd == 128);
     {
-      EpiArgs e = epi(EPI_STORE, DO, m.dq, act);
+      EpiArgs e = epi(delta_fused ? EPI_STORE_DELTA : EPI_STORE, DO, m.dq, act);
+      if (delta_fused) {
+        e.aux = c->ws + p.O[l]; e.ldaux = m.dq; e.hd = m.hd;
+        e.delta = c->at<float>(p.DELTA); e.seq = c->S; e.nheads = m.hq;
+      }
       GemmDesc g = gdesc(T, m.dq, m.d, DXA, m.d, true, c->W(o.w_o), m.dq, false);
       if (r) ZL_HIP(lora_bwd_dx(DXA, m.d, lo->o_a, r, lo->o_b, w_d, 1, m.dq, true, g));
       ZL_HIP(run_gemm(c, s, g, e));
@@ -1024,6 +1030,7 @@ zl_status zl_chunk_backward(zl_chunk* c, float grad_scale, int accumulate, void*
       a.seq_lens = c->at<int32_t>(p.seqlens);
       a.dout = DO; a.lddo = m.dq;
       a.delta = c->at<float>(p.DELTA);
+      a.delta_ready = delta_fused ? 1 : 0;
       a.dq = DQKV; a.dk = c->A(p.DQKV, m.dq); a.dv = c->A(p.DQKV, m.dq + m.dkv);
       a.lddq = a.lddk = a.lddv = m.nqkv;
       a.scale = 1.f / sqrtf((float)m.hd);
