@@ -27,6 +27,7 @@ __device__ inline float wave_sum(float v) {
   return v;
 }
 
+template <int CM>
 __global__ void __launch_bounds__(RT)
 norm_fwd_kernel(int layernorm, const float* __restrict__ xa, const float* __restrict__ xb,
                 int64_t ldx, int row0, const float* __restrict__ w, const float* __restrict__ b,
@@ -38,19 +39,22 @@ norm_fwd_kernel(int layernorm, const float* __restrict__ xa, const float* __rest
   const float* x;
   if (xb) x = ((r & 1) ? xb : xa) + (int64_t)(row0 + (r >> 1)) * ldx;
   else x = xa + (int64_t)(row0 + r) * ldx;
-  float mu = 0.f;
-  if (layernorm) {
-    float s = 0.f;
-    for (int c = lane * 4; c < d; c += 256) {
-      const float4 v = *reinterpret_cast<const float4*>(x + c);
-      s += (v.x + v.y) + (v.z + v.w);
-    }
-    mu = wave_sum(s) / d;
+  // the row is read once into registers (lane owns columns 256 k + 4 lane)
+  float4 xv[CM];
+  float s = 0.f;
+#pragma unroll
+  for (int k = 0; k < CM; ++k) {
+    const int c = k * 256 + lane * 4;
+    xv[k] = c < d ? *reinterpret_cast<const float4*>(x + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+    s += (xv[k].x + xv[k].y) + (xv[k].z + xv[k].w);
   }
+  const float mu = layernorm ? wave_sum(s) / d : 0.f;
   float q = 0.f;
-  for (int c = lane * 4; c < d; c += 256) {
-    const float4 v = *reinterpret_cast<const float4*>(x + c);
-    const float a0 = v.x - mu, a1 = v.y - mu, a2 = v.z - mu, a3 = v.w - mu;
+#pragma unroll
+  for (int k = 0; k < CM; ++k) {
+    const int c = k * 256 + lane * 4;
+    if (c >= d) continue;
+    const float a0 = xv[k].x - mu, a1 = xv[k].y - mu, a2 = xv[k].z - mu, a3 = xv[k].w - mu;
     q += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
   }
   const float rs = rsqrtf(wave_sum(q) / d + eps);
@@ -58,8 +62,11 @@ norm_fwd_kernel(int layernorm, const float* __restrict__ xa, const float* __rest
     rstd[r] = rs;
     if (layernorm && mean) mean[r] = mu;
   }
-  for (int c = lane * 4; c < d; c += 256) {
-    const float4 v = *reinterpret_cast<const float4*>(x + c);
+#pragma unroll
+  for (int k = 0; k < CM; ++k) {
+    const int c = k * 256 + lane * 4;
+    if (c >= d) continue;
+    const float4 v = xv[k];
     const float4 g = *reinterpret_cast<const float4*>(w + c);
     float o0 = (v.x - mu) * rs * g.x, o1 = (v.y - mu) * rs * g.y;
     float o2 = (v.z - mu) * rs * g.z, o3 = (v.w - mu) * rs * g.w;
@@ -77,13 +84,31 @@ norm_fwd_kernel(int layernorm, const float* __restrict__ xa, const float* __rest
   }
 }
 
+static hipError_t norm_fwd_go(int layernorm, const float* xa, const float* xb, int64_t ldx,
+                              int row0, const float* w, const float* b, void* y, int64_t ldy,
+                              int ydt, float* mean, float* rstd, int rows, int d, float eps,
+                              hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if (d <= 0 || d % 4 || d > 8192) return hipErrorInvalidValue;
+  const dim3 grid((rows + 3) / 4), blk(RT);
+  const int cm = (d + 255) / 256;
+#define ZL_NF(CM) hipLaunchKernelGGL(norm_fwd_kernel<CM>, grid, blk, 0, s, layernorm, xa, xb, ldx, \
+                                     row0, w, b, y, ldy, ydt, mean, rstd, rows, d, eps)
+  if (cm <= 1) ZL_NF(1);
+  else if (cm <= 2) ZL_NF(2);
+  else if (cm <= 4) ZL_NF(4);
+  else if (cm <= 8) ZL_NF(8);
+  else if (cm <= 16) ZL_NF(16);
+  else ZL_NF(32);
+#undef ZL_NF
+  return hipGetLastError();
+}
+
 hipError_t launch_norm_fwd(bool layernorm, const float* x, int64_t ldx, const float* w,
                            const float* b, void* y, int64_t ldy, int ydtype, float* mean,
                            float* rstd, int T, int d, float eps, hipStream_t s) {
-  if (T <= 0) return hipSuccess;
-  hipLaunchKernelGGL(norm_fwd_kernel, dim3((T + 3) / 4), dim3(RT), 0, s, (int)layernorm, x,
-                     (const float*)nullptr, ldx, 0, w, b, y, ldy, ydtype, mean, rstd, T, d, eps);
-  return hipGetLastError();
+  return norm_fwd_go((int)layernorm, x, nullptr, ldx, 0, w, b, y, ldy, ydtype, mean, rstd, T, d,
+                     eps, s);
 }
 
 hipError_t launch_head_norm(bool layernorm, const float* xa, const float* xb, int64_t ldx,
@@ -91,26 +116,26 @@ hipError_t launch_head_norm(bool layernorm, const float* xa, const float* xb, in
                             int ydtype, float* mean, float* rstd, int d, float eps,
                             hipStream_t s) {
   const int out_rows = xb ? 2 * rows : rows;
-  if (out_rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(norm_fwd_kernel, dim3((out_rows + 3) / 4), dim3(RT), 0, s, (int)layernorm,
-                     xa, xb, ldx, row0, w, b, y, (int64_t)d, ydtype, mean, rstd, out_rows, d, eps);
-  return hipGetLastError();
+  return norm_fwd_go((int)layernorm, xa, xb, ldx, row0, w, b, y, (int64_t)d, ydtype, mean, rstd,
+                     out_rows, d, eps, s);
 }
 
 // ---------------------------------------------------------- norm backward
-// One wave per row, each wave owning a contiguous run of rows.  Per row:
+// One 256-thread block per run of rows; thread t owns columns 4 (256 k + t)
+// .. +3 (CM float4 groups), so a row is read once: dy and x stay in
+// registers between the row reduction and dx.  Per row:
 // g = dy * w, xhat = (x - mean) * rstd,
 //   rms: dx = rstd * (g - xhat * mean(g * xhat))
 //   ln:  dx = rstd * (g - mean(g) - xhat * mean(g * xhat))
-// The weight-gradient partials sum(dy * xhat) (and sum(dy)) over the wave's
-// rows accumulate in registers (lane l owns columns 256 k + 4 l .. +3, CM
-// chunks) and are written as one row of part_w / part_b per wave:
-// deterministic, no atomics, no LDS, so many waves stay resident.
+// The row sums meet across the 4 waves in LDS (double-buffered, one
+// barrier per row).  The weight-gradient partials sum(dy * xhat) (and
+// sum(dy)) of the block's rows stay in registers and are written as one
+// row of part_w / part_b per block: deterministic, no atomics.
 int norm_bwd_blocks(int T) {
-  // about four rows per wave, at least 1024 waves when there are rows for them
-  int waves = T / 4;
-  if (waves < 1024) waves = T < 1024 ? T : 1024;
-  return waves > 0 ? waves : 1;  // number of partial rows
+  int blocks = T / 16;  // about 16 rows per block
+  if (blocks < 256) blocks = T < 256 ? T : 256;
+  if (blocks > 2048) blocks = 2048;
+  return blocks > 0 ? blocks : 1;  // number of partial rows
 }
 
 template <int CM, bool LN>
@@ -119,57 +144,70 @@ norm_bwd_kernel(const float* __restrict__ dy, int64_t lddy, const float* __restr
                 const float* __restrict__ w, const float* __restrict__ mean,
                 const float* __restrict__ rstd, int rstride, const float* dres, float* dx,
                 void* dx_act, int adt, float* __restrict__ part_w, float* __restrict__ part_b,
-                int T, int d, int rpw, int nwaves, int row_out0) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int gw = blockIdx.x * (RT / 64) + wave;
+                int T, int d, int rpb, int nblk, int row_out0) {
+  __shared__ float red[2][2][RT / 64];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const bool want_part = part_w != nullptr;
-  float4 aw[CM], ab[CM];
+  float4 wv[CM], aw[CM], ab[CM];
 #pragma unroll
   for (int k = 0; k < CM; ++k) {
+    const int c = (k * RT + tid) * 4;
+    wv[k] = c < d ? *reinterpret_cast<const float4*>(w + c) : make_float4(0.f, 0.f, 0.f, 0.f);
     aw[k] = make_float4(0.f, 0.f, 0.f, 0.f);
     ab[k] = aw[k];
   }
-  const int r0 = gw * rpw, r1 = min(T, r0 + rpw);
-  for (int r = (gw < nwaves ? r0 : T); r < r1; ++r) {
+  const int r0 = blockIdx.x * rpb, r1 = min(T, r0 + rpb);
+  int par = 0;
+  for (int r = (blockIdx.x < nblk ? r0 : T); r < r1; ++r) {
     const float rs = rstd[(int64_t)r * rstride];
     const float mu = LN ? mean[(int64_t)r * rstride] : 0.f;
     const int ro = row_out0 + r;
     const float* dyr = dy + (int64_t)r * lddy;
     const float* xr = x + (int64_t)ro * d;
+    float4 av[CM], hv[CM];
     float sg = 0.f, sgx = 0.f;
 #pragma unroll
     for (int k = 0; k < CM; ++k) {
-      const int c = k * 256 + lane * 4;
-      if (c >= d) continue;
+      const int c = (k * RT + tid) * 4;
+      if (c >= d) { av[k] = make_float4(0.f, 0.f, 0.f, 0.f); hv[k] = av[k]; continue; }
       const float4 a = *reinterpret_cast<const float4*>(dyr + c);
       const float4 v = *reinterpret_cast<const float4*>(xr + c);
-      const float4 g = *reinterpret_cast<const float4*>(w + c);
-      const float h0 = (v.x - mu) * rs, h1 = (v.y - mu) * rs, h2 = (v.z - mu) * rs, h3 = (v.w - mu) * rs;
+      const float4 g = wv[k];
+      const float4 h = make_float4((v.x - mu) * rs, (v.y - mu) * rs, (v.z - mu) * rs, (v.w - mu) * rs);
+      av[k] = a;
+      hv[k] = h;
       const float g0 = a.x * g.x, g1 = a.y * g.y, g2 = a.z * g.z, g3 = a.w * g.w;
       sg += (g0 + g1) + (g2 + g3);
-      sgx += (g0 * h0 + g1 * h1) + (g2 * h2 + g3 * h3);
+      sgx += (g0 * h.x + g1 * h.y) + (g2 * h.z + g3 * h.w);
       if (want_part) {
-        aw[k].x += a.x * h0; aw[k].y += a.y * h1; aw[k].z += a.z * h2; aw[k].w += a.w * h3;
+        aw[k].x += a.x * h.x; aw[k].y += a.y * h.y; aw[k].z += a.z * h.z; aw[k].w += a.w * h.w;
         if (LN) { ab[k].x += a.x; ab[k].y += a.y; ab[k].z += a.z; ab[k].w += a.w; }
       }
     }
     if (!dx) continue;
-    const float mg = LN ? wave_sum(sg) / d : 0.f;
-    const float mgx = wave_sum(sgx) / d;
+    sg = wave_sum(sg);
+    sgx = wave_sum(sgx);
+    if (lane == 0) {
+      red[par][0][wave] = sg;
+      red[par][1][wave] = sgx;
+    }
+    __syncthreads();
+    float tg = 0.f, tgx = 0.f;
+#pragma unroll
+    for (int i = 0; i < RT / 64; ++i) {
+      tg += red[par][0][i];
+      tgx += red[par][1][i];
+    }
+    par ^= 1;
+    const float mg = LN ? tg / d : 0.f;
+    const float mgx = tgx / d;
 #pragma unroll
     for (int k = 0; k < CM; ++k) {
-      const int c = k * 256 + lane * 4;
+      const int c = (k * RT + tid) * 4;
       if (c >= d) continue;
-      const float4 a = *reinterpret_cast<const float4*>(dyr + c);
-      const float4 v = *reinterpret_cast<const float4*>(xr + c);
-      const float4 g = *reinterpret_cast<const float4*>(w + c);
-      float o[4];
-      const float av[4] = {a.x, a.y, a.z, a.w}, vv[4] = {v.x, v.y, v.z, v.w}, gv[4] = {g.x, g.y, g.z, g.w};
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float h = (vv[q] - mu) * rs;
-        o[q] = rs * (av[q] * gv[q] - mg - h * mgx);
-      }
+      const float4 a = av[k], h = hv[k], g = wv[k];
+      float o[4] = {rs * (a.x * g.x - mg - h.x * mgx), rs * (a.y * g.y - mg - h.y * mgx),
+                    rs * (a.z * g.z - mg - h.z * mgx), rs * (a.w * g.w - mg - h.w * mgx)};
       const int64_t off = (int64_t)ro * d + c;
       if (dres) {
         const float4 q = *reinterpret_cast<const float4*>(dres + off);
@@ -185,13 +223,13 @@ norm_bwd_kernel(const float* __restrict__ dy, int64_t lddy, const float* __restr
       }
     }
   }
-  if (want_part && gw < nwaves) {
+  if (want_part && blockIdx.x < nblk) {
 #pragma unroll
     for (int k = 0; k < CM; ++k) {
-      const int c = k * 256 + lane * 4;
+      const int c = (k * RT + tid) * 4;
       if (c >= d) continue;
-      *reinterpret_cast<float4*>(part_w + (int64_t)gw * d + c) = aw[k];
-      if (LN && part_b) *reinterpret_cast<float4*>(part_b + (int64_t)gw * d + c) = ab[k];
+      *reinterpret_cast<float4*>(part_w + (int64_t)blockIdx.x * d + c) = aw[k];
+      if (LN && part_b) *reinterpret_cast<float4*>(part_b + (int64_t)blockIdx.x * d + c) = ab[k];
     }
   }
 }
@@ -200,9 +238,9 @@ template <int CM, bool LN>
 static void norm_bwd_go(int blocks, hipStream_t s, const float* dy, int64_t lddy, const float* x,
                         const float* w, const float* mean, const float* rstd, int rstride,
                         const float* dres, float* dx, void* dx_act, int adt, float* part_w,
-                        float* part_b, int T, int d, int rpw, int nw, int row_out0) {
+                        float* part_b, int T, int d, int rpb, int nb, int row_out0) {
   hipLaunchKernelGGL((norm_bwd_kernel<CM, LN>), dim3(blocks), dim3(RT), 0, s, dy, lddy, x, w,
-                     mean, rstd, rstride, dres, dx, dx_act, adt, part_w, part_b, T, d, rpw, nw,
+                     mean, rstd, rstride, dres, dx, dx_act, adt, part_w, part_b, T, d, rpb, nb,
                      row_out0);
 }
 
@@ -211,29 +249,24 @@ static hipError_t norm_bwd_launch(bool layernorm, const float* dy, int64_t lddy,
                                   int rstride, const float* dres, float* dx, void* dx_act,
                                   int adt, float* part_w, float* part_b, int T, int d,
                                   int row_out0, int* nblk_out, hipStream_t s) {
-  const int nw = norm_bwd_blocks(T);
-  const int rpw = (T + nw - 1) / nw;
-  if (nblk_out) *nblk_out = nw;
+  const int nb = norm_bwd_blocks(T);
+  const int rpb = (T + nb - 1) / nb;
+  if (nblk_out) *nblk_out = nb;
   if (d <= 0 || d % 4 || d > 8192) return hipErrorInvalidValue;
-  const int blocks = (nw + 3) / 4;
 #define ZL_NB(CM, LN)                                                                       \
-  norm_bwd_go<CM, LN>(blocks, s, dy, lddy, x, w, mean, rstd, rstride, dres, dx, dx_act, adt, \
-                      part_w, part_b, T, d, rpw, nw, row_out0)
-  const int cm = (d + 255) / 256;
+  norm_bwd_go<CM, LN>(nb, s, dy, lddy, x, w, mean, rstd, rstride, dres, dx, dx_act, adt,     \
+                      part_w, part_b, T, d, rpb, nb, row_out0)
+  const int cm = (d + 4 * RT - 1) / (4 * RT);
   if (layernorm) {
     if (cm <= 1) ZL_NB(1, true);
     else if (cm <= 2) ZL_NB(2, true);
     else if (cm <= 4) ZL_NB(4, true);
-    else if (cm <= 8) ZL_NB(8, true);
-    else if (cm <= 16) ZL_NB(16, true);
-    else ZL_NB(32, true);
+    else ZL_NB(8, true);
   } else {
     if (cm <= 1) ZL_NB(1, false);
     else if (cm <= 2) ZL_NB(2, false);
     else if (cm <= 4) ZL_NB(4, false);
-    else if (cm <= 8) ZL_NB(8, false);
-    else if (cm <= 16) ZL_NB(16, false);
-    else ZL_NB(32, false);
+    else ZL_NB(8, false);
   }
 #undef ZL_NB
   return hipGetLastError();
