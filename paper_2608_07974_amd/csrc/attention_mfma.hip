@@ -180,6 +180,21 @@ struct TileDma {
 // than 8 (probabilities stay <= 2^8, exact after the final division), so
 // the O rescale is skipped on most tiles.  Causal/length masks are applied
 // only on tiles that cross the diagonal or the end of the keys.
+// Causal work per workgroup grows (forward, dQ) or shrinks (dK/dV) with the
+// x index of the grid, and workgroups are dispatched with x varying
+// fastest.  Reading the linear dispatch index as (x slowest, then y, then
+// z) starts the longest blocks of every (batch, head group) first, which
+// keeps the last wave of the launch short (longest-first list scheduling).
+struct CausalOrder {
+  int x, y, z;
+};
+__device__ inline CausalOrder causal_order() {
+  const int nyz = gridDim.y * gridDim.z;
+  const int lin = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+  const int r = lin % nyz;
+  return CausalOrder{lin / nyz, r % (int)gridDim.y, r / (int)gridDim.y};
+}
+
 constexpr int FW_WAVES = 8;
 constexpr int FW_NT = FW_WAVES * 64;
 constexpr float RESCALE_TAU = 8.f;
@@ -190,8 +205,9 @@ __global__ void __launch_bounds__(FW_NT) attn_fwd_mfma(AttnDesc a) {
   constexpr int QB = QW * 32;          // queries per workgroup
   constexpr uint32_t TB = BT * HD * 2; // bytes of one K or V tile
   extern __shared__ __align__(16) unsigned char smem[];
-  const int qb = gridDim.x - 1 - blockIdx.x;  // longest causal rows first
-  const int hb = blockIdx.y * HPW, b = blockIdx.z;
+  const CausalOrder co = causal_order();
+  const int qb = gridDim.x - 1 - co.x;  // longest causal rows first
+  const int hb = co.y * HPW, b = co.z;
   const int kvh = hb / (a.Hq / a.Hkv);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int c = lane & 15, g = lane >> 4;
@@ -387,8 +403,9 @@ __global__ void __launch_bounds__(KV_NT) attn_dkv_mfma(AttnDesc a) {
   constexpr uint32_t STAT0 = 2 * STAGE;    // [stage][lse2 64 | delta 64] floats
   extern __shared__ __align__(16) unsigned char smem[];
   float* stat = reinterpret_cast<float*>(smem + STAT0);
-  const int kblk = blockIdx.x;             // early keys see the most queries: first
-  const int kvh = blockIdx.y, b = blockIdx.z;
+  const CausalOrder co = causal_order();
+  const int kblk = co.x;                   // early keys see the most queries: first
+  const int kvh = co.y, b = co.z;
   const int grp = a.Hq / a.Hkv;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int c = lane & 15, g = lane >> 4;
@@ -554,8 +571,9 @@ __global__ void __launch_bounds__(FW_NT) attn_dq_mfma(AttnDesc a) {
   constexpr int QB = QW * 32;
   constexpr uint32_t TB = BT * HD * 2;
   extern __shared__ __align__(16) unsigned char smem[];
-  const int qblk = gridDim.x - 1 - blockIdx.x;
-  const int hb = blockIdx.y * HPW, b = blockIdx.z;
+  const CausalOrder co = causal_order();
+  const int qblk = gridDim.x - 1 - co.x;
+  const int hb = co.y * HPW, b = co.z;
   const int kvh = hb / (a.Hq / a.Hkv);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int c = lane & 15, g = lane >> 4;
