@@ -172,14 +172,7 @@ struct TileDma {
   }
 };
 
-// ------------------------------------------------------------------ forward
-// Workgroup: 8 waves; HPW q-heads of one kv group (they share every K/V
-// tile) x 256 / HPW queries; each wave owns 32 queries of one head.
-// Online softmax in the log2 domain with a lazily moved reference maximum:
-// a row's reference only moves when the running maximum exceeds it by more
-// than 8 (probabilities stay <= 2^8, exact after the final division), so
-// the O rescale is skipped on most tiles.  Causal/length masks are applied
-// only on tiles that cross the diagonal or the end of the keys.
+// ------------------------------------------------------- workgroup order
 // Causal work per workgroup grows (forward, dQ) or shrinks (dK/dV) with the
 // x index of the grid, and workgroups are dispatched with x varying
 // fastest.  Reading the linear dispatch index as (x slowest, then y, then
@@ -195,6 +188,14 @@ __device__ inline CausalOrder causal_order() {
   return CausalOrder{lin / nyz, r % (int)gridDim.y, r / (int)gridDim.y};
 }
 
+// ------------------------------------------------------------------ forward
+// Workgroup: 8 waves; HPW q-heads of one kv group (they share every K/V
+// tile) x 256 / HPW queries; each wave owns 32 queries of one head.
+// Online softmax in the log2 domain with a lazily moved reference maximum:
+// a row's reference only moves when the running maximum exceeds it by more
+// than 8 (probabilities stay <= 2^8, exact after the final division), so
+// the O rescale is skipped on most tiles.  Causal/length masks are applied
+// only on tiles that cross the diagonal or the end of the keys.
 constexpr int FW_WAVES = 8;
 constexpr int FW_NT = FW_WAVES * 64;
 constexpr float RESCALE_TAU = 8.f;
@@ -264,22 +265,26 @@ __global__ void __launch_bounds__(FW_NT) attn_fwd_mfma(AttnDesc a) {
     const bf16_t* kt = reinterpret_cast<const bf16_t*>(smem + (t & 1) * 2 * TB);
     const bf16_t* vt = kt + BT * HD;
     // S^T: 8 independent accumulators per k-step; the K fragments of the
-    // next k-step are read while the current step's MFMAs run
+    // k-step two ahead are read while the current step's MFMAs run
+    constexpr int NK = HD / 32, KA = NK < 3 ? NK : 3;
     f32x4_t s[2][4];
-    bf16x8_t kb[2][4];
+    bf16x8_t kb[KA][4];
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) {
       s[0][blk] = f32x4_t{0.f, 0.f, 0.f, 0.f};
       s[1][blk] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-      kb[0][blk] = frag_row<HD>(kt, blk * 16 + c, g);
     }
 #pragma unroll
-    for (int kk = 0; kk < HD / 32; ++kk) {
-      const int cur = kk & 1;
-      if (kk + 1 < HD / 32) {
+    for (int kk = 0; kk < KA - 1; ++kk)
+#pragma unroll
+      for (int blk = 0; blk < 4; ++blk) kb[kk][blk] = frag_row<HD>(kt, blk * 16 + c, g + 4 * kk);
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) {
+      const int cur = kk % KA;
+      if (kk + KA - 1 < NK) {
 #pragma unroll
         for (int blk = 0; blk < 4; ++blk)
-          kb[cur ^ 1][blk] = frag_row<HD>(kt, blk * 16 + c, g + 4 * (kk + 1));
+          kb[(kk + KA - 1) % KA][blk] = frag_row<HD>(kt, blk * 16 + c, g + 4 * (kk + KA - 1));
       }
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -288,17 +293,25 @@ __global__ void __launch_bounds__(FW_NT) attn_fwd_mfma(AttnDesc a) {
         s[1][blk] = mfma16(kb[cur][blk], qf[1][kk], s[1][blk]);
       }
     }
+    // V^T fragments of the O update: a ring of VA reads in flight, the first
+    // VA issued before the softmax so that it hides their latency
+    constexpr int NV = 2 * (HD / 16), VA = 4;
+    bf16x8_t vb[VA];
+#pragma unroll
+    for (int i = 0; i < VA; ++i) vb[i] = frag_col<HD>(vt, 32 * (i & 1), g, 16 * (i >> 1), c);
     // some key of the tile lies after some query of the wave, or past kend
     const bool masked = k0 + BT - 1 > qw0 || k0 + BT > kend;
     bf16x8_t pf[2][2];
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
+      // raw scores: the maximum is taken before scaling (cs > 0) and the
+      // scale is folded into the exponent's FMA
       float x[4][4];
       float tmax = -INFINITY;
 #pragma unroll
       for (int blk = 0; blk < 4; ++blk)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) x[blk][r] = s[j][blk][r] * cs;
+        for (int r = 0; r < 4; ++r) x[blk][r] = s[j][blk][r];
       if (masked) {
 #pragma unroll
         for (int blk = 0; blk < 4; ++blk)
@@ -313,6 +326,7 @@ __global__ void __launch_bounds__(FW_NT) attn_fwd_mfma(AttnDesc a) {
         tmax = fmaxf(tmax, fmaxf(fmaxf(x[blk][0], x[blk][1]), fmaxf(x[blk][2], x[blk][3])));
       tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
       tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+      tmax *= cs;
       const bool move = tmax > m[j] + RESCALE_TAU;
       if (__any(move)) {
         const float mnew = move ? tmax : m[j];
@@ -322,28 +336,25 @@ __global__ void __launch_bounds__(FW_NT) attn_fwd_mfma(AttnDesc a) {
 #pragma unroll
         for (int db = 0; db < HD / 16; ++db) o[j][db] *= alpha;
       }
-      const float ms = m[j] == -INFINITY ? 0.f : m[j];
+      const float nms = m[j] == -INFINITY ? 0.f : -m[j];
       float psum = 0.f;
 #pragma unroll
       for (int blk = 0; blk < 4; ++blk)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float p = __builtin_amdgcn_exp2f(x[blk][r] - ms);
+          const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(x[blk][r], cs, nms));
           psum += p;
           pf[j][blk >> 1][(blk & 1) * 4 + r] = (__bf16)p;
         }
       lsum[j] += psum;
     }
-    bf16x8_t vb[2];
-    vb[0] = frag_col<HD>(vt, 0, g, 0, c);
 #pragma unroll
-    for (int i = 0; i < 2 * (HD / 16); ++i) {  // i = 2 db + kk
-      const int db = i >> 1, kk = i & 1, cur = i & 1;
-      if (i + 1 < 2 * (HD / 16))
-        vb[cur ^ 1] = frag_col<HD>(vt, 32 * ((i + 1) & 1), g, 16 * ((i + 1) >> 1), c);
+    for (int i = 0; i < NV; ++i) {  // i = 2 db + kk
+      const int db = i >> 1, kk = i & 1, cur = i % VA;
       __builtin_amdgcn_sched_barrier(0);
       o[0][db] = mfma16(vb[cur], pf[0][kk], o[0][db]);
       o[1][db] = mfma16(vb[cur], pf[1][kk], o[1][db]);
+      if (i + VA < NV) vb[cur] = frag_col<HD>(vt, 32 * ((i + VA) & 1), g, 16 * ((i + VA) >> 1), c);
     }
   }
   dma_wait();
@@ -678,16 +689,18 @@ __global__ void __launch_bounds__(FW_NT) attn_dq_mfma(AttnDesc a) {
           dsk[j][blk >> 1][(blk & 1) * 4 + r] = (__bf16)(p * (dpt[j][r] - dl[j]));
         }
     }
-    bf16x8_t kc[2];
-    kc[0] = frag_col<HD>(kt, 0, g, 0, c);
+    // K^T fragments of the dQ update: a ring of KA reads in flight
+    constexpr int NC = 2 * (HD / 16), KA = 4;
+    bf16x8_t kc[KA];
 #pragma unroll
-    for (int i = 0; i < 2 * (HD / 16); ++i) {  // i = 2 db + kk
-      const int db = i >> 1, kk = i & 1, cur = i & 1;
-      if (i + 1 < 2 * (HD / 16))
-        kc[cur ^ 1] = frag_col<HD>(kt, 32 * ((i + 1) & 1), g, 16 * ((i + 1) >> 1), c);
+    for (int i = 0; i < KA; ++i) kc[i] = frag_col<HD>(kt, 32 * (i & 1), g, 16 * (i >> 1), c);
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {  // i = 2 db + kk
+      const int db = i >> 1, kk = i & 1, cur = i % KA;
       __builtin_amdgcn_sched_barrier(0);
       dq[0][db] = mfma16(dsk[0][kk], kc[cur], dq[0][db]);
       dq[1][db] = mfma16(dsk[1][kk], kc[cur], dq[1][db]);
+      if (i + KA < NC) kc[cur] = frag_col<HD>(kt, 32 * ((i + KA) & 1), g, 16 * ((i + KA) >> 1), c);
     }
   }
   dma_wait();
