@@ -43,11 +43,15 @@ zl_status zl_inspect(const zl_chunk* chunk, const char* name, int layer, zl_view
  * A[k*lda + m] and likewise for B, A2 (lda2) and B2 (ldb2) in the layouts of
  * A and B; the GEMM kernel used for every linear of the chunk (Eq. (1)), the
  * second segment carrying the LoRA term (K2 = 0: none, A2 and B2 unused),
- * and the head (Eq. (2)).  dtype ZL_BF16 (MFMA) or ZL_F32 (SIMT). */
+ * and the head (Eq. (2)).  dtype ZL_BF16 (MFMA) or ZL_F32 (SIMT).
+ * workspace (device, workspace_elems floats, or NULL): lets a bf16 GEMM
+ * whose output has too few tiles to fill the GPU split K into fp32 partials
+ * there, summed in a fixed order (the chunk's own GEMMs use a region of its
+ * workspace for this); its contents are scratch. */
 zl_status zl_kernel_gemm(int M, int N, int K, const void* A, int64_t lda, int a_kmajor,
                          const void* B, int64_t ldb, int b_kmajor, int K2, const void* A2,
                          int64_t lda2, const void* B2, int64_t ldb2, float* C, int64_t ldc,
-                         int dtype, void* stream);
+                         float* workspace, size_t workspace_elems, int dtype, void* stream);
 
 /* Causal GQA attention forward (backward = 0: o, lse) or backward
  * (backward = 1: dq, dk, dv and delta from q, k, v, o, lse, dout), the

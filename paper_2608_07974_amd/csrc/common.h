@@ -62,6 +62,14 @@ struct GemmDesc {
   int64_t lda2;
   const void* B2;
   int64_t ldb2;
+  // Split-K workspace (bf16 direct-to-LDS path): with part != nullptr a GEMM
+  // whose output has too few tiles to fill the chip may split K over the
+  // grid's z dimension into fp32 partials [splits][M][N] (at most part_elems
+  // floats), summed in split order by a second kernel that applies the
+  // epilogue.  ksplit (K elements per split) is set by launch_gemm.
+  float* part;
+  size_t part_elems;
+  int ksplit;
 };
 
 enum EpiKind {
@@ -108,6 +116,7 @@ struct EpiArgs {
   const int32_t* pos;   // EPI_ROPE: position of row m
   const float2* rope;   // EPI_ROPE: (cos, sin) table [max_pos, hd/2]
   int max_pos, hd, n_rot;
+  int64_t zstride;      // split-K partials: raw fp32 store to out + z * zstride (set by launch_gemm)
 };
 
 // *kname (optional) receives a static name of the kernel instantiation used.

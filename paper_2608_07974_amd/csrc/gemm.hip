@@ -10,6 +10,8 @@
 // fp32: a plain LDS-tiled SIMT kernel (the fp32 configuration is small).
 #include <stdio.h>
 
+#include <cstring>
+
 #include "common.h"
 
 #ifndef GEMM_IL  // main-loop schedule of the direct-to-LDS kernel
@@ -284,7 +286,23 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[BM / WM / 32][B
     // EW consecutive columns per lane: a row of TN columns takes TN / EW lanes
     constexpr int QPR = TN / EW;
     static_assert(TN % EW == 0, "wave tile width must hold whole column groups");
-    if (e.kind == EPI_ROPE) {
+    if (e.zstride) {
+      // split-K partial: raw fp32 accumulators of split z (no epilogue)
+      float* base = static_cast<float*>(e.out) + (size_t)blockIdx.z * e.zstride;
+      for (int t = lane; t < 32 * QPR; t += 64) {
+        const int row = t / QPR, col = (t % QPR) * EW;
+        const int m = mb + row, n = nb + col;
+        if (m >= g.M) continue;
+        float* o = base + (size_t)m * e.ldo + n;
+        if (n + EW <= g.N && (e.ldo & 3) == 0) {
+#pragma unroll
+          for (int k = 0; k < EW; k += 4)
+            *reinterpret_cast<float4*>(o + k) = *reinterpret_cast<const float4*>(&ep[row * LDW + col + k]);
+        } else {
+          for (int k = 0; k < EW && n + k < g.N; ++k) o[k] = ep[row * LDW + col + k];
+        }
+      }
+    } else if (e.kind == EPI_ROPE) {
       // wave tiles are head-aligned (nb % hd == 0, TN % hd == 0) and half =
       // hd / 2 is a multiple of EW, so the partner columns j +- hd/2 of a
       // column group are again EW consecutive columns of the staged row
@@ -802,8 +820,12 @@ gemm_dma_kernel(GemmDesc g, EpiArgs e) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int wm = wave / WN, wn = wave % WN;
 
-  const bf16_t* A = reinterpret_cast<const bf16_t*>(g.A);
-  const bf16_t* B = reinterpret_cast<const bf16_t*>(g.B);
+  // split K: this block's range [kbeg, kbeg + ksplit) of the reduction
+  const int kz = blockIdx.z, kbeg = kz * g.ksplit;
+  const int klen = min(g.K - kbeg, g.ksplit);
+  const int ka = min(g.ka - kbeg, g.ksplit), kb = min(g.kb - kbeg, g.ksplit);
+  const bf16_t* A = reinterpret_cast<const bf16_t*>(g.A) + (AK ? kbeg : (int64_t)kbeg * g.lda);
+  const bf16_t* B = reinterpret_cast<const bf16_t*>(g.B) + (BKM ? kbeg : (int64_t)kbeg * g.ldb);
   const i32x4_t ra = buffer_rsrc(A + (AK ? (int64_t)m0 * g.lda : (int64_t)m0));
   const i32x4_t rb = buffer_rsrc(B + (BKM ? (int64_t)n0 * g.ldb : (int64_t)n0));
   TA da;
@@ -824,15 +846,15 @@ gemm_dma_kernel(GemmDesc g, EpiArgs e) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>(smem);
-  const int nk = (g.K + BK - 1) / BK;
+  const int nk = (klen + BK - 1) / BK;
   // prologue: tiles 0 .. NST-2, or 0 .. NST-1 when each tile's copy is
   // issued as soon as its stage is released (tiles past K are zero-filled,
   // never used)
   constexpr int PRO = GEMM_IL == 2 ? NST : NST - 1;
 #pragma unroll
   for (int t = 0; t < PRO; ++t) {
-    da.issue(lds0 + t * STAGE, wave, t * BK, g.ka, ra);
-    db.issue(lds0 + t * STAGE + ABYTES, wave, t * BK, g.kb, rb);
+    da.issue(lds0 + t * STAGE, wave, t * BK, ka, ra);
+    db.issue(lds0 + t * STAGE + ABYTES, wave, t * BK, kb, rb);
   }
   wait_vmcnt<(PRO - 1) * PER_TILE>();
   __syncthreads();
@@ -853,8 +875,8 @@ gemm_dma_kernel(GemmDesc g, EpiArgs e) {
   for (int kt = 0; kt < nk; ++kt) {
     const uint32_t dst = lds0 + wr * STAGE;
     const int k0n = (kt + NST - 1) * BK;
-    if constexpr (RA) da.load(rga, k0n, g.ka, ra);
-    if constexpr (RB) db.load(rgb, k0n, g.kb, rb);
+    if constexpr (RA) da.load(rga, k0n, ka, ra);
+    if constexpr (RB) db.load(rgb, k0n, kb, rb);
     const int rn = rd + 1 == NST ? 0 : rd + 1;
     const bf16_t* as = reinterpret_cast<const bf16_t*>(smem + rd * STAGE);
     const bf16_t* an = reinterpret_cast<const bf16_t*>(smem + rn * STAGE);
@@ -898,8 +920,8 @@ gemm_dma_kernel(GemmDesc g, EpiArgs e) {
 #pragma unroll
         for (int u = 0; u < TOT; ++u) {
           if (u < lo || u >= hi || (u - lo) * NMF / span != t) continue;
-          if (u < TA::ITEMS) da.issue_one(u, ddst, wave, dk0, g.ka, ra);
-          else db.issue_one(u - TA::ITEMS, ddst + ABYTES, wave, dk0, g.kb, rb);
+          if (u < TA::ITEMS) da.issue_one(u, ddst, wave, dk0, ka, ra);
+          else db.issue_one(u - TA::ITEMS, ddst + ABYTES, wave, dk0, kb, rb);
         }
         __builtin_amdgcn_sched_barrier(0);
       }
@@ -932,8 +954,8 @@ gemm_dma_kernel(GemmDesc g, EpiArgs e) {
         for (int t = 0; t < TOT; ++t) {
           if (t < lo || t >= hi) continue;
           const int ta = RA ? 0 : TA::ITEMS;
-          if (t < ta) da.issue_one(t, dst, wave, k0n, g.ka, ra);
-          else db.issue_one(t - ta, dst + ABYTES, wave, k0n, g.kb, rb);
+          if (t < ta) da.issue_one(t, dst, wave, k0n, ka, ra);
+          else db.issue_one(t - ta, dst + ABYTES, wave, k0n, kb, rb);
         }
       }
       __builtin_amdgcn_sched_barrier(0);
@@ -950,9 +972,10 @@ gemm_dma_kernel(GemmDesc g, EpiArgs e) {
   }
   dma_wait();  // the zero-fill copies past K must land before LDS is reused
   __syncthreads();
-  if (g.K2 > 0) {
+  if (g.K2 > 0 && kz == 0) {
     // second K segment (same layouts): one BK-deep tile at a time through
-    // stage 0, copied and multiplied without overlap (K2 is a few tiles)
+    // stage 0, copied and multiplied without overlap (K2 is a few tiles);
+    // with split K the first split carries it
     const i32x4_t ra2 = buffer_rsrc(reinterpret_cast<const bf16_t*>(g.A2) +
                                     (AK ? (int64_t)m0 * g.lda2 : (int64_t)m0));
     const i32x4_t rb2 = buffer_rsrc(reinterpret_cast<const bf16_t*>(g.B2) +
@@ -1092,8 +1115,27 @@ static const char* layout_tag(bool ak, bool bk) {
 #endif
 
 
+// Split-K reduction: C = sum over splits z = 0, 1, .. (in that order) of the
+// fp32 partials, then the epilogue per element.
+__global__ void __launch_bounds__(256) splitk_reduce_kernel(const float* __restrict__ part, int nz,
+                                                            int M, int N, EpiArgs e) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t mn = (int64_t)M * N;
+  if (i >= mn) return;
+  float acc = 0.f;
+  for (int z = 0; z < nz; ++z) acc += part[z * mn + i];
+  epilogue(e, M, N, (int)(i / N), (int)(i % N), acc);
+}
+
+// Epilogues applied per element by the split-K reduction (the others need
+// whole rows or column pairs of the staged tile).
+static bool splitk_kind_ok(EpiKind k) {
+  return k == EPI_STORE || k == EPI_RESID || k == EPI_GELU || k == EPI_GRAD ||
+         k == EPI_SWIGLU_BWD || k == EPI_GELU_BWD;
+}
+
 template <int BM, int BN, int WM, int WN, int BK, int NST, bool AK, bool BKM>
-static hipError_t run_dma(const GemmDesc& g, const EpiArgs& e, hipStream_t s) {
+static hipError_t run_dma(const GemmDesc& g, const EpiArgs& e, hipStream_t s, int nz = 1) {
   auto kern = gemm_dma_kernel<BM, BN, WM, WN, BK, NST, GEMM_DS, AK, BKM, GEMM_RA, GEMM_RB>;
   const size_t lds_main = (size_t)NST * (BM + BN) * BK * sizeof(bf16_t);
   const size_t lds_epi = (size_t)WM * WN * 32 * (BN / WN + 4) * sizeof(float);
@@ -1107,7 +1149,47 @@ static hipError_t run_dma(const GemmDesc& g, const EpiArgs& e, hipStream_t s) {
     attr_set = true;
   }
   const int nb = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
-  hipLaunchKernelGGL(kern, dim3(nb), dim3(WM * WN * 64), lds, s, g, e);
+  hipLaunchKernelGGL(kern, dim3(nb, 1, nz), dim3(WM * WN * 64), lds, s, g, e);
+  return hipGetLastError();
+}
+
+// Splits of K for a GEMM of `tiles` output tiles: none from 3/4 of a wave
+// of blocks (one per CU) up, else enough to give the chip about 256 blocks,
+// each split at least 8 k-tiles deep, the partials within the workspace.
+// Returns 1 for no split.
+static int splitk_count(const GemmDesc& g, const EpiArgs& e, long tiles, int bk) {
+  if (!g.part || !splitk_kind_ok(e.kind) || tiles > 192) return 1;
+  int nz = (int)((256 + tiles - 1) / tiles);
+  const int by_k = g.K / (8 * bk);
+  if (nz > by_k) nz = by_k;
+  const size_t mn = (size_t)g.M * g.N;
+  if (mn && (size_t)nz * mn > g.part_elems) nz = (int)(g.part_elems / mn);
+  return nz >= 2 ? nz : 1;
+}
+
+template <int BM, int BN, int WM, int WN, int BK, int NST, bool AK, bool BKM>
+static hipError_t run_dma_split(const GemmDesc& g, const EpiArgs& e, hipStream_t s) {
+  const long tiles = (long)((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
+  int nz = splitk_count(g, e, tiles, BK);
+  GemmDesc gs = g;
+  gs.ksplit = g.K;
+  if (nz == 1) return run_dma<BM, BN, WM, WN, BK, NST, AK, BKM>(gs, e, s, 1);
+  // K per split, a multiple of the k-tile, so every split but the last is whole
+  gs.ksplit = ((g.K + nz - 1) / nz + BK - 1) / BK * BK;
+  nz = (g.K + gs.ksplit - 1) / gs.ksplit;
+  EpiArgs ep;
+  memset(&ep, 0, sizeof(ep));
+  ep.kind = EPI_STORE;
+  ep.out = g.part;
+  ep.ldo = g.N;
+  ep.out_dtype = F32;
+  ep.scale = 1.f;
+  ep.zstride = (int64_t)g.M * g.N;
+  hipError_t err = run_dma<BM, BN, WM, WN, BK, NST, AK, BKM>(gs, ep, s, nz);
+  if (err != hipSuccess) return err;
+  const int64_t mn = (int64_t)g.M * g.N;
+  hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((mn + 255) / 256)), dim3(256), 0, s,
+                     (const float*)g.part, nz, g.M, g.N, e);
   return hipGetLastError();
 }
 
@@ -1148,8 +1230,8 @@ static hipError_t run_layout(const GemmDesc& g, const EpiArgs& e, int dtype, hip
       // an M-contiguous A (weight gradients) runs best with shallower,
       // deeper-pipelined k tiles
       constexpr int BKL = AK ? GEMM_BK : GEMM_BK_MN, NSTL = AK ? GEMM_NST : GEMM_NST_MN;
-      if (large) { err = run_dma<256, 256, GEMM_WM, GEMM_WN, BKL, NSTL, AK, BKM>(g, e, s); which = 3; }
-      else { err = run_dma<128, 128, 2, 2, BKL, NSTL, AK, BKM>(g, e, s); which = 4; }
+      if (large) { err = run_dma_split<256, 256, GEMM_WM, GEMM_WN, BKL, NSTL, AK, BKM>(g, e, s); which = 3; }
+      else { err = run_dma_split<128, 128, 2, 2, BKL, NSTL, AK, BKM>(g, e, s); which = 4; }
     } else if (large) {
       if constexpr (AK && BKM) err = run_mfma<256, 256, 4, 2, AK, BKM>(g, e, s);
       else err = run_mfma<256, 256, 2, 2, AK, BKM>(g, e, s);

@@ -276,6 +276,7 @@ struct Plan {
   std::vector<size_t> LXQ, LXO, LXU, LXD;
   size_t LBD, LE;
   size_t part_elems;
+  size_t SPK, spk_elems;  // split-K partials of the GEMMs
 };
 
 void build_plan(const zl_config& c, Plan& p) {
@@ -358,6 +359,11 @@ void build_plan(const zl_config& c, Plan& p) {
   const size_t bd_q = (size_t)m.nqkv * m.nqa, bd_u = (size_t)m.nup * m.nua;
   p.LBD = take(lr && m.llama ? (bd_q > bd_u ? bd_q : bd_u) * act : 0);
   p.LE = take(T * m.nqa * act);
+  // split-K partials (bf16 GEMMs whose outputs hold too few tiles to fill
+  // the chip: the LoRA factor GEMMs); launch_gemm splits less if they do
+  // not fit
+  p.spk_elems = act == 2 ? (size_t)4 << 20 : 0;
+  p.SPK = take(p.spk_elems * 4);
   p.total = off;
 }
 
@@ -425,6 +431,7 @@ static GemmDesc gdesc(int M, int N, int K, const void* A, int64_t lda, bool ak, 
   g.A = A; g.lda = lda; g.a_kmajor = ak;
   g.B = B; g.ldb = ldb; g.b_kmajor = bk;
   g.K2 = 0; g.A2 = nullptr; g.lda2 = 0; g.B2 = nullptr; g.ldb2 = 0;
+  g.part = nullptr; g.part_elems = 0; g.ksplit = K;
   return g;
 }
 
@@ -440,7 +447,10 @@ static hipError_t run_gemm(zl_chunk* c, hipStream_t s, const GemmDesc& g, const 
                            double k_alg = -1) {
   const int pi = c->prof_start(s);
   const char* kn = "gemm";
-  hipError_t err = launch_gemm(g, e, c->act, s, &kn);
+  GemmDesc gs = g;
+  gs.part = c->plan.spk_elems ? c->at<float>(c->plan.SPK) : nullptr;
+  gs.part_elems = c->plan.spk_elems;
+  hipError_t err = launch_gemm(gs, e, c->act, s, &kn);
   c->prof_stop(pi, s, kn, 2.0 * g.M * g.N * ((k_alg < 0 ? g.K : k_alg) + g.K2), 0.0);
   return err;
 }
@@ -1219,7 +1229,7 @@ zl_status zl_device_info(int device, int* cu_count, int* clock_khz, char* arch, 
 zl_status zl_kernel_gemm(int M, int N, int K, const void* A, int64_t lda, int a_kmajor,
                          const void* B, int64_t ldb, int b_kmajor, int K2, const void* A2,
                          int64_t lda2, const void* B2, int64_t ldb2, float* C, int64_t ldc,
-                         int dtype, void* stream) {
+                         float* workspace, size_t workspace_elems, int dtype, void* stream) {
   if (M < 0 || N < 0 || K < 0 || K2 < 0 || !A || !B || !C || (K2 > 0 && (!A2 || !B2)))
     return fail(ZL_ERR_INVALID_ARG, "bad gemm args");
   if (dtype != ZL_F32 && dtype != ZL_BF16) return fail(ZL_ERR_INVALID_ARG, "bad dtype");
@@ -1233,6 +1243,11 @@ zl_status zl_kernel_gemm(int M, int N, int K, const void* A, int64_t lda, int a_
   }
   GemmDesc g = gdesc(M, N, K, A, lda, a_kmajor != 0, B, ldb, b_kmajor != 0);
   if (K2 > 0) { g.K2 = K2; g.A2 = A2; g.lda2 = lda2; g.B2 = B2; g.ldb2 = ldb2; }
+  if (workspace && workspace_elems) {
+    if ((uintptr_t)workspace % 16) return fail(ZL_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
+    g.part = workspace;
+    g.part_elems = workspace_elems;
+  }
   EpiArgs e = epi(EPI_STORE, C, ldc, F32);
   ZL_HIP(launch_gemm(g, e, dtype == ZL_BF16 ? BF16 : F32, S_(stream)));
   return ZL_OK;

@@ -114,7 +114,8 @@ def load(path=None):
         "zl_status_string": [c],
         "zl_last_error": [],
         "zl_inspect": [vp, ctypes.c_char_p, c, P(zl_view)],
-        "zl_kernel_gemm": [c, c, c, vp, i64, c, vp, i64, c, c, vp, i64, vp, i64, vp, i64, c, vp],
+        "zl_kernel_gemm": [c, c, c, vp, i64, c, vp, i64, c, c, vp, i64, vp, i64, vp, i64, vp, sz, c,
+                           vp],
         "zl_kernel_attention": [c, c, c, c, c, vp, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, vp,
                                 c, c, vp],
         "zl_profile_begin": [vp, c],
@@ -253,9 +254,10 @@ def zl_inspect(h, name, layer=0):
 
 
 def zl_kernel_gemm(M, N, K, A, lda, a_kmajor, B, ldb, b_kmajor, C, ldc, dtype, stream=0,
-                   K2=0, A2=None, lda2=0, B2=None, ldb2=0):
+                   K2=0, A2=None, lda2=0, B2=None, ldb2=0, workspace=None, workspace_elems=0):
     _check(load().zl_kernel_gemm(M, N, K, A, lda, int(a_kmajor), B, ldb, int(b_kmajor), K2, A2,
-                                 lda2, B2, ldb2, C, ldc, dtype, stream), "zl_kernel_gemm")
+                                 lda2, B2, ldb2, C, ldc, workspace, workspace_elems, dtype, stream),
+           "zl_kernel_gemm")
 
 
 def zl_kernel_attention(B, S, Hq, Hkv, hd, q, k, v, ld_qkv, seq_lens, o, lse, dout, dq, dk, dv,

@@ -1,5 +1,5 @@
 """Single-kernel parity on the GPU through the C ABI (zl_inspect.h):
-the GEMM in its three operand layouts and causal GQA attention, against
+the GEMM in its operand layouts (with the LoRA segment and split K) and causal GQA attention, against
 fp64 references computed on the CPU from the same (bf16-rounded) inputs."""
 import numpy as np
 import pytest
@@ -99,6 +99,44 @@ def test_gemm_second_segment(dtype, layout, M, N, K, K2):
     got = C.cpu().double().numpy()
     assert np.all(np.isfinite(got))
     assert rel_err(got, ref) < 2e-6
+
+
+@pytest.mark.parametrize("a_k,b_k", [(True, True), (True, False), (False, False), (False, True)])
+@pytest.mark.parametrize("M,N,K,K2", [(16, 4104, 16384, 0), (4096, 16, 16384, 16), (200, 136, 3000, 24),
+                                      (48, 1000, 1024, 0)])
+def test_gemm_split_k(a_k, b_k, M, N, K, K2):
+    """Outputs of too few tiles to fill the GPU (the LoRA factor GEMMs) split
+    K into fp32 partials in the caller's workspace: same result as one pass
+    within fp32 summation error, identical on a repeat (fixed summation
+    order), and still correct when the workspace only holds two partials."""
+    zl = _zl()
+    rng = np.random.default_rng(M + N + K + K2 + 2 * a_k + b_k)
+
+    def op(rows, k, kmaj):
+        x = rng.standard_normal((rows, k) if kmaj else (k, rows)).astype(np.float32)
+        return torch.tensor(x, device=_dev()).to(torch.bfloat16)
+    At, Bt = op(M, K, a_k), op(N, K, b_k)
+    A2, B2 = (op(M, K2, a_k), op(N, K2, b_k)) if K2 else (None, None)
+    seg = dict(K2=K2, A2=A2.data_ptr(), lda2=A2.shape[1], B2=B2.data_ptr(), ldb2=B2.shape[1]) if K2 else {}
+
+    def run(ws_elems):
+        C = torch.full((M, N), float("nan"), dtype=torch.float32, device=_dev())
+        ws = torch.full((max(ws_elems, 1),), float("nan"), dtype=torch.float32, device=_dev())
+        torch.cuda.synchronize()
+        zl.zl_kernel_gemm(M, N, K, At.data_ptr(), At.shape[1], a_k, Bt.data_ptr(), Bt.shape[1], b_k,
+                          C.data_ptr(), N, zl.ZL_BF16, _stream(), workspace=ws.data_ptr() if ws_elems else None,
+                          workspace_elems=ws_elems, **seg)
+        torch.cuda.synchronize()
+        return C.cpu().double().numpy()
+    ref = _gemm_ref(At, Bt, a_k, b_k) + (_gemm_ref(A2, B2, a_k, b_k) if K2 else 0.0)
+    one = run(0)
+    split = run(64 * M * N)
+    again = run(64 * M * N)
+    two = run(2 * M * N)
+    for got in (one, split, two):
+        assert np.all(np.isfinite(got))
+        assert rel_err(got, ref) < 2e-6
+    assert np.array_equal(split, again)
 
 
 def test_gemm_register_staged_path_with_second_segment():
