@@ -237,9 +237,8 @@ struct SoftPart { float m, s, e; };
 // Grouped (GROUP_M row panels) order, then remapped so that the blocks the
 // dispatcher places on one XCD (round-robin over 8) take a contiguous range
 // of the grouped order and share A/B panels in that XCD's L2.
-__device__ inline void tile_coords(int nbm, int nbn, int& tm, int& tn) {
+__device__ inline void tile_coords(int b, int nbm, int nbn, int& tm, int& tn) {
   const int nb = nbm * nbn;
-  int b = blockIdx.x;
   if (nb >= 64) {
     const int per = nb / 8, rem = nb % 8;
     const int x = b % 8, idx = b / 8;
@@ -530,7 +529,7 @@ gemm_mfma_kernel(GemmDesc g, EpiArgs e) {
 
   const int nbm = (g.M + BM - 1) / BM, nbn = (g.N + BN - 1) / BN;
   int tm, tn;
-  tile_coords(nbm, nbn, tm, tn);
+  tile_coords(blockIdx.x, nbm, nbn, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int wm = wave / WN, wn = wave % WN;
@@ -795,10 +794,11 @@ __device__ inline void wait_vmcnt() {
 }
 
 // NST-stage pipeline: the tile NST - 1 steps ahead is in flight while the
-// current one is multiplied; one barrier per BK-deep tile.
+// current one is multiplied; one barrier per BK-deep tile.  bl is the
+// block's index among the tiles of its problem.
 template <int BM, int BN, int WM, int WN, int BK, int NST, int DS, bool AK, bool BKM, bool RA, bool RB>
-__global__ void __launch_bounds__(WM * WN * 64)
-gemm_dma_kernel(GemmDesc g, EpiArgs e) {
+__device__ __forceinline__ void gemm_dma_body(const GemmDesc& g, const EpiArgs& e, const int bl,
+                                              unsigned char* smem) {
   constexpr int NT = WM * WN * 64;
   constexpr int TM = BM / WM, TN = BN / WN;
   constexpr int FM = TM / 32, FN = TN / 32;
@@ -811,11 +811,10 @@ gemm_dma_kernel(GemmDesc g, EpiArgs e) {
   static_assert(!(RA || RB) || NST == 2, "register staging uses two stages");
   static_assert(DS >= 1 && DS < NS, "the tile copy is spread over slices before the last");
   static_assert(NS % 2 == 0, "slice parity must repeat per tile");
-  extern __shared__ __align__(16) unsigned char smem[];
 
   const int nbm = (g.M + BM - 1) / BM, nbn = (g.N + BN - 1) / BN;
   int tm, tn;
-  tile_coords(nbm, nbn, tm, tn);
+  tile_coords(bl, nbm, nbn, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int wm = wave / WN, wn = wave % WN;
@@ -1006,6 +1005,20 @@ gemm_dma_kernel(GemmDesc g, EpiArgs e) {
   store_tile<BM, BN, WM, WN>(acc, smem, g, e, m0, n0, wave, lane);
 }
 
+// One launch, one or two problems of the same layout: blocks below nb1 take
+// (g, e), the rest (g2, e2) (two independent weight gradients share a launch
+// so the last wave of one is filled by the other).  The problem is uniform
+// per block; each branch inlines the body with its own descriptors.
+template <int BM, int BN, int WM, int WN, int BK, int NST, int DS, bool AK, bool BKM, bool RA, bool RB>
+__global__ void __launch_bounds__(WM * WN * 64)
+gemm_dma_kernel(GemmDesc g, EpiArgs e, GemmDesc g2, EpiArgs e2, int nb1) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  if ((int)blockIdx.x < nb1)
+    gemm_dma_body<BM, BN, WM, WN, BK, NST, DS, AK, BKM, RA, RB>(g, e, blockIdx.x, smem);
+  else
+    gemm_dma_body<BM, BN, WM, WN, BK, NST, DS, AK, BKM, RA, RB>(g2, e2, blockIdx.x - nb1, smem);
+}
+
 // ------------------------------------------------------------ SIMT (fp32)
 template <bool AK, bool BKM>
 __global__ void __launch_bounds__(256) gemm_simt_kernel(GemmDesc g, EpiArgs e) {
@@ -1135,7 +1148,8 @@ static bool splitk_kind_ok(EpiKind k) {
 }
 
 template <int BM, int BN, int WM, int WN, int BK, int NST, bool AK, bool BKM>
-static hipError_t run_dma(const GemmDesc& g, const EpiArgs& e, hipStream_t s, int nz = 1) {
+static hipError_t run_dma(const GemmDesc& g, const EpiArgs& e, hipStream_t s, int nz = 1,
+                          const GemmDesc* g2 = nullptr, const EpiArgs* e2 = nullptr) {
   auto kern = gemm_dma_kernel<BM, BN, WM, WN, BK, NST, GEMM_DS, AK, BKM, GEMM_RA, GEMM_RB>;
   const size_t lds_main = (size_t)NST * (BM + BN) * BK * sizeof(bf16_t);
   const size_t lds_epi = (size_t)WM * WN * 32 * (BN / WN + 4) * sizeof(float);
@@ -1149,7 +1163,9 @@ static hipError_t run_dma(const GemmDesc& g, const EpiArgs& e, hipStream_t s, in
     attr_set = true;
   }
   const int nb = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
-  hipLaunchKernelGGL(kern, dim3(nb, 1, nz), dim3(WM * WN * 64), lds, s, g, e);
+  const int nb2 = g2 ? ((g2->M + BM - 1) / BM) * ((g2->N + BN - 1) / BN) : 0;
+  hipLaunchKernelGGL(kern, dim3(nb + nb2, 1, nz), dim3(WM * WN * 64), lds, s, g, e, g2 ? *g2 : g,
+                     e2 ? *e2 : e, nb);
   return hipGetLastError();
 }
 
@@ -1251,6 +1267,53 @@ static hipError_t run_layout(const GemmDesc& g, const EpiArgs& e, int dtype, hip
     *kname = names[which];
   }
   return err;
+}
+
+// Two GEMMs of one layout in one launch (256 x 256 direct-to-LDS tiles,
+// no split K, no second K segment), else one after the other.
+template <bool AK, bool BKM>
+static hipError_t run_pair_layout(const GemmDesc& g1, const EpiArgs& e1, const GemmDesc& g2,
+                                  const EpiArgs& e2, int dtype, hipStream_t s, bool* fused) {
+  *fused = false;
+  if (dtype != BF16 || g1.K2 != 0 || g2.K2 != 0) return hipSuccess;
+  auto ok = [](const GemmDesc& g, const EpiArgs& e) {
+    const long tiles = (long)((g.M + 255) / 256) * ((g.N + 255) / 256);
+    constexpr int BKL = AK ? GEMM_BK : GEMM_BK_MN;
+    return tiles >= 240 && e.kind != EPI_ROPE && e.kind != EPI_STORE_DELTA && e.kind != EPI_LOGITS &&
+           splitk_count(g, e, tiles, BKL) == 1 && dma_operand_ok(g.A, g.lda, AK, g.M, g.ka, 256) &&
+           dma_operand_ok(g.B, g.ldb, BKM, g.N, g.kb, 256);
+  };
+  if (!ok(g1, e1) || !ok(g2, e2)) return hipSuccess;
+  constexpr int BKL = AK ? GEMM_BK : GEMM_BK_MN, NSTL = AK ? GEMM_NST : GEMM_NST_MN;
+  GemmDesc a = g1, b = g2;
+  a.ksplit = a.K;
+  b.ksplit = b.K;
+  *fused = true;
+  return run_dma<256, 256, GEMM_WM, GEMM_WN, BKL, NSTL, AK, BKM>(a, e1, s, 1, &b, &e2);
+}
+
+hipError_t launch_gemm_pair(const GemmDesc& g1, const EpiArgs& e1, const GemmDesc& g2,
+                            const EpiArgs& e2, int dtype, hipStream_t s, const char** kname) {
+  if (g1.a_kmajor == g2.a_kmajor && g1.b_kmajor == g2.b_kmajor && g1.M > 0 && g1.N > 0 &&
+      g2.M > 0 && g2.N > 0) {
+    bool fused = false;
+    hipError_t err = hipSuccess;
+    if (g1.a_kmajor && g1.b_kmajor) err = run_pair_layout<true, true>(g1, e1, g2, e2, dtype, s, &fused);
+    else if (g1.a_kmajor) err = run_pair_layout<true, false>(g1, e1, g2, e2, dtype, s, &fused);
+    else if (!g1.b_kmajor) err = run_pair_layout<false, false>(g1, e1, g2, e2, dtype, s, &fused);
+    else err = run_pair_layout<false, true>(g1, e1, g2, e2, dtype, s, &fused);
+    if (fused) {
+      if (kname) {
+        static char buf[4][48];
+        const int w = (g1.a_kmajor ? 2 : 0) + (g1.b_kmajor ? 1 : 0);
+        snprintf(buf[w], sizeof(buf[w]), "gemm_dma_256x256_%s", layout_tag(g1.a_kmajor, g1.b_kmajor));
+        *kname = buf[w];
+      }
+      return err;
+    }
+  }
+  hipError_t err = launch_gemm(g1, e1, dtype, s, kname);
+  return err == hipSuccess ? launch_gemm(g2, e2, dtype, s, kname) : err;
 }
 
 hipError_t launch_gemm(const GemmDesc& g, const EpiArgs& e, int dtype, hipStream_t s,

@@ -265,7 +265,7 @@ struct Plan {
   size_t rope, seqlens, pos;
   std::vector<size_t> X;  // L + 1
   std::vector<size_t> N1, RS1, MU1, QKV, O, LSE, X2, N2, RS2, MU2, UP, ACT;
-  size_t DX, DXA, DUP, DN, DO, DQKV, DELTA, PART;
+  size_t DX, DXA, DXB, DUP, DN, DO, DQKV, DELTA, PART;
   size_t HN, HRS, HMU, ZC, HST, DZ, DNF, ROWLOSS, NOMEGA;
   int nst;  // 64-column blocks of a logit row (softmax partials, bf16 path)
   // readout adapter: act copy of h_out, pre-activation, activation, h',
@@ -318,6 +318,7 @@ void build_plan(const zl_config& c, Plan& p) {
   p.X[m.L] = take(T * m.d * 4);
   p.DX = take(T * m.d * 4);
   p.DXA = take(T * m.d * act);
+  p.DXB = take(T * m.d * act);
   p.DUP = take(T * m.nup * act);
   p.DN = take(T * m.d * 4);
   p.DO = take(T * m.dq * act);
@@ -452,6 +453,20 @@ static hipError_t run_gemm(zl_chunk* c, hipStream_t s, const GemmDesc& g, const 
   gs.part_elems = c->plan.spk_elems;
   hipError_t err = launch_gemm(gs, e, c->act, s, &kn);
   c->prof_stop(pi, s, kn, 2.0 * g.M * g.N * ((k_alg < 0 ? g.K : k_alg) + g.K2), 0.0);
+  return err;
+}
+
+// Two independent GEMMs, one launch when they share a kernel.
+static hipError_t run_gemm_pair(zl_chunk* c, hipStream_t s, const GemmDesc& g1, const EpiArgs& e1,
+                                const GemmDesc& g2, const EpiArgs& e2) {
+  const int pi = c->prof_start(s);
+  const char* kn = "gemm";
+  GemmDesc a = g1, b = g2;
+  a.part = b.part = c->plan.spk_elems ? c->at<float>(c->plan.SPK) : nullptr;
+  a.part_elems = b.part_elems = c->plan.spk_elems;
+  hipError_t err = launch_gemm_pair(a, e1, b, e2, c->act, s, &kn);
+  c->prof_stop(pi, s, kn, 2.0 * g1.M * g1.N * (g1.K + g1.K2) + 2.0 * g2.M * g2.N * (g2.K + g2.K2),
+               0.0);
   return err;
 }
 
@@ -887,7 +902,11 @@ zl_status zl_chunk_backward(zl_chunk* c, float grad_scale, int accumulate, void*
   const bool ln = !m.llama;
   const int acc = (accumulate && !c->grad_fresh) ? 1 : 0;
   float* DX = c->at<float>(p.DX);
+  // MFMA copies of the residual-stream gradient: DXA from the norm-1 backward
+  // (or the head) feeds the down projection, DXB from the norm-2 backward the
+  // output projection, so the down weight gradient can wait for the QKV one
   void* DXA = c->ws + p.DXA;
+  void* DXB = c->ws + p.DXB;
   void* DUP = c->ws + p.DUP;
   float* DN = c->at<float>(p.DN);
   void* DO = c->ws + p.DO;
@@ -901,6 +920,18 @@ zl_status zl_chunk_backward(zl_chunk* c, float grad_scale, int accumulate, void*
     e.scale = grad_scale;
     e.accumulate = acc;
     return run_gemm(c, s, gdesc(M, N, T, A, lda, false, Bm, ldb, false), e);
+  };
+  // Two layer weight gradients in one launch: the tail wave of one is
+  // filled with tiles of the other (both read buffers that stay unchanged
+  // until the launch, and write disjoint gradients).
+  auto wgrad2 = [&](int M1, int N1, const void* A1, int64_t lda1, const void* B1, int64_t ldb1,
+                    size_t goff1, int M2, int N2, const void* A2, int64_t lda2, const void* B2,
+                    int64_t ldb2, size_t goff2) -> hipError_t {
+    EpiArgs e1 = epi(EPI_GRAD, c->G(goff1), N1, F32), e2 = epi(EPI_GRAD, c->G(goff2), N2, F32);
+    e1.scale = e2.scale = grad_scale;
+    e1.accumulate = e2.accumulate = acc;
+    return run_gemm_pair(c, s, gdesc(M1, N1, T, A1, lda1, false, B1, ldb1, false), e1,
+                         gdesc(M2, N2, T, A2, lda2, false, B2, ldb2, false), e2);
   };
   auto bias_grad = [&](const void* x, int dt, int n, size_t goff) -> hipError_t {
     int nblk = 0;
@@ -976,9 +1007,8 @@ zl_status zl_chunk_backward(zl_chunk* c, float grad_scale, int accumulate, void*
     if (r) {
       ZL_HIP(lora_bwd_w(DXA, m.d, c->ws + p.ACT[l], m.ff, lo->down_a, r, c->ws + p.LXD[l],
                         lo->down_b, w_d, 1));
-    } else {
-      ZL_HIP(wgrad(m.d, m.ff, DXA, m.d, c->ws + p.ACT[l], m.ff, o.w_down));
-      if (ln) ZL_HIP(bias_grad(DX, F32, m.d, o.b_down));
+    } else if (ln) {  // the down weight gradient runs with the QKV one below
+      ZL_HIP(bias_grad(DX, F32, m.d, o.b_down));
     }
     // up projection (gate|up or fc)
     {
@@ -992,16 +1022,15 @@ zl_status zl_chunk_backward(zl_chunk* c, float grad_scale, int accumulate, void*
     if (r) {
       ZL_HIP(lora_bwd_w(DUP, m.nup, c->ws + p.N2[l], m.d, lo->up_a, m.nua, c->ws + p.LXU[l],
                         lo->up_b, m.llama ? w_up : w_up1, n_up));
-    } else {
-      ZL_HIP(wgrad(m.nup, m.d, DUP, m.nup, c->ws + p.N2[l], m.d, o.w_up));
-      if (ln) ZL_HIP(bias_grad(DUP, act, m.nup, o.b_up));
+    } else if (ln) {  // the up weight gradient runs with the output projection's below
+      ZL_HIP(bias_grad(DUP, act, m.nup, o.b_up));
     }
     // norm 2
     {
       int nblk = 0;
       ZL_RUN("norm_bwd", 0, (double)T * m.d * (16 + c->asz()), launch_norm_bwd(ln, DN, c->at<float>(p.X2[l]), c->V32(o.ln2_w),
                              ln ? c->at<float>(p.MU2[l]) : nullptr, c->at<float>(p.RS2[l]), DX, DX,
-                             DXA, act, r ? nullptr : PART, ln && !r ? PART + half_part : nullptr,
+                             DXB, act, r ? nullptr : PART, ln && !r ? PART + half_part : nullptr,
                              T, m.d, s, &nblk));
       if (!r) {
         ZL_RUN("reduce_rows", 0, 0, launch_reduce_rows(PART, nblk, m.d, c->G(o.ln2_w), grad_scale, acc, s));
@@ -1017,15 +1046,18 @@ zl_status zl_chunk_backward(zl_chunk* c, float grad_scale, int accumulate, void*
         e.aux = c->ws + p.O[l]; e.ldaux = m.dq; e.hd = m.hd;
         e.delta = c->at<float>(p.DELTA); e.seq = c->S; e.nheads = m.hq;
       }
-      GemmDesc g = gdesc(T, m.dq, m.d, DXA, m.d, true, c->W(o.w_o), m.dq, false);
-      if (r) ZL_HIP(lora_bwd_dx(DXA, m.d, lo->o_a, r, lo->o_b, w_d, 1, m.dq, true, g));
+      GemmDesc g = gdesc(T, m.dq, m.d, DXB, m.d, true, c->W(o.w_o), m.dq, false);
+      if (r) ZL_HIP(lora_bwd_dx(DXB, m.d, lo->o_a, r, lo->o_b, w_d, 1, m.dq, true, g));
       ZL_HIP(run_gemm(c, s, g, e));
     }
     if (r) {
-      ZL_HIP(lora_bwd_w(DXA, m.d, c->ws + p.O[l], m.dq, lo->o_a, r, c->ws + p.LXO[l], lo->o_b,
+      ZL_HIP(lora_bwd_w(DXB, m.d, c->ws + p.O[l], m.dq, lo->o_a, r, c->ws + p.LXO[l], lo->o_b,
                         w_d, 1));
     } else {
-      ZL_HIP(wgrad(m.d, m.dq, DXA, m.d, c->ws + p.O[l], m.dq, o.w_o));
+      // up (dy = DUP, kept until the next layer's down data gradient) with
+      // the output projection (dy = DXB)
+      ZL_HIP(wgrad2(m.nup, m.d, DUP, m.nup, c->ws + p.N2[l], m.d, o.w_up,
+                    m.d, m.dq, DXB, m.d, c->ws + p.O[l], m.dq, o.w_o));
       if (ln) ZL_HIP(bias_grad(DX, F32, m.d, o.b_o));
     }
     // attention
@@ -1070,7 +1102,10 @@ zl_status zl_chunk_backward(zl_chunk* c, float grad_scale, int accumulate, void*
       ZL_HIP(lora_bwd_w(DQKV, m.nqkv, c->ws + p.N1[l], m.d, lo->qkv_a, m.nqa, c->ws + p.LXQ[l],
                         lo->qkv_b, m.llama ? w_qkv : w_qkv1, n_qkv));
     } else {
-      ZL_HIP(wgrad(m.nqkv, m.d, DQKV, m.nqkv, c->ws + p.N1[l], m.d, o.w_qkv));
+      // down (dy = DXA, rewritten only by the norm-1 backward below) with
+      // QKV: 3.5 + 1.5 waves of tiles at 8B fill 5 waves instead of 4 + 2
+      ZL_HIP(wgrad2(m.d, m.ff, DXA, m.d, c->ws + p.ACT[l], m.ff, o.w_down,
+                    m.nqkv, m.d, DQKV, m.nqkv, c->ws + p.N1[l], m.d, o.w_qkv));
       if (ln) ZL_HIP(bias_grad(DQKV, act, m.nqkv, o.b_qkv));
     }
     // norm 1; layer 0 forms no gradient into h_in
