@@ -123,11 +123,12 @@ struct EpiArgs {
 // EPI_ROPE is supported by the bf16 MFMA path only (hd <= 128).
 hipError_t launch_gemm(const GemmDesc& g, const EpiArgs& e, int dtype, hipStream_t s,
                        const char** kname = nullptr);
-// Two GEMMs in one launch when both take the 256 x 256 direct-to-LDS path
-// in the same layout (per-element epilogues, no split K or second segment),
-// else launch_gemm on each in turn.  The problems must be independent.
+// Two independent GEMMs in one launch when both take the 256 x 256
+// direct-to-LDS path in the same layout (per-element epilogues, no split K
+// or second segment): *fused = true.  Otherwise nothing is launched and
+// *fused = false (the caller runs launch_gemm on each).
 hipError_t launch_gemm_pair(const GemmDesc& g1, const EpiArgs& e1, const GemmDesc& g2,
-                            const EpiArgs& e2, int dtype, hipStream_t s,
+                            const EpiArgs& e2, int dtype, hipStream_t s, bool* fused,
                             const char** kname = nullptr);
 
 // --------------------------------------------------------------- row ops

@@ -1293,27 +1293,24 @@ static hipError_t run_pair_layout(const GemmDesc& g1, const EpiArgs& e1, const G
 }
 
 hipError_t launch_gemm_pair(const GemmDesc& g1, const EpiArgs& e1, const GemmDesc& g2,
-                            const EpiArgs& e2, int dtype, hipStream_t s, const char** kname) {
-  if (g1.a_kmajor == g2.a_kmajor && g1.b_kmajor == g2.b_kmajor && g1.M > 0 && g1.N > 0 &&
-      g2.M > 0 && g2.N > 0) {
-    bool fused = false;
-    hipError_t err = hipSuccess;
-    if (g1.a_kmajor && g1.b_kmajor) err = run_pair_layout<true, true>(g1, e1, g2, e2, dtype, s, &fused);
-    else if (g1.a_kmajor) err = run_pair_layout<true, false>(g1, e1, g2, e2, dtype, s, &fused);
-    else if (!g1.b_kmajor) err = run_pair_layout<false, false>(g1, e1, g2, e2, dtype, s, &fused);
-    else err = run_pair_layout<false, true>(g1, e1, g2, e2, dtype, s, &fused);
-    if (fused) {
-      if (kname) {
-        static char buf[4][48];
-        const int w = (g1.a_kmajor ? 2 : 0) + (g1.b_kmajor ? 1 : 0);
-        snprintf(buf[w], sizeof(buf[w]), "gemm_dma_256x256_%s", layout_tag(g1.a_kmajor, g1.b_kmajor));
-        *kname = buf[w];
-      }
-      return err;
-    }
+                            const EpiArgs& e2, int dtype, hipStream_t s, bool* fused,
+                            const char** kname) {
+  *fused = false;
+  if (g1.a_kmajor != g2.a_kmajor || g1.b_kmajor != g2.b_kmajor || g1.M <= 0 || g1.N <= 0 ||
+      g2.M <= 0 || g2.N <= 0)
+    return hipSuccess;
+  hipError_t err = hipSuccess;
+  if (g1.a_kmajor && g1.b_kmajor) err = run_pair_layout<true, true>(g1, e1, g2, e2, dtype, s, fused);
+  else if (g1.a_kmajor) err = run_pair_layout<true, false>(g1, e1, g2, e2, dtype, s, fused);
+  else if (!g1.b_kmajor) err = run_pair_layout<false, false>(g1, e1, g2, e2, dtype, s, fused);
+  else err = run_pair_layout<false, true>(g1, e1, g2, e2, dtype, s, fused);
+  if (*fused && kname) {
+    static char buf[4][48];
+    const int w = (g1.a_kmajor ? 2 : 0) + (g1.b_kmajor ? 1 : 0);
+    snprintf(buf[w], sizeof(buf[w]), "gemm_dma_256x256_%s", layout_tag(g1.a_kmajor, g1.b_kmajor));
+    *kname = buf[w];
   }
-  hipError_t err = launch_gemm(g1, e1, dtype, s, kname);
-  return err == hipSuccess ? launch_gemm(g2, e2, dtype, s, kname) : err;
+  return err;
 }
 
 hipError_t launch_gemm(const GemmDesc& g, const EpiArgs& e, int dtype, hipStream_t s,

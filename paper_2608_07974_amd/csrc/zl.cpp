@@ -398,6 +398,9 @@ struct zl_chunk {
     hipEventRecord(prof_ev[2 * i], s);
     return i;
   }
+  void prof_cancel(int i) {  // the last prof_start recorded nothing worth keeping
+    if (i >= 0 && (size_t)i + 1 == prof_used) --prof_used;
+  }
   void prof_stop(int i, hipStream_t s, const char* name, double flops, double bytes) {
     if (i < 0) return;
     hipEventRecord(prof_ev[2 * i + 1], s);
@@ -456,7 +459,8 @@ static hipError_t run_gemm(zl_chunk* c, hipStream_t s, const GemmDesc& g, const 
   return err;
 }
 
-// Two independent GEMMs, one launch when they share a kernel.
+// Two independent GEMMs: one launch when they share a kernel, else one
+// after the other.
 static hipError_t run_gemm_pair(zl_chunk* c, hipStream_t s, const GemmDesc& g1, const EpiArgs& e1,
                                 const GemmDesc& g2, const EpiArgs& e2) {
   const int pi = c->prof_start(s);
@@ -464,10 +468,16 @@ static hipError_t run_gemm_pair(zl_chunk* c, hipStream_t s, const GemmDesc& g1, 
   GemmDesc a = g1, b = g2;
   a.part = b.part = c->plan.spk_elems ? c->at<float>(c->plan.SPK) : nullptr;
   a.part_elems = b.part_elems = c->plan.spk_elems;
-  hipError_t err = launch_gemm_pair(a, e1, b, e2, c->act, s, &kn);
-  c->prof_stop(pi, s, kn, 2.0 * g1.M * g1.N * (g1.K + g1.K2) + 2.0 * g2.M * g2.N * (g2.K + g2.K2),
-               0.0);
-  return err;
+  bool fused = false;
+  hipError_t err = launch_gemm_pair(a, e1, b, e2, c->act, s, &fused, &kn);
+  if (fused || err != hipSuccess) {
+    c->prof_stop(pi, s, kn, 2.0 * g1.M * g1.N * (g1.K + g1.K2) + 2.0 * g2.M * g2.N * (g2.K + g2.K2),
+                 0.0);
+    return err;
+  }
+  c->prof_cancel(pi);
+  err = run_gemm(c, s, g1, e1);
+  return err == hipSuccess ? run_gemm(c, s, g2, e2) : err;
 }
 
 #define ZL_RUN(name, flops, bytes, call)                                             \

@@ -233,3 +233,40 @@ def test_attention_fwd_bwd(dtype, B, S, Hq, Hkv, hd, lens):
                     assert abs(lse[b, h, i] - ref) < 1e-4 * max(1, abs(ref))
                 else:
                     assert lse[b, h, i] == -np.inf
+
+
+def _backward_profile(shp):
+    import workload
+    from tests.gpu_cases import make_inputs, device_chunk, to_dev
+    zl = _zl()
+    params, batch = make_inputs(shp, seed=3)
+    ch = device_chunk(shp, params, batch)
+    d = to_dev(batch, shp.dtype)
+    ch.forward(d["h_in"], d["seq_lens"], d["pos_ids"])
+    ch.objective(d["labels"])
+    torch.cuda.synchronize()
+    zl.zl_profile_begin(ch.handle, 4096)
+    ch.backward(1.0, 0)
+    torch.cuda.synchronize()
+    prof = zl.zl_profile_end(ch.handle, 256)
+    ch.close()
+    return [e for e in prof if e["name"].endswith("_mn")]
+
+
+def test_backward_pairs_weight_gradients():
+    """The weight-gradient GEMMs of an 8B-shaped layer run as two launches,
+    down with QKV and up with the output projection (their tiles fill whole
+    waves together), each carrying the FLOPs of both; a 1B-shaped layer's
+    QKV and output projections have too few tiles to pair and run alone."""
+    import workload
+    shp = workload.get_config("8b").with_(n_layers=1, batch=1, seq=256)
+    T, d, ff = 256, shp.d_model, shp.d_ff
+    nqkv = (shp.n_heads + 2 * shp.n_kv_heads) * shp.head_dim
+    mn = _backward_profile(shp)
+    assert [e["name"] for e in mn] == ["gemm_dma_256x256_mn"]
+    assert mn[0]["launches"] == 2
+    want = 2.0 * T * (d * ff + 2 * ff * d + d * shp.n_heads * shp.head_dim + nqkv * d)
+    assert mn[0]["flops"] == pytest.approx(want, rel=1e-9)
+    shp1 = workload.get_config("1b").with_(n_layers=1, batch=1, seq=512)
+    launches = sum(e["launches"] for e in _backward_profile(shp1))
+    assert launches == 4
