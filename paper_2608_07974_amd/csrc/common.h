@@ -11,7 +11,14 @@ namespace zl {
 // ------------------------------------------------------------------ types
 typedef uint16_t bf16_t;  // storage type of bf16 values
 
-enum DType { F32 = 0, BF16 = 1 };
+// F16 only stores the bf16 path's logit cache (values of a few tens, where
+// fp16 keeps 3 more mantissa bits than bf16).
+enum DType { F32 = 0, BF16 = 1, F16 = 2 };
+
+__device__ inline uint16_t f32_to_f16(float f) {  // round to nearest even
+  return __builtin_bit_cast(uint16_t, (_Float16)f);
+}
+__device__ inline float f16_to_f32(uint16_t h) { return (float)__builtin_bit_cast(_Float16, h); }
 
 __host__ __device__ inline float bf16_to_f32(bf16_t h) {
   uint32_t u = (uint32_t)h << 16;
@@ -113,6 +120,8 @@ struct EpiArgs {
   float4* stats;        // EPI_LOGITS
   int64_t ldst;
   int pair;
+  const int32_t* lab;   // EPI_LOGITS (optional): label of each token; the
+  float* zy;            //   fp32 logit of the label, z[token, lab], goes to zy
   const int32_t* pos;   // EPI_ROPE: position of row m
   const float2* rope;   // EPI_ROPE: (cos, sin) table [max_pos, hd/2]
   int max_pos, hd, n_rot;
@@ -211,8 +220,10 @@ hipError_t launch_attn_bwd(const AttnDesc& a, int dtype, hipStream_t s, bool* ro
 
 // -------------------------------------------------------------- objective
 struct ObjDesc {
-  const float* zc;      // logits cache [rows_stacked, ldz]; row 2i = z, 2i+1 = z' (stacked)
+  const void* zc;       // logits cache [rows_stacked, ldz]; row 2i = z, 2i+1 = z' (stacked)
   int64_t ldz;
+  int z_dtype;          // F32, or F16 (with stats and zy)
+  const float* zy;      // optional fp32 logit of each row's label (used for the loss)
   int stacked;          // 2 when z' rows are interleaved, else 1
   const int32_t* labels;  // [rows] for this row block
   int rows, V, Vpad;

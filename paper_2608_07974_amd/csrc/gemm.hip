@@ -39,10 +39,12 @@ __device__ inline float gelu_grad_f(float x) {
 }
 
 __device__ __forceinline__ float ld_act(const void* p, int dt, size_t i) {
+  if (dt == F16) return f16_to_f32(((const uint16_t*)p)[i]);
   return dt == BF16 ? bf16_to_f32(((const bf16_t*)p)[i]) : ((const float*)p)[i];
 }
 __device__ __forceinline__ void st_act(void* p, int dt, size_t i, float v) {
-  if (dt == BF16) ((bf16_t*)p)[i] = f32_to_bf16(v);
+  if (dt == F16) ((uint16_t*)p)[i] = f32_to_f16(v);
+  else if (dt == BF16) ((bf16_t*)p)[i] = f32_to_bf16(v);
   else ((float*)p)[i] = v;
 }
 
@@ -129,6 +131,12 @@ __device__ __forceinline__ void stv_act(void* p, int dt, size_t i, const float (
     for (int k = 0; k < 4; ++k)
       w[k] = (uint32_t)f32_to_bf16(v[2 * k]) | ((uint32_t)f32_to_bf16(v[2 * k + 1]) << 16);
     *reinterpret_cast<uint4*>(static_cast<bf16_t*>(p) + i) = make_uint4(w[0], w[1], w[2], w[3]);
+  } else if (dt == F16) {
+    uint32_t w[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      w[k] = (uint32_t)f32_to_f16(v[2 * k]) | ((uint32_t)f32_to_f16(v[2 * k + 1]) << 16);
+    *reinterpret_cast<uint4*>(static_cast<uint16_t*>(p) + i) = make_uint4(w[0], w[1], w[2], w[3]);
   } else {
     float* q = static_cast<float*>(p) + i;
 #pragma unroll
@@ -381,6 +389,14 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[BM / WM / 32][B
           w[k] = x.x - y.x; w[k + 1] = x.y - y.y; w[k + 2] = x.z - y.z; w[k + 3] = x.w - y.w;
         }
         epilogue_v(e, g.M, g.N, m, n, v, vec);
+        // the label's logit of a z row, in fp32 (the cache may be fp16)
+        if (e.zy && m < g.M && !(e.pair && (m & 1))) {
+          const int tok = e.pair ? m >> 1 : m;
+          const int y = e.lab[tok];
+#pragma unroll
+          for (int k = 0; k < EW; ++k)
+            if (y == n + k) e.zy[tok] = v[k];
+        }
         // block maximum first (8 lanes), then one exponential per logit
         float mx = -INFINITY;
 #pragma unroll
@@ -1320,7 +1336,8 @@ hipError_t launch_gemm(const GemmDesc& g, const EpiArgs& e, int dtype, hipStream
   if (g.K2 < 0 || (g.K2 > 0 && (!g.A2 || !g.B2))) return hipErrorInvalidValue;
   if (e.kind == EPI_ROPE && (dtype != BF16 || e.hd > 128 || 128 % e.hd != 0 || !e.pos || !e.rope))
     return hipErrorInvalidValue;
-  if (e.kind == EPI_LOGITS && (dtype != BF16 || !e.stats || e.out_dtype != F32 || (e.pair && g.M % 2)))
+  if (e.kind == EPI_LOGITS && (dtype != BF16 || !e.stats || (e.out_dtype != F32 && e.out_dtype != F16) ||
+                              (e.pair && g.M % 2) || (e.zy && !e.lab)))
     return hipErrorInvalidValue;
   if (e.kind == EPI_STORE_DELTA &&
       (dtype != BF16 || !e.delta || !e.aux || e.hd < EW || e.hd > 128 || 128 % e.hd ||

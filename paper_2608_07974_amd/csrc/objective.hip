@@ -1,8 +1,10 @@
 // Local objective of Eq. (3)-(5) on the frozen readout of Eq. (2).
 //
-// The head GEMM writes fp32 logits of a row block: rows of z (readout of
+// The head GEMM writes the logits of a row block: rows of z (readout of
 // h_out) interleaved with rows of z' (readout of h_in, the stop-gradient
-// consistency target) when alpha < 1.  One workgroup per token row then
+// consistency target) when alpha < 1; fp32, or fp16 in the bf16 path, where
+// the GEMM's epilogue also leaves the fp32 statistics of pass 1 and the
+// fp32 label logit z_y.  One workgroup per token row then
 //   pass 1: online max / sum-exp of z and z', plus the KL statistic
 //           E = sum_v p_v (z_v - z'_v)   (reverse)   or
 //           F = sum_v q_v (z'_v - z_v)   (forward),
@@ -104,11 +106,25 @@ __device__ inline void st_dz4(const ObjDesc& o, int64_t i, const float (&g)[4]) 
   }
 }
 
+// Logits as cached: fp32, or fp16 (ZT = uint16_t) in the bf16 path.
+__device__ inline float ldz1(const float* p, int64_t v) { return p[v]; }
+__device__ inline float ldz1(const uint16_t* p, int64_t v) { return f16_to_f32(p[v]); }
+__device__ inline void ldz4(const float* p, int64_t v, float (&x)[4]) {
+  const float4 a = *reinterpret_cast<const float4*>(p + v);
+  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+}
+__device__ inline void ldz4(const uint16_t* p, int64_t v, float (&x)[4]) {
+  const uint2 a = *reinterpret_cast<const uint2*>(p + v);
+  x[0] = f16_to_f32((uint16_t)(a.x & 0xffff)); x[1] = f16_to_f32((uint16_t)(a.x >> 16));
+  x[2] = f16_to_f32((uint16_t)(a.y & 0xffff)); x[3] = f16_to_f32((uint16_t)(a.y >> 16));
+}
+
+template <typename ZT>
 __global__ void __launch_bounds__(OT) objective_rows_kernel(ObjDesc o) {
   __shared__ Soft red[OT / 64];
   const int i = blockIdx.x;
-  const float* z = o.zc + (int64_t)i * o.stacked * o.ldz;
-  const float* zp = o.stacked == 2 ? z + o.ldz : nullptr;
+  const ZT* z = static_cast<const ZT*>(o.zc) + (int64_t)i * o.stacked * o.ldz;
+  const ZT* zp = o.stacked == 2 ? z + o.ldz : nullptr;
   const int y = o.labels[i];
   const bool in_omega = label_ok(y, o.V);
   const float nomega = o.n_omega[0];
@@ -137,13 +153,9 @@ __global__ void __launch_bounds__(OT) objective_rows_kernel(ObjDesc o) {
     }
   }
   for (int v = o.stats ? V4 : threadIdx.x * 4; v < V4; v += OT * 4) {
-    const float4 a4 = *reinterpret_cast<const float4*>(z + v);
-    const float a[4] = {a4.x, a4.y, a4.z, a4.w};
-    float b[4] = {0.f, 0.f, 0.f, 0.f};
-    if (zp) {
-      const float4 b4 = *reinterpret_cast<const float4*>(zp + v);
-      b[0] = b4.x; b[1] = b4.y; b[2] = b4.z; b[3] = b4.w;
-    }
+    float a[4], b[4] = {0.f, 0.f, 0.f, 0.f};
+    ldz4(z, v, a);
+    if (zp) ldz4(zp, v, b);
     const float ab[4] = {a[0] - b[0], a[1] - b[1], a[2] - b[2], a[3] - b[3]};
     sp = soft_add4(sp, a, ab);  // e accumulates sum p (z - z') unnormalised
     if (zp) {
@@ -152,8 +164,8 @@ __global__ void __launch_bounds__(OT) objective_rows_kernel(ObjDesc o) {
     }
   }
   for (int v = V4 + threadIdx.x; v < (o.stats ? 0 : o.V); v += OT) {
-    const float a = z[v];
-    const float b = zp ? zp[v] : 0.f;
+    const float a = ldz1(z, v);
+    const float b = zp ? ldz1(zp, v) : 0.f;
     sp = soft_add(sp, a, a - b);
     if (zp) sq = soft_add(sq, b, b - a);
   }
@@ -166,7 +178,7 @@ __global__ void __launch_bounds__(OT) objective_rows_kernel(ObjDesc o) {
     lse2 = sq.m + __logf(sq.s);
     F = sq.e / sq.s;
   }
-  const float zy = z[y];
+  const float zy = o.zy ? o.zy[i] : ldz1(z, y);
   const float ce = lse - zy;
   float kl = 0.f;
   if (zp) kl = rev ? (E - lse + lse2) : (F - lse2 + lse);
@@ -186,15 +198,15 @@ __global__ void __launch_bounds__(OT) objective_rows_kernel(ObjDesc o) {
   for (int v = threadIdx.x * 4; v < o.Vpad; v += OT * 4) {
     float g[4] = {0.f, 0.f, 0.f, 0.f};
     if (v < V4) {
-      const float4 a4 = *reinterpret_cast<const float4*>(z + v);
-      float4 b4 = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (zp) b4 = *reinterpret_cast<const float4*>(zp + v);
-      g[0] = grad(v, a4.x, b4.x); g[1] = grad(v + 1, a4.y, b4.y);
-      g[2] = grad(v + 2, a4.z, b4.z); g[3] = grad(v + 3, a4.w, b4.w);
+      float a4[4], b4[4] = {0.f, 0.f, 0.f, 0.f};
+      ldz4(z, v, a4);
+      if (zp) ldz4(zp, v, b4);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) g[k] = grad(v + k, a4[k], b4[k]);
     } else {
 #pragma unroll
       for (int k = 0; k < 4; ++k)
-        if (v + k < o.V) g[k] = grad(v + k, z[v + k], zp ? zp[v + k] : 0.f);
+        if (v + k < o.V) g[k] = grad(v + k, ldz1(z, v + k), zp ? ldz1(zp, v + k) : 0.f);
     }
     st_dz4(o, orow + v, g);
   }
@@ -202,7 +214,12 @@ __global__ void __launch_bounds__(OT) objective_rows_kernel(ObjDesc o) {
 
 hipError_t launch_objective_rows(const ObjDesc& o, hipStream_t s) {
   if (o.rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(objective_rows_kernel, dim3(o.rows), dim3(OT), 0, s, o);
+  if (o.z_dtype == F16) {
+    if (!o.stats) return hipErrorInvalidValue;  // fp16 logits come with the GEMM's statistics
+    hipLaunchKernelGGL(objective_rows_kernel<uint16_t>, dim3(o.rows), dim3(OT), 0, s, o);
+  } else {
+    hipLaunchKernelGGL(objective_rows_kernel<float>, dim3(o.rows), dim3(OT), 0, s, o);
+  }
   return hipGetLastError();
 }
 

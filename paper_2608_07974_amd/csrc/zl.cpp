@@ -266,7 +266,7 @@ struct Plan {
   std::vector<size_t> X;  // L + 1
   std::vector<size_t> N1, RS1, MU1, QKV, O, LSE, X2, N2, RS2, MU2, UP, ACT;
   size_t DX, DXA, DXB, DUP, DN, DO, DQKV, DELTA, PART;
-  size_t HN, HRS, HMU, ZC, HST, DZ, DNF, ROWLOSS, NOMEGA;
+  size_t HN, HRS, HMU, ZC, HST, ZY, DZ, DNF, ROWLOSS, NOMEGA;
   int nst;  // 64-column blocks of a logit row (softmax partials, bf16 path)
   // readout adapter: act copy of h_out, pre-activation, activation, h',
   // dL/dh' (fp32 and act), dL/dU
@@ -334,9 +334,10 @@ void build_plan(const zl_config& c, Plan& p) {
   p.HN = take(S2 * m.d * act);
   p.HRS = take(S2 * 4);
   p.HMU = take(S2 * 4);
-  p.ZC = take(S2 * p.Vpad * 4);
+  p.ZC = take(S2 * p.Vpad * (act == 2 ? 2 : 4));  // fp16 logits in the bf16 path
   p.nst = (m.V + 63) / 64;
   p.HST = take(act == 2 ? S2 * p.nst * 16 : 0);
+  p.ZY = take(act == 2 ? R * 4 : 0);
   p.DZ = take(R * p.Vpad * act);
   p.DNF = take(R * m.d * 4);
   p.ROWLOSS = take(T * 4);
@@ -841,20 +842,26 @@ zl_status zl_local_objective(zl_chunk* c, const int32_t* labels, float* loss_out
     {
       // bf16: the GEMM's epilogue also leaves per-row softmax partials of
       // 64-column blocks (z rows paired with their z' rows), which replace
-      // the objective's statistics pass over the logits
+      // the objective's statistics pass over the logits, and the fp32 logit
+      // of each label; the cached logits are then fp16 (they only form
+      // dL/dz)
       const bool fused = act == BF16;
-      EpiArgs e = epi(fused ? EPI_LOGITS : EPI_STORE, c->at<float>(p.ZC), p.Vpad, F32);
+      EpiArgs e = epi(fused ? EPI_LOGITS : EPI_STORE, c->ws + p.ZC, p.Vpad, fused ? F16 : F32);
       if (fused) {
         e.stats = c->at<float4>(p.HST);
         e.ldst = p.nst;
         e.pair = stk == 2;
+        e.lab = labels + r0;
+        e.zy = c->at<float>(p.ZY);
       }
       ZL_HIP(run_gemm(c, s, gdesc(stk * rows, m.V, m.d, c->ws + p.HN, m.d, true, c->buf.head_w, m.d,
                                true), e));
     }
     {
       ObjDesc o;
-      o.zc = c->at<float>(p.ZC); o.ldz = p.Vpad; o.stacked = stk;
+      o.zc = c->ws + p.ZC; o.ldz = p.Vpad; o.stacked = stk;
+      o.z_dtype = act == BF16 ? F16 : F32;
+      o.zy = act == BF16 ? c->at<float>(p.ZY) : nullptr;
       o.labels = labels + r0; o.rows = rows; o.V = m.V; o.Vpad = p.Vpad;
       o.alpha = c->cfg.alpha; o.consis = c->cfg.consis; o.n_omega = nomega;
       o.dz = c->ws + p.DZ; o.lddz = p.Vpad; o.dz_dtype = act;
@@ -862,7 +869,7 @@ zl_status zl_local_objective(zl_chunk* c, const int32_t* labels, float* loss_out
       o.stats = act == BF16 ? c->at<float4>(p.HST) : nullptr;
       o.ldst = p.nst;
       o.nst = p.nst;
-      ZL_RUN("objective_rows", 0, (double)rows * (stk * 4.0 * m.V + c->asz() * p.Vpad), launch_objective_rows(o, s));
+      ZL_RUN("objective_rows", 0, (double)rows * (stk * (act == BF16 ? 2.0 : 4.0) * m.V + c->asz() * p.Vpad), launch_objective_rows(o, s));
     }
     {
       GemmDesc g = gdesc(rows, m.d, p.Vpad, c->ws + p.DZ, p.Vpad, true, c->buf.head_w, m.d, false);
