@@ -52,6 +52,20 @@ __device__ inline bf16x8_t zero8() {
 
 __device__ inline __bf16 to_bf16(float f) { return __builtin_bit_cast(__bf16, f32_to_bf16(f)); }
 
+// Max over lanes l and l ^ 16 (l ^ 32): the permlane swaps exchange 16-lane
+// rows (32-lane halves) of two copies of x, so each lane ends up holding its
+// own value and its partner's in the two results (VALU, no LDS round trip).
+__device__ inline float max_xor16(float x) {
+  const unsigned u = __builtin_bit_cast(unsigned, x);
+  const auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  return fmaxf(__builtin_bit_cast(float, r[0]), __builtin_bit_cast(float, r[1]));
+}
+__device__ inline float max_xor32(float x) {
+  const unsigned u = __builtin_bit_cast(unsigned, x);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return fmaxf(__builtin_bit_cast(float, r[0]), __builtin_bit_cast(float, r[1]));
+}
+
 // A 64 x HD tile staged global -> registers -> LDS (row-major, swizzled).
 template <int HD>
 struct TileStage {
@@ -324,9 +338,7 @@ __global__ void __launch_bounds__(FW_NT) attn_fwd_mfma(AttnDesc a) {
 #pragma unroll
       for (int blk = 0; blk < 4; ++blk)
         tmax = fmaxf(tmax, fmaxf(fmaxf(x[blk][0], x[blk][1]), fmaxf(x[blk][2], x[blk][3])));
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-      tmax *= cs;
+      tmax = max_xor32(max_xor16(tmax)) * cs;
       const bool move = tmax > m[j] + RESCALE_TAU;
       if (__any(move)) {
         const float mnew = move ? tmax : m[j];
