@@ -193,8 +193,42 @@ def test_window_accumulation_fp32():
     ch.close()
 
 
+def _window_case(shp, tol_g, tol_p, seeds=(0, 5)):
+    """Two micro-batches, grad_scale 1/2, accumulate -> one step (S3)."""
+    params, b1 = make_inputs(shp, seed=seeds[0])
+    _, b2 = make_inputs(shp, seed=seeds[1])
+    b2["head_w"], b2["head_norm_w"], b2["head_norm_b"] = b1["head_w"], b1["head_norm_w"], b1["head_norm_b"]
+    ch = device_chunk(shp, params, b1)
+    for b in (b1, b2):
+        d = to_dev(b, shp.dtype)
+        ch.forward(d["h_in"], d["seq_lens"], d["pos_ids"])
+        ch.objective(d["labels"])
+        ch.backward(0.5, 1)
+    torch.cuda.synchronize()
+    g = ch.tensors(ch.grad)
+    ch.step()
+    p = ch.tensors(ch.master)
+    cfg = oracle_cfg(shp)
+    mbs = [dict(h_in=b["h_in"], labels=b["labels"], seq_lens=b["seq_lens"], pos_ids=b["pos_ids"])
+           for b in (b1, b2)]
+    r = oracle.chunk_update_ref(cfg, params, init_opt_state(), mbs, b1["head_w"], b1["head_norm_w"],
+                                b1["head_norm_b"])
+    for k in r["grads"]:
+        assert rel_err(g[k], r["grads"][k]) < tol_g, (k, rel_err(g[k], r["grads"][k]))
+        assert rel_err(p[k], r["params"][k]) < tol_p, (k, rel_err(p[k], r["params"][k]))
+    ch.close()
+
+
 # --------------------------------------------------------------- bf16 shapes
 GPT2 = workload.get_config("gpt2")
+
+
+def test_llama1b_bf16_lora_window_two_microbatches():
+    """The window in bf16 with LoRA at T = 512: the factor weight gradients
+    split K, so the second micro-batch adds its split partials into the
+    first one's gradient."""
+    _window_case(workload.get_config("1b").with_(n_layers=1, batch=1, seq=512, lora_rank=16),
+                 TOL_GRAD["bf16"], TOL["bf16"])
 
 
 def test_gpt2_bf16_reduced_tokens():
