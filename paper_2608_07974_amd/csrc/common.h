@@ -15,7 +15,11 @@ typedef uint16_t bf16_t;  // storage type of bf16 values
 // fp16 keeps 3 more mantissa bits than bf16).
 enum DType { F32 = 0, BF16 = 1, F16 = 2 };
 
-__device__ inline uint16_t f32_to_f16(float f) {  // round to nearest even
+// Round to nearest even; finite values beyond the fp16 range saturate at
+// +-65504 instead of becoming infinite (dL/dz of such a row is then inexact;
+// the loss, taken from fp32 statistics, is not), NaN stays NaN.
+__device__ inline uint16_t f32_to_f16(float f) {
+  f = f > 65504.f ? 65504.f : (f < -65504.f ? -65504.f : f);
   return __builtin_bit_cast(uint16_t, (_Float16)f);
 }
 __device__ inline float f16_to_f32(uint16_t h) { return (float)__builtin_bit_cast(_Float16, h); }
