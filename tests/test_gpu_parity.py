@@ -130,8 +130,11 @@ def _case(shp, steps=1, seed=0, stress=True, seq_lens=None, drop=0, alpha=0.5, c
 TINY = workload.get_config("tiny")
 
 
-@pytest.mark.parametrize("alpha,consis", [(0.5, "reverse"), (1.0, "reverse"), (0.3, "forward")])
+@pytest.mark.parametrize("alpha,consis", [(0.5, "reverse"), (1.0, "reverse"), (0.3, "forward"),
+                                         (0.05, "reverse"), (0.05, "forward")])
 def test_tiny_fp32_chunk1(alpha, consis):
+    """alpha = 1: cross-entropy only; alpha = 0.05: almost all consistency
+    term (Eq. (3); alpha is read as a weight in (0, 1]), both KL directions."""
     _case(TINY, alpha=alpha, consis=consis)
 
 
