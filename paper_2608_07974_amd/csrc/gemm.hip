@@ -252,8 +252,8 @@ __device__ inline void tile_coords(int b, int nbm, int nbn, int& tm, int& tn) {
     const int x = b % 8, idx = b / 8;
     b = (x < rem ? x * (per + 1) : rem * (per + 1) + (x - rem) * per) + idx;
   }
-#ifndef GEMM_GROUP_M
-#define GEMM_GROUP_M 8
+#ifndef GEMM_GROUP_M  // 4 measured best in the 8B update (2, 6, 8 and 16 slower)
+#define GEMM_GROUP_M 4
 #endif
   const int GROUP_M = GEMM_GROUP_M;
   const int group = b / (GROUP_M * nbn);
