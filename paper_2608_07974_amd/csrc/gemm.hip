@@ -1127,6 +1127,13 @@ static const char* layout_tag(bool ak, bool bk) {
 #ifndef GEMM_NST_MN
 #define GEMM_NST_MN 3
 #endif
+// k-tile depth and stages per operand layout: both K-major (forward) BK 64
+// with two stages; otherwise (an MN-major operand: data and weight
+// gradients) BK 32 with three stages, measured faster in the 8B update
+template <bool AK, bool BKM> struct KTile {
+  static constexpr int BK = AK && BKM ? GEMM_BK : GEMM_BK_MN;
+  static constexpr int NST = AK && BKM ? GEMM_NST : GEMM_NST_MN;
+};
 #ifndef GEMM_DS
 #define GEMM_DS 1
 #endif
@@ -1259,9 +1266,7 @@ static hipError_t run_layout(const GemmDesc& g, const EpiArgs& e, int dtype, hip
                      (g.K2 <= 0 || (dma_operand_ok(g.A2, g.lda2, AK, g.M, g.K2, R) &&
                                     dma_operand_ok(g.B2, g.ldb2, BKM, g.N, g.K2, R)));
     if (dma) {
-      // an M-contiguous A (weight gradients) runs best with shallower,
-      // deeper-pipelined k tiles
-      constexpr int BKL = AK ? GEMM_BK : GEMM_BK_MN, NSTL = AK ? GEMM_NST : GEMM_NST_MN;
+      constexpr int BKL = KTile<AK, BKM>::BK, NSTL = KTile<AK, BKM>::NST;
       if (large) { err = run_dma_split<256, 256, GEMM_WM, GEMM_WN, BKL, NSTL, AK, BKM>(g, e, s); which = 3; }
       else { err = run_dma_split<128, 128, 2, 2, BKL, NSTL, AK, BKM>(g, e, s); which = 4; }
     } else if (large) {
@@ -1294,13 +1299,13 @@ static hipError_t run_pair_layout(const GemmDesc& g1, const EpiArgs& e1, const G
   if (dtype != BF16 || g1.K2 != 0 || g2.K2 != 0) return hipSuccess;
   auto ok = [](const GemmDesc& g, const EpiArgs& e) {
     const long tiles = (long)((g.M + 255) / 256) * ((g.N + 255) / 256);
-    constexpr int BKL = AK ? GEMM_BK : GEMM_BK_MN;
+    constexpr int BKL = KTile<AK, BKM>::BK;
     return tiles >= 240 && e.kind != EPI_ROPE && e.kind != EPI_STORE_DELTA && e.kind != EPI_LOGITS &&
            splitk_count(g, e, tiles, BKL) == 1 && dma_operand_ok(g.A, g.lda, AK, g.M, g.ka, 256) &&
            dma_operand_ok(g.B, g.ldb, BKM, g.N, g.kb, 256);
   };
   if (!ok(g1, e1) || !ok(g2, e2)) return hipSuccess;
-  constexpr int BKL = AK ? GEMM_BK : GEMM_BK_MN, NSTL = AK ? GEMM_NST : GEMM_NST_MN;
+  constexpr int BKL = KTile<AK, BKM>::BK, NSTL = KTile<AK, BKM>::NST;
   GemmDesc a = g1, b = g2;
   a.ksplit = a.K;
   b.ksplit = b.K;
