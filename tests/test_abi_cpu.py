@@ -172,6 +172,21 @@ def test_create_rejects_bad_buffers_without_gpu():
     assert ei.value.status == zl.ZL_ERR_WORKSPACE
 
 
+@pytest.mark.parametrize("M,N,K,a_k,b_k,lda,ldb,A", [
+    (129, 136, 1000, False, True, 129, 1000, 4096),   # M-contiguous A, M % 8 != 0
+    (128, 130, 64, True, False, 64, 130, 4096),       # N-contiguous B, N % 8 != 0
+    (128, 128, 60, True, True, 60, 60, 4096),          # K-contiguous operands, K % 8 != 0
+    (128, 128, 64, True, True, 64, 64, 4100),          # A not 16-byte aligned
+])
+def test_kernel_gemm_rejects_unaligned_bf16(M, N, K, a_k, b_k, lda, ldb, A):
+    """bf16 operands are read in 16-byte chunks: a contiguous dimension or
+    leading dimension not a multiple of 8 elements, or a pointer not 16-byte
+    aligned, is an argument error raised before anything is launched."""
+    with pytest.raises(zl.ZlError) as ei:
+        zl.zl_kernel_gemm(M, N, K, A, lda, a_k, 8192, ldb, b_k, 12288, N, zl.ZL_BF16)
+    assert ei.value.status == zl.ZL_ERR_INVALID_ARG and "8-element" in str(ei.value)
+
+
 def test_null_handle_calls_fail_cleanly():
     lib = zl.load()
     assert lib.zl_chunk_forward(None, None, None, None, 1, 1, None, None) == zl.ZL_ERR_INVALID_ARG
