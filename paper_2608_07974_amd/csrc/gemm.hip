@@ -1259,7 +1259,16 @@ static hipError_t run_layout(const GemmDesc& g, const EpiArgs& e, int dtype, hip
   } else {
     const long big = (long)((g.M + 255) / 256) * ((g.N + 255) / 256);
     // the RoPE and delta epilogues need head-aligned wave tiles of 128 columns
-    const bool large = big >= 240 || e.kind == EPI_ROPE || e.kind == EPI_STORE_DELTA;
+    bool large = big >= 240 || e.kind == EPI_ROPE || e.kind == EPI_STORE_DELTA;
+    if (!large && dtype == BF16) {
+      // A long reduction over few, nearly full large tiles (the head's data
+      // gradient with K = V): large tiles split over K to fill the chip move
+      // half the tile bytes per FLOP of 128 x 128 tiles, and each split stays
+      // long enough to amortize its partials.
+      const int nz = splitk_count(g, e, big, KTile<AK, BKM>::BK);
+      large = nz >= 2 && big * nz >= 240 && g.K / nz >= 8192 &&
+              (double)g.M * g.N >= 0.9 * (double)big * 65536.0;
+    }
     const int R = large ? 256 : 128;
     const bool dma = dma_operand_ok(g.A, g.lda, AK, g.M, g.ka, R) &&
                      dma_operand_ok(g.B, g.ldb, BKM, g.N, g.kb, R) &&

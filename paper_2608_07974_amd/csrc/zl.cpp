@@ -453,8 +453,10 @@ static hipError_t run_gemm(zl_chunk* c, hipStream_t s, const GemmDesc& g, const 
   const int pi = c->prof_start(s);
   const char* kn = "gemm";
   GemmDesc gs = g;
-  gs.part = c->plan.spk_elems ? c->at<float>(c->plan.SPK) : nullptr;
-  gs.part_elems = c->plan.spk_elems;
+  if (!gs.part) {
+    gs.part = c->plan.spk_elems ? c->at<float>(c->plan.SPK) : nullptr;
+    gs.part_elems = c->plan.spk_elems;
+  }
   hipError_t err = launch_gemm(gs, e, c->act, s, &kn);
   c->prof_stop(pi, s, kn, 2.0 * g.M * g.N * ((k_alg < 0 ? g.K : k_alg) + g.K2), 0.0);
   return err;
@@ -874,6 +876,12 @@ zl_status zl_local_objective(zl_chunk* c, const int32_t* labels, float* loss_out
     {
       GemmDesc g = gdesc(rows, m.d, p.Vpad, c->ws + p.DZ, p.Vpad, true, c->buf.head_w, m.d, false);
       g.kb = m.V;
+      if (act == BF16) {
+        // the logit cache is free once the objective has formed dZ: it
+        // holds the split-K partials when rows x d is too few tiles
+        g.part = c->at<float>(p.ZC);
+        g.part_elems = (size_t)stk * p.R * p.Vpad * 2 / 4;
+      }
       EpiArgs e = epi(EPI_STORE, c->at<float>(p.DNF), m.d, F32);
       ZL_HIP(run_gemm(c, s, g, e, (double)m.V));
     }

@@ -142,6 +142,41 @@ def test_gemm_split_k(a_k, b_k, M, N, K, K2):
     assert np.array_equal(split, again)
 
 
+@pytest.mark.parametrize("a_k,b_k", [(True, False), (True, True)])
+def test_gemm_long_k_large_tiles_split(a_k, b_k):
+    """A long reduction over few large tiles (the head's data gradient, K = V
+    with rows x d small: here 2048 x 1024 x 65536, 32 tiles of 256 x 256)
+    runs as large tiles split eight ways over K: sampled rows against fp64,
+    the whole output against the unsplit launch, identical on a repeat."""
+    zl = _zl()
+    M, N, K = 2048, 1024, 65536
+    gen = torch.Generator(device=_dev()).manual_seed(5)
+    At = torch.randn((M, K) if a_k else (K, M), device=_dev(), generator=gen).to(torch.bfloat16)
+    Bt = torch.randn((N, K) if b_k else (K, N), device=_dev(), generator=gen).to(torch.bfloat16)
+
+    def run(ws_elems):
+        C = torch.full((M, N), float("nan"), dtype=torch.float32, device=_dev())
+        ws = torch.full((max(ws_elems, 1),), float("nan"), dtype=torch.float32, device=_dev())
+        torch.cuda.synchronize()
+        zl.zl_kernel_gemm(M, N, K, At.data_ptr(), At.shape[1], a_k, Bt.data_ptr(), Bt.shape[1], b_k,
+                          C.data_ptr(), N, zl.ZL_BF16, _stream(),
+                          workspace=ws.data_ptr() if ws_elems else None, workspace_elems=ws_elems)
+        torch.cuda.synchronize()
+        return C
+    one = run(0)
+    split = run(8 * M * N)
+    again = run(8 * M * N)
+    assert bool(torch.isfinite(split).all())
+    assert torch.equal(split, again)
+    assert rel_err(split.cpu().double().numpy(), one.cpu().double().numpy()) < 2e-6
+    rows = np.random.default_rng(3).choice(M, size=48, replace=False)
+    ridx = torch.tensor(rows, device=_dev())
+    a = (At[ridx] if a_k else At[:, ridx].t()).double().cpu().numpy()
+    b = (Bt if b_k else Bt.t()).double().cpu().numpy()
+    ref = a @ b.T
+    assert rel_err(split[ridx].cpu().double().numpy(), ref) < 2e-6
+
+
 def test_gemm_register_staged_path_with_second_segment():
     """Both operands MN-major with A's row stride 16384 and K = 66000: A's
     tile offsets pass 2^31 bytes, so the direct-to-LDS kernel is not used and
