@@ -376,28 +376,11 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[BM / WM / 32][B
     } else if (e.kind == EPI_LOGITS) {
       // 8 lanes cover a 64-column block of one row (64 % EW == 0, TN % 64 == 0)
       static_assert(TN % 64 == 0, "logit statistics need 64-column blocks");
-      for (int t = lane; t < 32 * QPR; t += 64) {
-        const int row = t / QPR, col = (t % QPR) * EW;
-        const int m = mb + row, n = nb + col;
-        float v[EW], w[EW];
-#pragma unroll
-        for (int k = 0; k < EW; k += 4) {
-          const float4 x = *reinterpret_cast<const float4*>(&ep[row * LDW + col + k]);
-          v[k] = x.x; v[k + 1] = x.y; v[k + 2] = x.z; v[k + 3] = x.w;
-          float4 y = make_float4(0.f, 0.f, 0.f, 0.f);
-          if (e.pair) y = *reinterpret_cast<const float4*>(&ep[(row ^ 1) * LDW + col + k]);
-          w[k] = x.x - y.x; w[k + 1] = x.y - y.y; w[k + 2] = x.z - y.z; w[k + 3] = x.w - y.w;
-        }
-        epilogue_v(e, g.M, g.N, m, n, v, vec);
-        // the label's logit of a z row, in fp32 (the cache may be fp16)
-        if (e.zy && m < g.M && !(e.pair && (m & 1))) {
-          const int tok = e.pair ? m >> 1 : m;
-          const int y = e.lab[tok];
-#pragma unroll
-          for (int k = 0; k < EW; ++k)
-            if (y == n + k) e.zy[tok] = v[k];
-        }
-        // block maximum first (8 lanes), then one exponential per logit
+      // Softmax partials of one row's 64-column block: the block maximum,
+      // then one exponential per logit (exp2 of a fused multiply-add).
+      auto block_stats = [&](const int m, const int n, const float (&v)[EW], const float (&w)[EW])
+          __attribute__((always_inline)) {
+        constexpr float L2E = 1.4426950408889634f;
         float mx = -INFINITY;
 #pragma unroll
         for (int k = 0; k < EW; ++k) mx = n + k < g.N ? fmaxf(mx, v[k]) : mx;
@@ -405,9 +388,10 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[BM / WM / 32][B
         for (int off = 1; off < 64 / EW; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
         SoftPart sp = {mx, 0.f, 0.f};
         if (mx != -INFINITY) {
+          const float nm = -mx * L2E;
 #pragma unroll
           for (int k = 0; k < EW; ++k) {
-            const float p = n + k < g.N ? __expf(v[k] - mx) : 0.f;
+            const float p = n + k < g.N ? __builtin_amdgcn_exp2f(__builtin_fmaf(v[k], L2E, nm)) : 0.f;
             sp.s += p;
             sp.e += p * w[k];
           }
@@ -419,6 +403,59 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[BM / WM / 32][B
         }
         if ((lane & (64 / EW - 1)) == 0 && m < g.M && n < g.N)
           e.stats[(int64_t)m * e.ldst + n / 64] = make_float4(sp.m, sp.s, sp.e, 0.f);
+      };
+      // the label's logit of a z row, in fp32 (the cache may be fp16)
+      auto label_logit = [&](const int m, const int n, const float (&v)[EW])
+          __attribute__((always_inline)) {
+        if (e.zy && m < g.M) {
+          const int tok = e.pair ? m >> 1 : m;
+          const int y = e.lab[tok];
+#pragma unroll
+          for (int k = 0; k < EW; ++k)
+            if (y == n + k) e.zy[tok] = v[k];
+        }
+      };
+      if (e.pair) {
+        // z rows are even and their z' rows follow (mb is even): a lane takes
+        // both rows of its columns, so each staged value is read once and
+        // z - z' is formed once
+        static_assert((16 * QPR) % 64 == 0, "row pairs must divide over the lanes");
+        for (int t = lane; t < 16 * QPR; t += 64) {
+          const int row = 2 * (t / QPR), col = (t % QPR) * EW;
+          const int m = mb + row, n = nb + col;
+          float v[EW], u[EW], w[EW], wn[EW];
+#pragma unroll
+          for (int k = 0; k < EW; k += 4) {
+            const float4 x = *reinterpret_cast<const float4*>(&ep[row * LDW + col + k]);
+            const float4 y = *reinterpret_cast<const float4*>(&ep[(row + 1) * LDW + col + k]);
+            v[k] = x.x; v[k + 1] = x.y; v[k + 2] = x.z; v[k + 3] = x.w;
+            u[k] = y.x; u[k + 1] = y.y; u[k + 2] = y.z; u[k + 3] = y.w;
+          }
+#pragma unroll
+          for (int k = 0; k < EW; ++k) {
+            w[k] = v[k] - u[k];
+            wn[k] = -w[k];
+          }
+          epilogue_v(e, g.M, g.N, m, n, v, vec);
+          epilogue_v(e, g.M, g.N, m + 1, n, u, vec);
+          label_logit(m, n, v);
+          block_stats(m, n, v, w);
+          block_stats(m + 1, n, u, wn);
+        }
+      } else {
+        for (int t = lane; t < 32 * QPR; t += 64) {
+          const int row = t / QPR, col = (t % QPR) * EW;
+          const int m = mb + row, n = nb + col;
+          float v[EW];
+#pragma unroll
+          for (int k = 0; k < EW; k += 4) {
+            const float4 x = *reinterpret_cast<const float4*>(&ep[row * LDW + col + k]);
+            v[k] = x.x; v[k + 1] = x.y; v[k + 2] = x.z; v[k + 3] = x.w;
+          }
+          epilogue_v(e, g.M, g.N, m, n, v, vec);
+          label_logit(m, n, v);
+          block_stats(m, n, v, v);
+        }
       }
     } else {
       for (int t = lane; t < 32 * QPR; t += 64) {
