@@ -238,6 +238,25 @@ __device__ __forceinline__ void epilogue_v(const EpiArgs& e, int M, int N, int m
   }
 }
 
+// Reductions over aligned groups of 8 lanes with DPP moves, no LDS
+// traffic: the partner across lane bit 0, then bit 1 (quad permutations),
+// then the mirrored lane of the other quad of the 8 (row_half_mirror).
+// Every lane of the group ends with the same value.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float max8(float x) {
+  x = fmaxf(x, dpp_f32<0xB1>(x));   // quad_perm [1, 0, 3, 2]
+  x = fmaxf(x, dpp_f32<0x4E>(x));   // quad_perm [2, 3, 0, 1]
+  return fmaxf(x, dpp_f32<0x141>(x));
+}
+__device__ __forceinline__ float sum8(float x) {
+  x += dpp_f32<0xB1>(x);
+  x += dpp_f32<0x4E>(x);
+  return x + dpp_f32<0x141>(x);
+}
+
 // Online-softmax partials (max, sum exp(x - max), sum exp(x - max) w).
 struct SoftPart { float m, s, e; };
 
@@ -384,8 +403,8 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[BM / WM / 32][B
         float mx = -INFINITY;
 #pragma unroll
         for (int k = 0; k < EW; ++k) mx = n + k < g.N ? fmaxf(mx, v[k]) : mx;
-#pragma unroll
-        for (int off = 1; off < 64 / EW; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+        static_assert(64 / EW == 8, "a 64-column block spans 8 lanes");
+        mx = max8(mx);
         SoftPart sp = {mx, 0.f, 0.f};
         if (mx != -INFINITY) {
           const float nm = -mx * L2E;
@@ -396,11 +415,8 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[BM / WM / 32][B
             sp.e += p * w[k];
           }
         }
-#pragma unroll
-        for (int off = 1; off < 64 / EW; off <<= 1) {
-          sp.s += __shfl_xor(sp.s, off, 64);
-          sp.e += __shfl_xor(sp.e, off, 64);
-        }
+        sp.s = sum8(sp.s);
+        sp.e = sum8(sp.e);
         if ((lane & (64 / EW - 1)) == 0 && m < g.M && n < g.N)
           e.stats[(int64_t)m * e.ldst + n / 64] = make_float4(sp.m, sp.s, sp.e, 0.f);
       };
