@@ -79,7 +79,7 @@ __device__ __forceinline__ void epilogue(const EpiArgs& e, int M, int N, int m, 
     case EPI_SWIGLU_BWD: {
       float g = ld_act(e.aux, e.out_dtype, mo * e.ldaux + n);
       float u = ld_act(e.aux, e.out_dtype, mo * e.ldaux + n + e.ff);
-      float sg = 1.f / (1.f + __expf(-g));
+      float sg = __builtin_amdgcn_rcpf(1.f + __expf(-g));  // hardware reciprocal (1 ulp)
       float silu = g * sg;
       float dsilu = sg * (1.f + g * (1.f - sg));
       st_act(e.out, e.out_dtype, mo * e.ldo + n, acc * u * dsilu);
@@ -213,7 +213,7 @@ __device__ __forceinline__ void epilogue_v(const EpiArgs& e, int M, int N, int m
       ldv_act(e.aux, e.out_dtype, mo * e.ldaux + n + e.ff, u);
 #pragma unroll
       for (int i = 0; i < EW; ++i) {
-        const float sg = 1.f / (1.f + __expf(-g[i]));
+        const float sg = __builtin_amdgcn_rcpf(1.f + __expf(-g[i]));  // hardware reciprocal (1 ulp)
         const float silu = g[i] * sg;
         const float dsilu = sg * (1.f + g[i] * (1.f - sg));
         v[i] = a[i] * u[i] * dsilu;
