@@ -20,6 +20,47 @@ def current_stream():
     return torch.cuda.current_stream().cuda_stream
 
 
+def _check_int_tensor(name, t, device, numel):
+    if t.dtype != torch.int32 or not t.is_contiguous():
+        raise TypeError(f"{name} must be a contiguous int32 tensor")
+    if t.device != device:
+        raise ValueError(f"{name} must be on {device}, not {t.device}")
+    if numel is not None and t.numel() != numel:
+        raise ValueError(f"{name} must hold {numel} elements, not {t.numel()}")
+
+
+def check_batch(dtype, d_model, device, h_in, seq_lens=None, pos_ids=None, labels=None,
+                h_out=None, max_batch=None, max_seq=None):
+    """Raises before any pointer reaches libzl when a tensor does not match
+    what the kernels read: h_in a contiguous [B, S, d_model] tensor of the
+    chunk's dtype on `device`; seq_lens B, pos_ids and labels B*S int32
+    elements on the same device; h_out like h_in.  The kernels index these
+    buffers by B and S alone, so a short or host-side tensor would be read
+    out of bounds on the GPU."""
+    device = torch.device(device)
+    if device.type == "cuda" and device.index is None:
+        device = torch.device("cuda", torch.cuda.current_device())
+    if h_in.dtype != dtype or not h_in.is_contiguous() or h_in.dim() != 3:
+        raise TypeError(f"h_in must be a contiguous [B, S, d] {dtype} tensor")
+    if h_in.device != device:
+        raise ValueError(f"h_in must be on {device}, not {h_in.device}")
+    B, S, d = h_in.shape
+    if d != d_model:
+        raise ValueError(f"h_in's last dimension is {d}, the chunk's d_model is {d_model}")
+    if B < 1 or S < 1 or (max_batch is not None and B > max_batch) or \
+            (max_seq is not None and S > max_seq):
+        raise ValueError(f"B = {B}, S = {S} outside [1, {max_batch}] x [1, {max_seq}]")
+    for name, t, n in (("seq_lens", seq_lens, B), ("pos_ids", pos_ids, B * S),
+                       ("labels", labels, B * S)):
+        if t is not None:
+            _check_int_tensor(name, t, device, n)
+    if h_out is not None:
+        if h_out.dtype != dtype or h_out.shape != h_in.shape or not h_out.is_contiguous():
+            raise TypeError("h_out must match h_in in shape and dtype and be contiguous")
+        if h_out.device != device:
+            raise ValueError(f"h_out must be on {device}, not {h_out.device}")
+
+
 def config_from_shape(shp, alpha=0.5, consis="reverse", optimizer="adamw", lr=1e-4, wd=0.01,
                       max_batch=None, max_seq=None):
     """zl_config for a workload shape (arch, widths, dtype) and objective."""
@@ -79,6 +120,7 @@ class TorchChunk:
                              _ptr(self.head_norm_w), _ptr(self.head_norm_b),
                              _ptr(self.base_master), _ptr(self.base_shadow))
         self.handle = zl.zl_chunk_create(cfg, bufs, self.ws_ptr, self.ws_bytes)
+        self._tokens = None  # B*S of the last forward (labels must match it)
         self.by_key = {f"L{t['layer']}.{t['name']}": t for t in self.layout}
         self.base_by_key = {f"L{t['layer']}.{t['name']}": t for t in self.base_layout}
 
@@ -124,17 +166,13 @@ class TorchChunk:
 
     # ------------------------------------------------------------ update
     def _check_inputs(self, h_in, seq_lens=None, pos_ids=None, labels=None, h_out=None):
-        if h_in.dtype != self.dtype or not h_in.is_contiguous() or h_in.dim() != 3:
-            raise TypeError(f"h_in must be a contiguous [B, S, d] {self.dtype} tensor")
-        for name, t in (("seq_lens", seq_lens), ("pos_ids", pos_ids), ("labels", labels)):
-            if t is not None and (t.dtype != torch.int32 or not t.is_contiguous()):
-                raise TypeError(f"{name} must be a contiguous int32 tensor")
-        if h_out is not None and (h_out.dtype != self.dtype or h_out.shape != h_in.shape):
-            raise TypeError("h_out must match h_in in shape and dtype")
+        check_batch(self.dtype, self.cfg.d_model, self.device, h_in, seq_lens, pos_ids, labels,
+                    h_out, max_batch=self.cfg.max_batch, max_seq=self.cfg.max_seq)
 
     def forward(self, h_in, seq_lens=None, pos_ids=None, h_out=None):
         self._check_inputs(h_in, seq_lens, pos_ids, None, h_out)
         B, S, _ = h_in.shape
+        self._tokens = B * S
         if h_out is None:
             h_out = torch.empty_like(h_in)
         zl.zl_chunk_forward(self.handle, _ptr(h_in), _ptr(seq_lens), _ptr(pos_ids), B, S,
@@ -142,8 +180,9 @@ class TorchChunk:
         return h_out
 
     def objective(self, labels):
-        if labels.dtype != torch.int32 or not labels.is_contiguous():
-            raise TypeError("labels must be a contiguous int32 tensor")
+        _check_int_tensor("labels", labels, self.device, None)
+        if self._tokens is not None and labels.numel() != self._tokens:
+            raise ValueError(f"labels must hold B*S = {self._tokens} elements")
         zl.zl_local_objective(self.handle, _ptr(labels), _ptr(self.loss), current_stream())
         return self.loss
 

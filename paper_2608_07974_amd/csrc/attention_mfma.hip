@@ -14,8 +14,9 @@
 //  - dK/dV: one workgroup per (128 keys, kv-head), walking every q-head of
 //    its group and every later query tile (no cross-workgroup reduction).
 //  - dQ: one workgroup per (128 queries, q-head).
-// Tiles of 64 rows are staged through registers into double-buffered LDS
-// (16-byte chunks XOR-swizzled by row) so global loads overlap the MFMAs.
+// Tiles of 64 rows are copied global -> LDS by the buffer unit
+// (buffer_load ... lds, no staging registers) into double-buffered LDS,
+// 16-byte chunks XOR-swizzled by row, so the copies overlap the MFMAs.
 // Operands needed transposed are read from the same row-major tiles with
 // ds_read_b64_tr_b16: within each 16-lane group, lane r addresses row
 // q0 + r/4, columns d0 + 4 (r % 4) .. +3, and lane i receives column d0 + i
@@ -65,33 +66,6 @@ __device__ inline float max_xor32(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
   return fmaxf(__builtin_bit_cast(float, r[0]), __builtin_bit_cast(float, r[1]));
 }
-
-// A 64 x HD tile staged global -> registers -> LDS (row-major, swizzled).
-template <int HD>
-struct TileStage {
-  static constexpr int CH = HD / 8;                 // 16-byte chunks per row
-  static constexpr int PER = BT * CH / NTH;         // chunks per thread
-  uint4 r[PER];
-  __device__ inline void load(const bf16_t* G, int64_t ld, int64_t rowbase, int row0,
-                              int nvalid, int64_t col0) {
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int c = threadIdx.x + i * NTH;
-      const int row = c / CH, ch = c % CH;
-      const int t = row0 + row;
-      r[i] = t < nvalid ? *reinterpret_cast<const uint4*>(G + (rowbase + t) * ld + col0 + ch * 8)
-                        : make_uint4(0, 0, 0, 0);
-    }
-  }
-  __device__ inline void store(bf16_t* lds) const {
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int c = threadIdx.x + i * NTH;
-      const int row = c / CH, ch = c % CH;
-      *reinterpret_cast<uint4*>(lds + row * HD + ((ch ^ swz<HD>(row)) * 8)) = r[i];
-    }
-  }
-};
 
 // 8 consecutive bf16 of row `row`, 16-byte chunk `ch`.
 template <int HD>

@@ -5,7 +5,7 @@ every step runs in libzl."""
 import torch
 
 from . import zl
-from .chunk import TorchChunk, current_stream
+from .chunk import TorchChunk, check_batch, current_stream
 
 
 class Pipeline:
@@ -36,14 +36,18 @@ class Pipeline:
 
     def submit(self, h0, labels, pos_ids=None, seq_lens=None, losses=None):
         """Queue one micro-batch through all stages; returns (mb, losses[K])."""
-        if h0.dtype != self.dtype or not h0.is_contiguous() or h0.dim() != 3:
-            raise TypeError(f"h0 must be a contiguous [B, S, d] {self.dtype} tensor")
-        for name, t in (("labels", labels), ("pos_ids", pos_ids), ("seq_lens", seq_lens)):
-            if t is not None and (t.dtype != torch.int32 or not t.is_contiguous()):
-                raise TypeError(f"{name} must be a contiguous int32 tensor")
+        c0 = self.chunks[0]
+        if labels is None:
+            raise ValueError("labels are required")
+        check_batch(self.dtype, c0.cfg.d_model, c0.device, h0, seq_lens, pos_ids, labels,
+                    max_batch=c0.cfg.max_batch, max_seq=c0.cfg.max_seq)
         B, S, _ = h0.shape
         if losses is None:
             losses = torch.zeros(self.K, dtype=torch.float32, device=h0.device)
+        elif (losses.dtype != torch.float32 or not losses.is_contiguous()
+              or losses.numel() < self.K or losses.device != h0.device):
+            raise ValueError(f"losses must be a contiguous float32 tensor of {self.K} elements "
+                             f"on {h0.device}")
         # stage 0 copies its inputs on its own stream: order it after the
         # caller's stream (the inputs were produced there)
         ev = torch.cuda.Event()
