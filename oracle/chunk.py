@@ -55,7 +55,19 @@ class OracleConfig:
     adapter_rank: int = 0
     lora_rank: int = 0
     lora_alpha: float = 16.0
+    # Reading r4 (the bf16 storage floor): when set, every intermediate that a
+    # bf16 implementation keeps in bf16 between steps (norm outputs, q/k/v
+    # after RoPE, the attention output, MLP pre-activations and activation,
+    # the residual-stream gradient as a matrix operand, data gradients, the
+    # head's normalised rows and dL/dz) is rounded to bf16 where it is
+    # stored, the arithmetic staying fp64.  Off by default; it exists only to
+    # measure how far bf16 storage alone moves each result.
+    store_bf16: bool = False
     extra: dict = field(default_factory=dict)
+
+    def st(self, x):
+        """x as stored between steps: bf16-rounded under store_bf16."""
+        return bf16_round(x) if self.store_bf16 else x
 
     @property
     def lora_scale(self):
@@ -156,7 +168,8 @@ def chunk_grads_ref(cfg, params, h_in, labels, head_w, head_norm_w, head_norm_b=
         h_out.reshape(B * S, d), fw["h_in"].reshape(B * S, d), np.asarray(labels).reshape(-1),
         W, cfg.arch, np.asarray(head_norm_w, np.float64),
         None if head_norm_b is None else np.asarray(head_norm_b, np.float64),
-        cfg.norm_eps, cfg.alpha, cfg.consis, adapter=adapter)
+        cfg.norm_eps, cfg.alpha, cfg.consis, adapter=adapter,
+        store=cfg.st if cfg.store_bf16 else None)
     _, grads = chunk_backward_ref(cfg, dh.reshape(B, S, d), fw, need_dx=False)
     if adapter is not None:
         pre = f"L{cfg.n_layers}."

@@ -113,48 +113,74 @@ def loss_and_dlogits(z, zp, labels, alpha, consis):
     return loss, dz, dict(ce=ce, kl=kl, n_omega=n_omega)
 
 
-def adapter_fwd(h, w1, w2):
+def _keep(x):
+    return x
+
+
+def _block_fp16(z, width=64):
+    """z kept as fp16 offsets from the maximum of each row's 64-column block
+    (measuring the storage floor only)."""
+    out = np.empty_like(z)
+    for c0 in range(0, z.shape[1], width):
+        blk = z[:, c0:c0 + width]
+        m = np.max(blk, axis=1, keepdims=True)
+        out[:, c0:c0 + width] = m + (blk - m).astype(np.float16).astype(np.float64)
+    return out
+
+
+def adapter_fwd(h, w1, w2, st=_keep):
     """Readout adapter (Sec. III-B, Local Update interface (b)): a residual
     MLP h' = h + gelu(h W1^T) W2^T, W1 [r, d], W2 [d, r], that is the
-    identity when W2 = 0."""
-    u = h @ w1.T
-    a = ops.gelu_fwd(u)
-    return h + a @ w2.T, (h, u, a, w1, w2)
+    identity when W2 = 0.  st: how stored intermediates are kept (exact by
+    default; bf16 rounding when the storage floor is measured)."""
+    hs = st(h)
+    u = st(hs @ w1.T)
+    a = st(ops.gelu_fwd(u))
+    return h + a @ w2.T, (hs, u, a, w1, w2)
 
 
-def adapter_bwd(dhp, cache):
+def adapter_bwd(dhp, cache, st=_keep):
     """dL/dh and the weight gradients from dL/dh'."""
     h, u, a, w1, w2 = cache
-    du = ops.gelu_bwd(dhp @ w2, u)
-    return dhp + du @ w1, dict(w1=du.T @ h, w2=dhp.T @ a)
+    dhs = st(dhp)
+    du = st(ops.gelu_bwd(dhs @ w2, u))
+    return dhp + du @ w1, dict(w1=du.T @ h, w2=dhs.T @ a)
 
 
 def local_objective_ref(h_out, h_in, labels, head_w, arch, hn_w, hn_b, eps,
-                        alpha, consis="reverse", adapter=None):
+                        alpha, consis="reverse", adapter=None, store=None):
     """Loss and dL/dh_out for one micro-batch.  h_* [T, d], labels [T].
 
     h_in enters only through the stop-gradient readout; no gradient to it is
     formed.  adapter: optional (W1, W2); h_out is read out through it, the
     consistency target from h_in is the static head's readout.  The adapter
-    weight gradients are returned in info["adapter_grads"].
+    weight gradients are returned in info["adapter_grads"].  store: optional
+    rounding of the stored intermediates (the normalised rows the head reads
+    and dL/dz), used only to measure the bf16 storage floor.
     """
+    st = _keep if store is None else store
     h_out = np.asarray(h_out, np.float64)
     W = np.asarray(head_w, np.float64)
     ad_cache = None
     if adapter is not None:
         h_out, ad_cache = adapter_fwd(h_out, np.asarray(adapter[0], np.float64),
-                                      np.asarray(adapter[1], np.float64))
+                                      np.asarray(adapter[1], np.float64), st)
     n, c = head_norm_fwd(h_out, arch, hn_w, hn_b, eps)
-    z = n @ W.T
+    z = st(n) @ W.T
     zp = None
     if alpha < 1.0:
         n_in, _ = head_norm_fwd(np.asarray(h_in, np.float64), arch, hn_w, hn_b, eps)
-        zp = n_in @ W.T
+        zp = st(n_in) @ W.T
     loss, dz, rows = loss_and_dlogits(z, zp, np.asarray(labels).reshape(-1), alpha, consis)
-    dn = dz @ W
+    if store is not None:
+        # the logits as cached for dL/dz: fp16 values of z minus the maximum
+        # of their 64-column block; the loss keeps its exact statistics
+        _, dz, _ = loss_and_dlogits(_block_fp16(z), None if zp is None else _block_fp16(zp),
+                                    np.asarray(labels).reshape(-1), alpha, consis)
+    dn = st(dz) @ W
     dh = head_norm_bwd(dn, arch, c)
     info = dict(z=z, zp=zp, dz=dz, **rows)
     if ad_cache is not None:
         info["dh_adapted"] = dh
-        dh, info["adapter_grads"] = adapter_bwd(dh, ad_cache)
+        dh, info["adapter_grads"] = adapter_bwd(dh, ad_cache, st)
     return loss, dh, info

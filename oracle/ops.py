@@ -81,12 +81,18 @@ def attention_mask(B, S, seq_lens):
     return m
 
 
-def attention_fwd(q, k, v, seq_lens):
+def _exact(x):
+    return x
+
+
+def attention_fwd(q, k, v, seq_lens, st=None):
     """Causal GQA attention; q [B,S,Hq,hd], k,v [B,S,Hkv,hd].
 
     q-head h reads kv-head h // (Hq/Hkv).  Scores q.k / sqrt(hd).  A query
-    with no allowed key gets output 0.
+    with no allowed key gets output 0.  st (measuring the bf16 storage
+    floor only): how the probabilities are kept as the operand of P V.
     """
+    st = _exact if st is None else st
     B, S, Hq, hd = q.shape
     Hkv = k.shape[2]
     grp = Hq // Hkv
@@ -105,12 +111,14 @@ def attention_fwd(q, k, v, seq_lens):
             den = np.sum(e, axis=-1, keepdims=True)
             p = np.where(den > 0, e / np.where(den > 0, den, 1.0), 0.0)
             P[b, h] = p
-            o[b, :, h, :] = p @ v[b, :, g, :]
-    return o, (q, k, v, P)
+            o[b, :, h, :] = st(p) @ v[b, :, g, :]
+    return o, (q, k, v, P, st)
 
 
 def attention_bwd(do, cache):
-    q, k, v, P = cache
+    """st of the forward (if any) also keeps P as the operand of P^T dO and
+    dS as the operand of dS K and dS^T Q."""
+    q, k, v, P, st = cache
     B, S, Hq, hd = q.shape
     Hkv = k.shape[2]
     grp = Hq // Hkv
@@ -122,9 +130,9 @@ def attention_bwd(do, cache):
         for h in range(Hq):
             g = h // grp
             p = P[b, h]
-            dv[b, :, g, :] += p.T @ do[b, :, h, :]
+            dv[b, :, g, :] += st(p).T @ do[b, :, h, :]
             dp = do[b, :, h, :] @ v[b, :, g, :].T
-            ds = p * (dp - np.sum(dp * p, axis=-1, keepdims=True))
+            ds = st(p * (dp - np.sum(dp * p, axis=-1, keepdims=True)))
             dq[b, :, h, :] = (ds @ k[b, :, g, :]) * scale
             dk[b, :, g, :] += (ds.T @ q[b, :, h, :]) * scale
     return dq, dk, dv
