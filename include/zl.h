@@ -87,15 +87,19 @@ typedef struct zl_config {
                         (W2 = 0 makes the adapter the identity).             */
   int lora_rank;     /* LoRA rank r (Sec. II.A: Delta w_l = B_l A_l on the
                         frozen w_l, trained by Eq. (6)); 0 = the whole chunk
-                        is trainable.  Else a multiple of 8 up to 256: every
-                        linear (llama wq wk wv wo wg wu wd, gpt2 wqkv wo wfc
-                        wproj) computes y = x W^T (+ b) + s (x A^T) B^T with
-                        s = lora_alpha / r; W, norms and biases are frozen and
-                        read from base_master / base_shadow; the trainable set
-                        is the factors A [r, in], B [out, r] (and the readout
-                        adapter).  A smaller rank q runs as r = 8 with rows
-                        q.. of A and columns q.. of B zero (they stay zero
-                        under SGD and AdamW) and lora_alpha scaled by 8 / q. */
+                        is trainable.  Else 1..256: every linear (llama wq wk
+                        wv wo wg wu wd, gpt2 wqkv wo wfc wproj) computes
+                        y = x W^T (+ b) + s (x A^T) B^T with s = lora_alpha /
+                        r; W, norms and biases are frozen and read from
+                        base_master / base_shadow; the trainable set is the
+                        factors A [r, in], B [out, r] (and the readout
+                        adapter).  The factors are stored r8 = r rounded up
+                        to a multiple of 8 wide (A [r8, in], B [out, r8], the
+                        shapes zl_param_layout reports); rows r.. of A and
+                        columns r.. of B are padding, which zl_refresh_shadow
+                        sets to zero and which then stays zero: its gradient
+                        is exactly zero, so neither SGD nor AdamW moves it,
+                        and the result is that of rank r.                  */
   float lora_alpha;  /* s = lora_alpha / lora_rank; > 0 when lora_rank > 0  */
 } zl_config;
 
@@ -171,9 +175,10 @@ zl_status zl_chunk_create(const zl_config* cfg, const zl_buffers* bufs,
 void zl_chunk_destroy(zl_chunk* chunk);
 
 /* Writes the bf16 shadow from the fp32 master (round to nearest even), and
- * with lora_rank > 0 also base_shadow from base_master.  Call after
- * initialising or loading master (or the base) in ZL_BF16 mode; a no-op for
- * ZL_F32. */
+ * with lora_rank > 0 also base_shadow from base_master.  With a lora_rank
+ * that is not a multiple of 8 it first zeroes the padding of the stored
+ * factors in master (see zl_config.lora_rank).  Call after initialising or
+ * loading master (or the base), in either dtype. */
 zl_status zl_refresh_shadow(zl_chunk* chunk, void* stream);
 
 /* Forward-and-Output (Sec. III-B; Eq. (1)).  h_in and h_out are [B, S, d]

@@ -35,6 +35,20 @@ typedef struct zl_view {
  *   "dh_out"   fp32 dL/dh_out after zl_local_objective            [T, d]
  *   "row_loss" fp32 per-token loss terms (0 outside Omega)        [T, 1]
  *   "n_omega"  fp32 |Omega|                                        [1, 1]
+ * After zl_local_objective, of the head's last row block (R = min(T, 4096)
+ * rows, or fewer when T is not a multiple of R; Vp = vocab rounded up to 8):
+ *   "dz"       dL/dz in the activation dtype                       [R, Vp]
+ *   "dnf"      fp32 dL/dz W_lm, the head's data gradient before its
+ *              norm backward                                       [R, d]
+ * After zl_chunk_backward, the operands of layer 0's weight gradients (the
+ * backward's scratch, left by the last layer it processed), activation dtype:
+ *   "dxa"      dL/d(layer output), the down projection's dy        [T, d]
+ *   "dup"      dL/d(gate|up) (fc) pre-activations                   [T, 2ff or ff]
+ *   "dxb"      dL/d(x2), the output projection's dy                [T, d]
+ *   "do"       dL/d(attention output)                              [T, hq*hd]
+ *   "dqkv"     dL/d(q|k|v projections), the rotation undone        [T, (hq+2hkv)*hd]
+ *   "dn"       fp32 dL/d(n1) = dqkv W_qkv, the norm-1 backward's input [T, d]
+ *              (layer 0 of a LoRA chunk skips it: then left by layer 1) 
  * Pointers are device pointers into the workspace; do not write them. */
 zl_status zl_inspect(const zl_chunk* chunk, const char* name, int layer, zl_view* out);
 

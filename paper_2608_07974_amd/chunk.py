@@ -20,6 +20,14 @@ def current_stream():
     return torch.cuda.current_stream().cuda_stream
 
 
+def _norm_device(device):
+    """torch.device with the index filled in ("cuda" -> the current GPU)."""
+    device = torch.device(device)
+    if device.type == "cuda" and device.index is None:
+        device = torch.device("cuda", torch.cuda.current_device())
+    return device
+
+
 def _check_int_tensor(name, t, device, numel):
     if t.dtype != torch.int32 or not t.is_contiguous():
         raise TypeError(f"{name} must be a contiguous int32 tensor")
@@ -37,9 +45,7 @@ def check_batch(dtype, d_model, device, h_in, seq_lens=None, pos_ids=None, label
     elements on the same device; h_out like h_in.  The kernels index these
     buffers by B and S alone, so a short or host-side tensor would be read
     out of bounds on the GPU."""
-    device = torch.device(device)
-    if device.type == "cuda" and device.index is None:
-        device = torch.device("cuda", torch.cuda.current_device())
+    device = _norm_device(device)
     if h_in.dtype != dtype or not h_in.is_contiguous() or h_in.dim() != 3:
         raise TypeError(f"h_in must be a contiguous [B, S, d] {dtype} tensor")
     if h_in.device != device:
@@ -85,7 +91,7 @@ class TorchChunk:
     def __init__(self, cfg, device="cuda", head=None):
         zl.load()
         self.cfg = cfg
-        self.device = torch.device(device)
+        self.device = _norm_device(device)
         self.dtype = _TORCH_DT[cfg.dtype]
         self.n_params, self.layout = zl.zl_param_layout(cfg)
         dev = self.device
@@ -137,16 +143,41 @@ class TorchChunk:
 
     # ------------------------------------------------------------ params
     def view(self, buf, key):
+        """A trainable tensor as stored (LoRA factors of a rank that is not a
+        multiple of 8 include their zero padding)."""
         t = self.by_key[key]
         return buf[t["offset"]: t["offset"] + t["numel"]].view(*t["shape"])
 
+    def logical(self, buf, key):
+        """A trainable tensor at its configured shape (LoRA factors without
+        their padding: A [r, in], B [out, r])."""
+        v = self.view(buf, key)
+        r = self.cfg.lora_rank
+        if key.endswith("_la"):
+            return v[:r]
+        if key.endswith("_lb"):
+            return v[:, :r]
+        return v
+
+    def padding(self, buf, key):
+        """The padding of a stored LoRA factor (empty for other tensors)."""
+        v = self.view(buf, key)
+        r = self.cfg.lora_rank
+        if key.endswith("_la"):
+            return v[r:]
+        if key.endswith("_lb"):
+            return v[:, r:]
+        return v[:0]
+
     def load_params(self, params):
-        """Trainable tensors by key into master; with LoRA, frozen base
-        tensors (keys of the base layout) into base_master."""
+        """Trainable tensors by key into master (at their configured shape;
+        the padding of stored LoRA factors is zeroed by zl_refresh_shadow);
+        with LoRA, frozen base tensors (keys of the base layout) into
+        base_master."""
         for key, val in params.items():
             src = torch.as_tensor(np.asarray(val, np.float32))
             if key in self.by_key:
-                self.view(self.master, key).copy_(src)
+                self.logical(self.master, key).copy_(src)
             elif key in self.base_by_key:
                 t = self.base_by_key[key]
                 self.base_master[t["offset"]: t["offset"] + t["numel"]].view(*t["shape"]).copy_(src)
@@ -161,8 +192,9 @@ class TorchChunk:
             self.head_norm_b.copy_(torch.as_tensor(np.asarray(head_norm_b, np.float32)))
 
     def tensors(self, buf):
+        """Every trainable tensor of `buf` at its configured shape, float64."""
         torch.cuda.synchronize(self.device)
-        return {k: self.view(buf, k).detach().cpu().double().numpy() for k in self.by_key}
+        return {k: self.logical(buf, k).detach().cpu().double().numpy() for k in self.by_key}
 
     # ------------------------------------------------------------ update
     def _check_inputs(self, h_in, seq_lens=None, pos_ids=None, labels=None, h_out=None):
@@ -209,16 +241,22 @@ class TorchChunk:
         """Load a checkpoint; returns its (microbatches, windows) progress."""
         return zl.zl_chunk_load(self.handle, path, current_stream())
 
-    def inspect(self, name, layer=0):
-        """Copy of a workspace view as a float64 numpy array."""
+    def inspect_device(self, name, layer=0):
+        """A workspace view as a [rows, cols] device tensor (no copy; valid
+        until the next call that rewrites the workspace; read only)."""
         v = zl.zl_inspect(self.handle, name, layer)
-        torch.cuda.synchronize(self.device)
         dt = torch.bfloat16 if v["dtype"] == zl.ZL_BF16 else torch.float32
         esz = 2 if dt == torch.bfloat16 else 4
         n = v["rows"] * v["ld"]
-        raw = torch.empty(n, dtype=dt, device=self.device)
-        # view the workspace bytes at v["ptr"] through the owning tensor
+        # the workspace bytes at v["ptr"], through the owning tensor
         off = v["ptr"] - self._ws.data_ptr()
+        if off < 0 or off + n * esz > self._ws.numel():
+            raise ValueError(f"view {name} lies outside the workspace")
         src = self._ws[off: off + n * esz].view(dt)
-        raw.copy_(src)
-        return raw.view(v["rows"], v["ld"])[:, : v["cols"]].double().cpu().numpy()
+        return src.view(v["rows"], v["ld"])[:, : v["cols"]]
+
+    def inspect(self, name, layer=0):
+        """Copy of a workspace view as a float64 numpy array."""
+        t = self.inspect_device(name, layer)
+        torch.cuda.synchronize(self.device)
+        return t.double().cpu().numpy()

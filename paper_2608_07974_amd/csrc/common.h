@@ -257,5 +257,9 @@ struct OptDesc {
 };
 hipError_t launch_optimizer(const OptDesc& o, hipStream_t s);
 hipError_t launch_shadow(const float* master, bf16_t* shadow, size_t n, hipStream_t s);
+// Zeroes rows [r0, r1) x columns [c0, c1) of a row-major fp32 matrix with row
+// stride ld.
+hipError_t launch_zero_block(float* p, int64_t ld, int64_t r0, int64_t r1, int64_t c0, int64_t c1,
+                             hipStream_t s);
 
 }  // namespace zl

@@ -395,16 +395,34 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[BM / WM / 32][B
     } else if (e.kind == EPI_LOGITS) {
       // 8 lanes cover a 64-column block of one row (64 % EW == 0, TN % 64 == 0)
       static_assert(TN % 64 == 0, "logit statistics need 64-column blocks");
-      // Softmax partials of one row's 64-column block: the block maximum,
-      // then one exponential per logit (exp2 of a fused multiply-add).
-      auto block_stats = [&](const int m, const int n, const float (&v)[EW], const float (&w)[EW])
-          __attribute__((always_inline)) {
-        constexpr float L2E = 1.4426950408889634f;
+      // The maximum of one row's 64-column block (every lane of the 8 gets it).
+      auto block_max = [&](const int n, const float (&v)[EW]) __attribute__((always_inline)) {
         float mx = -INFINITY;
 #pragma unroll
         for (int k = 0; k < EW; ++k) mx = n + k < g.N ? fmaxf(mx, v[k]) : mx;
         static_assert(64 / EW == 8, "a 64-column block spans 8 lanes");
-        mx = max8(mx);
+        return max8(mx);
+      };
+      // The cached logits: an fp16 cache holds z minus its block maximum
+      // (kept in fp32 in the statistics), so its rounding error is relative
+      // to |z - max|, not to |z|: large confident logits keep p = exp(z -
+      // lse) to fp16 precision where p matters.  An fp32 cache holds z.
+      auto store_logits = [&](const int m, const int n, const float (&v)[EW], const float mx)
+          __attribute__((always_inline)) {
+        if (e.out_dtype == F16) {
+          float r[EW];
+#pragma unroll
+          for (int k = 0; k < EW; ++k) r[k] = v[k] - mx;
+          epilogue_v(e, g.M, g.N, m, n, r, vec);
+        } else {
+          epilogue_v(e, g.M, g.N, m, n, v, vec);
+        }
+      };
+      // Softmax partials of one row's 64-column block: the block maximum,
+      // then one exponential per logit (exp2 of a fused multiply-add).
+      auto block_stats = [&](const int m, const int n, const float (&v)[EW], const float (&w)[EW],
+                             const float mx) __attribute__((always_inline)) {
+        constexpr float L2E = 1.4426950408889634f;
         SoftPart sp = {mx, 0.f, 0.f};
         if (mx != -INFINITY) {
           const float nm = -mx * L2E;
@@ -452,11 +470,12 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[BM / WM / 32][B
             w[k] = v[k] - u[k];
             wn[k] = -w[k];
           }
-          epilogue_v(e, g.M, g.N, m, n, v, vec);
-          epilogue_v(e, g.M, g.N, m + 1, n, u, vec);
+          const float mv = block_max(n, v), mu = block_max(n, u);
+          store_logits(m, n, v, mv);
+          store_logits(m + 1, n, u, mu);
           label_logit(m, n, v);
-          block_stats(m, n, v, w);
-          block_stats(m + 1, n, u, wn);
+          block_stats(m, n, v, w, mv);
+          block_stats(m + 1, n, u, wn, mu);
         }
       } else {
         for (int t = lane; t < 32 * QPR; t += 64) {
@@ -468,9 +487,10 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[BM / WM / 32][B
             const float4 x = *reinterpret_cast<const float4*>(&ep[row * LDW + col + k]);
             v[k] = x.x; v[k + 1] = x.y; v[k + 2] = x.z; v[k + 3] = x.w;
           }
-          epilogue_v(e, g.M, g.N, m, n, v, vec);
+          const float mv = block_max(n, v);
+          store_logits(m, n, v, mv);
           label_logit(m, n, v);
-          block_stats(m, n, v, v);
+          block_stats(m, n, v, v, mv);
         }
       }
     } else {

@@ -4,7 +4,8 @@
 // h_out) interleaved with rows of z' (readout of h_in, the stop-gradient
 // consistency target) when alpha < 1; fp32, or fp16 in the bf16 path, where
 // the GEMM's epilogue also leaves the fp32 statistics of pass 1 and the
-// fp32 label logit z_y.  One workgroup per token row then
+// fp32 label logit z_y, and the fp16 values are z minus the fp32 maximum of
+// their 64-column block.  One workgroup per token row then
 //   pass 1: online max / sum-exp of z and z', plus the KL statistic
 //           E = sum_v p_v (z_v - z'_v)   (reverse)   or
 //           F = sum_v q_v (z'_v - z_v)   (forward),
@@ -106,17 +107,24 @@ __device__ inline void st_dz4(const ObjDesc& o, int64_t i, const float (&g)[4]) 
   }
 }
 
-// Logits as cached: fp32, or fp16 (ZT = uint16_t) in the bf16 path.
-__device__ inline float ldz1(const float* p, int64_t v) { return p[v]; }
-__device__ inline float ldz1(const uint16_t* p, int64_t v) { return f16_to_f32(p[v]); }
-__device__ inline void ldz4(const float* p, int64_t v, float (&x)[4]) {
+// Logits as cached: fp32, or fp16 (ZT = uint16_t) in the bf16 path, where
+// the cache holds z minus the maximum of its 64-column block and `st`
+// points at the row's block statistics (the maximum in .x).
+__device__ inline float ldz1(const float* p, int64_t v, const float4*) { return p[v]; }
+__device__ inline float ldz1(const uint16_t* p, int64_t v, const float4* st) {
+  return f16_to_f32(p[v]) + st[v >> 6].x;
+}
+__device__ inline void ldz4(const float* p, int64_t v, float (&x)[4], const float4*) {
   const float4 a = *reinterpret_cast<const float4*>(p + v);
   x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
 }
-__device__ inline void ldz4(const uint16_t* p, int64_t v, float (&x)[4]) {
+__device__ inline void ldz4(const uint16_t* p, int64_t v, float (&x)[4], const float4* st) {
   const uint2 a = *reinterpret_cast<const uint2*>(p + v);
-  x[0] = f16_to_f32((uint16_t)(a.x & 0xffff)); x[1] = f16_to_f32((uint16_t)(a.x >> 16));
-  x[2] = f16_to_f32((uint16_t)(a.y & 0xffff)); x[3] = f16_to_f32((uint16_t)(a.y >> 16));
+  const float mx = st[v >> 6].x;  // four columns from v (v % 4 == 0) share a block
+  x[0] = f16_to_f32((uint16_t)(a.x & 0xffff)) + mx;
+  x[1] = f16_to_f32((uint16_t)(a.x >> 16)) + mx;
+  x[2] = f16_to_f32((uint16_t)(a.y & 0xffff)) + mx;
+  x[3] = f16_to_f32((uint16_t)(a.y >> 16)) + mx;
 }
 
 template <typename ZT>
@@ -140,9 +148,12 @@ __global__ void __launch_bounds__(OT) objective_rows_kernel(ObjDesc o) {
     return;
   }
 
+  // the row's 64-column block statistics (bf16 path; null in the fp32 path)
+  const float4* stz = o.stats ? o.stats + (int64_t)i * o.stacked * o.ldst : nullptr;
+  const float4* stq = o.stats && zp ? stz + o.ldst : nullptr;
   Soft sp = {-INFINITY, 0.f, 0.f}, sq = {-INFINITY, 0.f, 0.f};
   if (o.stats) {  // partials of 64-column blocks from the logit GEMM's epilogue
-    const float4* st = o.stats + (int64_t)i * o.stacked * o.ldst;
+    const float4* st = stz;
     for (int cb = threadIdx.x; cb < o.nst; cb += OT) {
       const float4 p = st[cb];
       sp = soft_merge(sp, {p.x, p.y, p.z});
@@ -154,8 +165,8 @@ __global__ void __launch_bounds__(OT) objective_rows_kernel(ObjDesc o) {
   }
   for (int v = o.stats ? V4 : threadIdx.x * 4; v < V4; v += OT * 4) {
     float a[4], b[4] = {0.f, 0.f, 0.f, 0.f};
-    ldz4(z, v, a);
-    if (zp) ldz4(zp, v, b);
+    ldz4(z, v, a, stz);
+    if (zp) ldz4(zp, v, b, stq);
     const float ab[4] = {a[0] - b[0], a[1] - b[1], a[2] - b[2], a[3] - b[3]};
     sp = soft_add4(sp, a, ab);  // e accumulates sum p (z - z') unnormalised
     if (zp) {
@@ -164,8 +175,8 @@ __global__ void __launch_bounds__(OT) objective_rows_kernel(ObjDesc o) {
     }
   }
   for (int v = V4 + threadIdx.x; v < (o.stats ? 0 : o.V); v += OT) {
-    const float a = ldz1(z, v);
-    const float b = zp ? ldz1(zp, v) : 0.f;
+    const float a = ldz1(z, v, stz);
+    const float b = zp ? ldz1(zp, v, stq) : 0.f;
     sp = soft_add(sp, a, a - b);
     if (zp) sq = soft_add(sq, b, b - a);
   }
@@ -178,7 +189,7 @@ __global__ void __launch_bounds__(OT) objective_rows_kernel(ObjDesc o) {
     lse2 = sq.m + __logf(sq.s);
     F = sq.e / sq.s;
   }
-  const float zy = o.zy ? o.zy[i] : ldz1(z, y);
+  const float zy = o.zy ? o.zy[i] : ldz1(z, y, stz);
   const float ce = lse - zy;
   float kl = 0.f;
   if (zp) kl = rev ? (E - lse + lse2) : (F - lse2 + lse);
@@ -199,14 +210,14 @@ __global__ void __launch_bounds__(OT) objective_rows_kernel(ObjDesc o) {
     float g[4] = {0.f, 0.f, 0.f, 0.f};
     if (v < V4) {
       float a4[4], b4[4] = {0.f, 0.f, 0.f, 0.f};
-      ldz4(z, v, a4);
-      if (zp) ldz4(zp, v, b4);
+      ldz4(z, v, a4, stz);
+      if (zp) ldz4(zp, v, b4, stq);
 #pragma unroll
       for (int k = 0; k < 4; ++k) g[k] = grad(v + k, a4[k], b4[k]);
     } else {
 #pragma unroll
       for (int k = 0; k < 4; ++k)
-        if (v + k < o.V) g[k] = grad(v + k, ldz1(z, v + k), zp ? ldz1(zp, v + k) : 0.f);
+        if (v + k < o.V) g[k] = grad(v + k, ldz1(z, v + k, stz), zp ? ldz1(zp, v + k, stq) : 0.f);
     }
     st_dz4(o, orow + v, g);
   }

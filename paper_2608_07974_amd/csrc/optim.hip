@@ -67,4 +67,22 @@ hipError_t launch_shadow(const float* master, bf16_t* shadow, size_t n, hipStrea
   return hipGetLastError();
 }
 
+__global__ void zero_block_kernel(float* __restrict__ p, int64_t ld, int64_t r0, int64_t r1,
+                                  int64_t c0, int64_t c1) {
+  const int64_t w = c1 - c0, n = (r1 - r0) * w;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[(r0 + i / w) * ld + c0 + i % w] = 0.f;
+}
+
+hipError_t launch_zero_block(float* p, int64_t ld, int64_t r0, int64_t r1, int64_t c0, int64_t c1,
+                             hipStream_t s) {
+  if (r1 <= r0 || c1 <= c0) return hipSuccess;
+  int64_t blocks = ((r1 - r0) * (c1 - c0) + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(zero_block_kernel, dim3((unsigned)blocks), dim3(256), 0, s, p, ld, r0, r1, c0,
+                     c1);
+  return hipGetLastError();
+}
+
 }  // namespace zl

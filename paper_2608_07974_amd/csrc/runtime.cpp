@@ -453,7 +453,7 @@ zl_status zl_chunk_load(zl_chunk* chunk, const char* path, int64_t* microbatches
   fclose(f);
   RT_OK(zl_set_step(chunk, h.step));
   zl::chunk_close_window(chunk);
-  if (cfg.dtype == ZL_BF16) RT_OK(zl_refresh_shadow(chunk, stream));
+  RT_OK(zl_refresh_shadow(chunk, stream));
   if (microbatches) *microbatches = h.microbatches;
   if (windows) *windows = h.windows;
   return ZL_OK;

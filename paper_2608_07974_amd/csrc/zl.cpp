@@ -57,9 +57,10 @@ struct LayerOff {
 struct Dims {
   int arch, L, d, hq, hkv, hd, ff, V, dq, dkv, nqkv, nup;
   int ar;  // readout adapter width (0 = none)
-  int lr;  // LoRA rank (0 = full training)
+  int lr;  // LoRA rank as stored: the configured rank rounded up to 8 (0 = full training)
+  int lq;  // the configured LoRA rank (factor rows/columns lq .. lr-1 are zero padding)
   int nqa, nua;  // rows of the stacked A factors of the QKV and up projections
-  float ls;      // LoRA scale lora_alpha / lr
+  float ls;      // LoRA scale lora_alpha / lq
   bool llama;
 };
 
@@ -79,10 +80,11 @@ Dims dims_of(const zl_config& c) {
   m.nqkv = m.dq + 2 * m.dkv;
   m.nup = m.llama ? 2 * m.ff : m.ff;
   m.ar = c.adapter_rank;
-  m.lr = c.lora_rank;
+  m.lq = c.lora_rank;
+  m.lr = (c.lora_rank + 7) / 8 * 8;
   m.nqa = m.llama ? 3 * m.lr : m.lr;
   m.nua = m.llama ? 2 * m.lr : m.lr;
-  m.ls = m.lr ? c.lora_alpha / (float)m.lr : 0.f;
+  m.ls = m.lq ? c.lora_alpha / (float)m.lq : 0.f;
   return m;
 }
 
@@ -129,8 +131,8 @@ zl_status check_config(const zl_config* c) {
     return fail(ZL_ERR_UNSUPPORTED, "max_batch * max_seq above 2^24 tokens");
   if (c->adapter_rank < 0 || c->adapter_rank % 16 || c->adapter_rank > 8192)
     return fail(ZL_ERR_INVALID_ARG, "adapter_rank must be 0 or a multiple of 16 up to 8192");
-  if (c->lora_rank < 0 || c->lora_rank % 8 || c->lora_rank > 256)
-    return fail(ZL_ERR_INVALID_ARG, "lora_rank must be 0 or a multiple of 8 up to 256");
+  if (c->lora_rank < 0 || c->lora_rank > 256)
+    return fail(ZL_ERR_INVALID_ARG, "lora_rank must be in [0, 256]");
   if (c->lora_rank && !(c->lora_alpha > 0.f && isfinite(c->lora_alpha)))
     return fail(ZL_ERR_INVALID_ARG, "lora_alpha must be finite and > 0");
   return ZL_OK;
@@ -205,8 +207,11 @@ void layer_tensors(const Dims& m, Packer& pk, std::vector<LayerOff>& lay) {
   }
 }
 
-// Every factor's element count is a multiple of 64 (r and the widths are
-// multiples of 8, d and ff of 64), so stacked factors are contiguous.
+// Every factor's element count is a multiple of 64 (the stored rank and the
+// widths are multiples of 8, d and ff of 64), so stacked factors are
+// contiguous.  A rank that is not a multiple of 8 is stored padded to the
+// next one (16-byte factor rows for the bf16 GEMMs): A [lr, in] with rows
+// lq.. zero, B [out, lr] with columns lq.. zero.
 void lora_tensors(const Dims& m, Packer& pk, std::vector<LoraOff>& lora) {
   const int r = m.lr;
   lora.resize(m.L);
@@ -605,6 +610,18 @@ void zl_chunk_destroy(zl_chunk* chunk) {
 
 zl_status zl_refresh_shadow(zl_chunk* c, void* stream) {
   if (!c) return fail(ZL_ERR_INVALID_ARG, "chunk is NULL");
+  if (c->m.lq < c->m.lr) {
+    // the padding of factors stored wider than their rank is zero: then its
+    // gradient is exactly zero and no step moves it
+    for (const zl_tensor_desc& t : c->layout.descs) {
+      const size_t nl = strlen(t.name);
+      if (nl < 3 || t.name[nl - 3] != '_' || t.name[nl - 2] != 'l') continue;
+      const bool a = t.name[nl - 1] == 'a';
+      const int64_t rows = t.shape[0], cols = t.shape[1];
+      ZL_HIP(launch_zero_block(c->buf.master + t.offset, cols, a ? c->m.lq : 0, rows,
+                               a ? 0 : c->m.lq, cols, S_(stream)));
+    }
+  }
   if (c->act != BF16) return ZL_OK;
   ZL_HIP(launch_shadow(c->buf.master, reinterpret_cast<bf16_t*>(c->buf.shadow),
                        c->layout.n_params, S_(stream)));
@@ -1213,6 +1230,19 @@ zl_status zl_inspect(const zl_chunk* c, const char* name, int layer, zl_view* v)
   if (n == "dh_out") return set(p.DX, T, m.d, ZL_F32);
   if (n == "row_loss") return set(p.ROWLOSS, T, 1, ZL_F32);
   if (n == "n_omega") return set(p.NOMEGA, 1, 1, ZL_F32);
+  if (n == "dz" || n == "dnf") {
+    if (T < 1) return fail(ZL_ERR_STATE, "no forward has run");
+    const int last = (T - 1) / p.R * p.R;  // first row of the last row block
+    const int rows = T - last;
+    if (n == "dz") return set(p.DZ, rows, p.Vpad, act);
+    return set(p.DNF, rows, m.d, ZL_F32);
+  }
+  if (n == "dxa") return set(p.DXA, T, m.d, act);
+  if (n == "dxb") return set(p.DXB, T, m.d, act);
+  if (n == "dup") return set(p.DUP, T, m.nup, act);
+  if (n == "do") return set(p.DO, T, m.dq, act);
+  if (n == "dqkv") return set(p.DQKV, T, m.nqkv, act);
+  if (n == "dn") return set(p.DN, T, m.d, ZL_F32);
   if (layer < 0 || layer >= m.L) return fail(ZL_ERR_INVALID_ARG, "layer out of range");
   if (n == "n1") return set(p.N1[layer], T, m.d, act);
   if (n == "qkv") return set(p.QKV[layer], T, m.nqkv, act);

@@ -103,12 +103,35 @@ def test_lora_layout_matches_workload_specs(adapter_rank):
                     assert by[(l, b)]["offset"] == by[(l, a)]["offset"] + by[(l, a)]["numel"]
 
 
-@pytest.mark.parametrize("rank,lalpha", [(-8, 16.0), (4, 16.0), (12, 16.0), (264, 16.0),
-                                         (8, 0.0), (8, float("nan"))])
+@pytest.mark.parametrize("rank,lalpha", [(-8, 16.0), (-1, 16.0), (257, 16.0), (264, 16.0),
+                                         (8, 0.0), (4, 0.0), (8, float("nan"))])
 def test_lora_rank_validated(rank, lalpha):
     b = ctypes.c_size_t()
     cfg = _cfg(lora_rank=rank, lora_alpha=lalpha)
     assert zl.load().zl_workspace_size(ctypes.byref(cfg), ctypes.byref(b)) == zl.ZL_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("rank", [1, 4, 12])
+def test_lora_rank_below_a_multiple_of_8_is_stored_padded(rank):
+    """The paper's rank 4 (Sec. IV setting): the factors are stored 8 (16)
+    wide, A [r8, in] and B [out, r8], in the order and offsets of the
+    rank-r8 layout; the configured rank sets the scale (lora_alpha / r)."""
+    import workload
+    r8 = (rank + 7) // 8 * 8
+    shp = workload.get_config("tiny", lora_rank=rank)
+    cfg = zl.make_config(zl.ZL_ARCH_LLAMA, shp.n_layers, shp.d_model, shp.n_heads, shp.n_kv_heads,
+                         shp.head_dim, shp.d_ff, shp.vocab, rope_theta=1e4, max_batch=1,
+                         max_seq=8, lora_rank=rank, lora_alpha=16.0)
+    n, lay = zl.zl_param_layout(cfg)
+    cfg8 = zl.make_config(zl.ZL_ARCH_LLAMA, shp.n_layers, shp.d_model, shp.n_heads,
+                          shp.n_kv_heads, shp.head_dim, shp.d_ff, shp.vocab, rope_theta=1e4,
+                          max_batch=1, max_seq=8, lora_rank=r8, lora_alpha=16.0)
+    n8, lay8 = zl.zl_param_layout(cfg8)
+    assert n == n8 and lay == lay8
+    specs = workload.param_specs(shp)
+    for t, (_, shape, _) in zip(lay, specs):
+        want = (r8, shape[1]) if t["name"].endswith("_la") else (shape[0], r8)
+        assert tuple(t["shape"]) == want
 
 
 def test_lora_create_needs_base_buffers():

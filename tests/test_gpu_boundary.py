@@ -57,8 +57,12 @@ def test_argument_errors_launch_nothing():
                             d["h_in"].data_ptr(), 0)
     assert e.value.status == zl.ZL_ERR_INVALID_ARG
     big = torch.zeros(TINY.batch + 1, TINY.seq, TINY.d_model, dtype=torch.float32, device="cuda")
-    with pytest.raises(zl.ZlError) as e:
+    with pytest.raises(ValueError):  # the binding refuses before any call
         ch.forward(big)
+    out = torch.empty_like(big)
+    with pytest.raises(zl.ZlError) as e:  # and so does the library
+        zl.zl_chunk_forward(ch.handle, big.data_ptr(), 0, 0, TINY.batch + 1, TINY.seq,
+                            out.data_ptr(), 0)
     assert e.value.status == zl.ZL_ERR_INVALID_ARG
     with pytest.raises(zl.ZlError) as e:
         zl.zl_chunk_backward(ch.handle, float("nan"), 0, 0)

@@ -199,3 +199,151 @@ def test_attention_full_size_one_head_group(name):
         mx = s.max(axis=1, keepdims=True)
         ref = (np.log(np.exp(s - mx).sum(axis=1, keepdims=True)) + mx)[:, 0]
         assert np.max(np.abs(lse[j] - ref) / np.maximum(1.0, np.abs(ref))) < 1e-4
+
+
+def _rows_per_tile(T, rng, tile=256):
+    """One row from every tile of `tile` rows (the GEMMs' row tiles)."""
+    return np.array([t + int(rng.integers(min(tile, T - t))) for t in range(0, T, tile)])
+
+
+def _dev_rows(ch, name, rows, layer=0):
+    t = ch.inspect_device(name, layer)
+    return t[torch.tensor(rows, device=t.device, dtype=torch.long)].double().cpu().numpy()
+
+
+def _dev_cols(ch, name, cols, layer=0):
+    t = ch.inspect_device(name, layer)
+    return t[:, torch.tensor(cols, device=t.device, dtype=torch.long)].double().cpu().numpy()
+
+
+def _near_bf16(got, ref, what):
+    """got is ref stored in bf16 (up to fp32 accumulation order): every
+    element within 2^-8 of itself plus 1e-3 of its row's RMS."""
+    rms = np.sqrt(np.mean(ref * ref, axis=-1, keepdims=True))
+    bad = np.abs(got - ref) > 2.0 ** -8 * np.abs(ref) + 1e-3 * rms
+    assert not bad.any(), (what, np.argwhere(bad)[:5])
+
+
+def _near_f32(got, ref, scale, what, rel=1e-4):
+    """got is ref accumulated in fp32: within rel of the size of its terms."""
+    bad = np.abs(got - ref) > rel * scale + 1e-30
+    assert not bad.any(), (what, np.argwhere(bad)[:5], np.max(np.abs(got - ref) / (scale + 1e-30)))
+
+
+def _rms_norm(x, w, eps):
+    return x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps) * w
+
+
+@pytest.mark.parametrize("name", ["8b", "1b-long"])
+def test_full_size_every_row_tile_and_weight_gradients(name):
+    """At the benchmarked B x S, element-wise, on layer 0 of the update:
+    one row from every 256-row tile of each forward GEMM's output (norm 1,
+    QKV with RoPE, output projection + residual, norm 2, gate/up, SwiGLU,
+    down + residual) and of the data gradients (down with the SwiGLU
+    backward, output projection, QKV), each from the device's own bf16
+    operands in fp64; sampled entries of the four weight gradients
+    dW = dy^T x over all B*S tokens (the two paired launches); sampled
+    entries of the head's data gradient dZ W_lm over the full vocabulary
+    (split over K at the 1B width); and the head's per-row loss and
+    dL/dh_out of one row from every tile against the oracle."""
+    shp = workload.get_config(name)
+    B, S, d, V = shp.batch, shp.seq, shp.d_model, shp.vocab
+    T = B * S
+    ff, hd = shp.d_ff, shp.head_dim
+    dq, dkv = shp.n_heads * hd, shp.n_kv_heads * hd
+    nqkv = dq + 2 * dkv
+    rng = np.random.default_rng(3)
+    ch, h_in, labels = _bench_chunk(shp)
+    ch.forward(h_in)
+    ch.objective(labels)
+    torch.cuda.synchronize()
+    dz_last = ch.inspect_device("dz")
+    R = dz_last.shape[0]
+    row_loss = ch.inspect("row_loss").reshape(-1)
+    dh_out = ch.inspect_device("dh_out")
+    rows = _rows_per_tile(T, rng)
+    dh_rows = dh_out[torch.tensor(rows, device=dh_out.device)].double().cpu().numpy()
+    # head data gradient of the last row block: entries over the full vocabulary
+    W_dev = ch.head_w
+    ii = np.concatenate([[0, R - 1], rng.integers(R, size=14)])
+    jj = np.concatenate([[0, d - 1], rng.integers(d, size=14)])
+    dnf = ch.inspect("dnf")
+    dzr = dz_last[torch.tensor(ii, device=dz_last.device)][:, :V].double().cpu().numpy()
+    Wc = W_dev[:, torch.tensor(jj, device=W_dev.device)].double().cpu().numpy()
+    terms = dzr[:, :, None] * Wc[None, :, :]  # [i, v, j]
+    ref = terms.sum(axis=1)
+    _near_f32(dnf[ii][:, jj], ref, np.abs(terms).sum(axis=1), "head dgrad", rel=2e-4)
+    del terms, dzr, Wc
+    ch.backward(1.0, 0)
+    torch.cuda.synchronize()
+
+    P0 = _layer_params(ch, ch.master, 0)
+    pos = rows % S
+    eps = shp.norm_eps
+    # ---- forward, one row per 256-row tile
+    x0 = _dev_rows(ch, "x", rows, 0)
+    n1 = _dev_rows(ch, "n1", rows)
+    _near_bf16(n1, _rms_norm(x0, P0["L0.ln1_w"], eps), "n1")
+    wqkv = np.concatenate([P0["L0.wq"], P0["L0.wk"], P0["L0.wv"]])
+    y = n1 @ wqkv.T
+    ang = ops.rope_angles(pos[None, :], hd, shp.rope_theta)  # [1, rows, hd/2]
+    nh = shp.n_heads + shp.n_kv_heads
+    qk = ops.rope_fwd(y[:, : nh * hd].reshape(1, len(rows), nh, hd), ang).reshape(len(rows), -1)
+    _near_bf16(_dev_rows(ch, "qkv", rows), np.concatenate([qk, y[:, nh * hd:]], axis=1), "qkv")
+    o = _dev_rows(ch, "o", rows)
+    x2 = _dev_rows(ch, "x2", rows)
+    _near_f32(x2, x0 + o @ P0["L0.wo"].T, np.abs(x0) + np.abs(o) @ np.abs(P0["L0.wo"]).T,
+              "output projection + residual")
+    n2 = _dev_rows(ch, "n2", rows)
+    _near_bf16(n2, _rms_norm(x2, P0["L0.ln2_w"], eps), "n2")
+    wgu = np.concatenate([P0["L0.wg"], P0["L0.wu"]])
+    up = _dev_rows(ch, "up", rows)
+    _near_bf16(up, n2 @ wgu.T, "gate/up")
+    act = _dev_rows(ch, "act", rows)
+    g, u = up[:, :ff], up[:, ff:]
+    _near_bf16(act, ops.swiglu_fwd(g, u), "swiglu")
+    x1 = _dev_rows(ch, "x", rows, 1)
+    t = act @ P0["L0.wd"].T
+    scale = np.abs(x2) + np.abs(act) @ np.abs(P0["L0.wd"]).T
+    _near_f32(x1, x2 + t, scale, "down + residual")
+    # ---- backward data gradients of layer 0, one row per tile
+    dxa = _dev_rows(ch, "dxa", rows)
+    dup = _dev_rows(ch, "dup", rows)
+    dg, du = ops.swiglu_bwd(dxa @ P0["L0.wd"], g, u)
+    _near_bf16(dup, np.concatenate([dg, du], axis=1), "down dgrad + SwiGLU backward")
+    dxb = _dev_rows(ch, "dxb", rows)
+    _near_bf16(_dev_rows(ch, "do", rows), dxb @ P0["L0.wo"], "output projection dgrad")
+    dqkv = _dev_rows(ch, "dqkv", rows)
+    t = dqkv @ wqkv
+    _near_f32(_dev_rows(ch, "dn", rows), t, np.abs(dqkv) @ np.abs(wqkv), "QKV dgrad")
+    # ---- weight gradients dW[o, i] = sum_t dy[t, o] x[t, i] over all T tokens
+    for wname, dyn, xn, nout, nin in (("wd", "dxa", "act", d, ff), ("wg", "dup", "n2", 2 * ff, d),
+                                      ("wo", "dxb", "o", d, dq), ("wq", "dqkv", "n1", nqkv, d)):
+        oo = np.concatenate([[0, nout - 1], rng.integers(nout, size=10)])
+        kk = np.concatenate([[0, nin - 1], rng.integers(nin, size=10)])
+        dy = _dev_cols(ch, dyn, oo)
+        xx = _dev_cols(ch, xn, kk)
+        terms = dy[:, :, None] * xx[:, None, :]  # [T, o, i]
+        tv = ch.by_key[f"L0.{wname}"]
+        G = ch.grad[tv["offset"]: tv["offset"] + nout * nin].view(nout, nin)
+        got = G[torch.tensor(oo, device=G.device)][:, torch.tensor(kk, device=G.device)]
+        _near_f32(got.double().cpu().numpy(), terms.sum(0), np.abs(terms).sum(0),
+                  f"dW {wname}", rel=2e-4)
+        del terms
+    # ---- the head: loss row and dL/dh_out of one row per tile (oracle)
+    lab = labels.cpu().numpy().reshape(-1)
+    hL = _dev_rows(ch, "x", rows, shp.n_layers)
+    hin = h_in.reshape(T, d)[torch.tensor(rows, device=h_in.device)].double().cpu().numpy()
+    Wh = W_dev.double().cpu().numpy()
+    hn = ch.head_norm_w.double().cpu().numpy()
+    _, dh_ref, info = local_objective_ref(hL, hin, lab[rows], Wh, shp.arch, hn, None, eps, 0.5)
+    del Wh
+    rows_ref = 0.5 * info["ce"] + 0.5 * info["kl"]
+    assert np.max(np.abs(row_loss[rows] - rows_ref) / np.maximum(np.abs(rows_ref), 1.0)) < 1e-3
+    n_total = int(np.sum((lab >= 0) & (lab < V)))
+    a, b = dh_rows * n_total, dh_ref * info["n_omega"]
+    rn = np.linalg.norm(a - b, axis=1) / np.maximum(np.linalg.norm(b, axis=1), 1e-30)
+    assert np.max(rn) < 2e-2, (rows[np.argmax(rn)], np.max(rn))
+    ch.close()
+    del ch, h_in
+    torch.cuda.empty_cache()
