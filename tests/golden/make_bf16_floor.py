@@ -18,11 +18,50 @@ import time
 ROOT = os.path.dirname(os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
 sys.path.insert(0, ROOT)
 
+import numpy as np  # noqa: E402
+
 from oracle import bf16_round  # noqa: E402
 from tests import gpu_cases, parity  # noqa: E402
 
 
+def _metrics(rounded, exact):
+    rounded = dict(rounded, h_out=bf16_round(rounded["h_out"]))  # h_out leaves in bf16
+    return {k: {m: float(v) for m, v in d.items()}
+            for k, d in parity.results_metrics(rounded, exact).items()
+            if k in ("h_out", "dh_out") or k.startswith("g")}
+
+
+def step_floors(name):
+    """Floors of each step of a several-step case, each taken from the same
+    state of the exact trajectory: the exact step against the bf16-storage
+    step from those parameters and optimizer moments."""
+    from oracle.chunk import chunk_update_ref, init_opt_state
+    shp, kw, steps, params, batch = gpu_cases.case_inputs(name)
+    fp = parity.fingerprint(params, batch)
+    mb = dict(h_in=batch["h_in"], labels=batch["labels"], seq_lens=batch["seq_lens"],
+              pos_ids=batch["pos_ids"])
+    P = {k: np.asarray(v, np.float64) for k, v in params.items()}
+    st = init_opt_state()
+    out = []
+    for _ in range(steps):
+        runs = []
+        for store in (False, True):
+            cfg = gpu_cases.oracle_cfg(shp, store_bf16=store, **kw)
+            r = chunk_update_ref(cfg, P, st, [mb], batch["head_w"], batch["head_norm_w"],
+                                 batch["head_norm_b"], grad_scale=1.0)
+            runs.append(r)
+        one = [dict(losses=r["losses"], grads=[r["grads"]], h_out=r["runs"][0]["h_out"],
+                    dh_out=r["runs"][0]["dh_out"]) for r in runs]
+        out.append(_metrics(one[1], one[0]))
+        P, st = runs[0]["params"], runs[0]["state"]
+        del runs, one
+    return fp, out
+
+
 def floor_of(name):
+    if gpu_cases.BF16_CASES[name].get("steps", 1) > 1:
+        fp, steps = step_floors(name)
+        return dict(fingerprint=fp, loss_rel=None, tensors=steps[0], steps=steps)
     exact, (params, batch) = gpu_cases.case_oracle(name, masters=False)
     exact.pop("masters")
     fp = parity.fingerprint(params, batch)

@@ -86,9 +86,10 @@ def fingerprint(params, batch):
     return h.hexdigest()
 
 
-def load_floor(case, params, batch):
+def load_floor(case, params, batch, per_step=False):
     """The stored bf16 storage floor of a case, checked to belong to these
-    inputs."""
+    inputs.  per_step: the list of floors of each step of a several-step
+    case (each from the same state of the exact trajectory)."""
     floors = json.load(open(FLOOR_FILE))
     if case not in floors:
         raise KeyError(f"no bf16 floor stored for case {case!r}: run tests/golden/make_bf16_floor.py")
@@ -96,6 +97,8 @@ def load_floor(case, params, batch):
     if f["fingerprint"] != fingerprint(params, batch):
         raise ValueError(f"the inputs of case {case!r} changed since its bf16 floor was stored: "
                          "run tests/golden/make_bf16_floor.py")
+    if per_step:
+        return f.get("steps", [f["tensors"]])
     return f["tensors"]
 
 

@@ -27,8 +27,11 @@ torch = pytest.importorskip("torch")
 def _run_device(shp, params, batch, steps=1, **kw):
     ch = device_chunk(shp, params, batch, **kw)
     d = to_dev(batch, shp.dtype)
-    out = dict(grads=[], masters=[ch.tensors(ch.master)], losses=[])
+    out = dict(grads=[], masters=[ch.tensors(ch.master)], losses=[], moments=[])
+    adam = ch.adam_m is not None
     for _ in range(steps):
+        if adam:  # the optimizer state entering this step
+            out["moments"].append((ch.tensors(ch.adam_m), ch.tensors(ch.adam_v)))
         h_out = ch.forward(d["h_in"], d["seq_lens"], d["pos_ids"])
         ch.objective(d["labels"])
         if not out["grads"]:
@@ -109,7 +112,52 @@ def _named(name):
         dev = _run_device(shp, params, batch, steps=steps, **kw)
         ref = oracle_run(shp, params, batch, steps=steps, **kw)
         np.testing.assert_array_equal(dev["h_in_after"].astype(np.float32), batch["h_in"])
+        if steps > 1:
+            return _gate_steps(shp, kw, params, batch, dev, ref,
+                               load_floor(name, params, batch, per_step=True))
     return gate(dev, ref, "bf16", kw["optimizer"], floor)
+
+
+def _gate_steps(shp, kw, params, batch, dev, ref, floors):
+    """Several bf16 steps.  The trajectories of device and oracle drift apart
+    by bf16 noise that Adam's sign-like first steps amplify, so each step is
+    gated from the state the device reached: the oracle runs that step from
+    the device's parameters and AdamW moments (step s's gradients, delta and
+    loss), against the floors of step s (measured from the same step of the
+    exact trajectory).  The whole trajectory is gated at the stated
+    tolerance on every step's loss and the final parameters."""
+    from oracle.chunk import chunk_update_ref
+    cfg = oracle_cfg(shp, **kw)
+    mb = dict(h_in=batch["h_in"], labels=batch["labels"], seq_lens=batch["seq_lens"],
+              pos_ids=batch["pos_ids"])
+    frozen = {k: np.asarray(v, np.float64) for k, v in params.items() if k not in dev["masters"][0]}
+    out = {}
+    for s in range(len(dev["grads"])):
+        P = dict(frozen, **dev["masters"][s])
+        if dev["moments"]:
+            m, v = dev["moments"][s]
+            state = dict(m=m, v=v, t=s)
+        else:
+            state = init_opt_state()
+        r = chunk_update_ref(cfg, P, state, [mb], batch["head_w"], batch["head_norm_w"],
+                             batch["head_norm_b"], grad_scale=1.0)
+        one_dev = dict(losses=[dev["losses"][s]], grads=[dev["grads"][s]],
+                       masters=[dev["masters"][s], dev["masters"][s + 1]])
+        one_ref = dict(losses=r["losses"], grads=[r["grads"]],
+                       masters=[{k: P[k] for k in dev["masters"][s]},
+                                {k: r["params"][k] for k in dev["masters"][s]}])
+        if s == 0:
+            one_dev.update(h_out=dev["h_out"], dh_out=dev["dh_out"])
+            one_ref.update(h_out=ref["h_out"], dh_out=ref["dh_out"])
+        for k, v in gate(one_dev, one_ref, "bf16", kw["optimizer"], floors[s]).items():
+            out[f"step{s}/{k}"] = v
+    for s, (a, b) in enumerate(zip(dev["losses"], ref["losses"])):
+        assert abs(a - b) <= TOL["bf16"] * abs(b), ("trajectory loss", s, a, b)
+    last = len(dev["masters"]) - 1
+    for k in dev["masters"][last]:
+        e = rel_err(dev["masters"][last][k], ref["masters"][last][k])
+        assert e < TOL["bf16"], ("trajectory parameters", k, e)
+    return out
 
 
 # ----------------------------------------------------------------- fp32 tiny
