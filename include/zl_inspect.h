@@ -77,6 +77,22 @@ zl_status zl_kernel_attention(int B, int S, int Hq, int Hkv, int hd, const void*
                               void* dq, void* dk, void* dv, float* delta, int dtype,
                               int backward, void* stream);
 
+/* The backward of zl_kernel_attention (backward = 1) for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): no delta argument; the softmax-backward
+ * row term delta = rowsum(dout * o), B * Hq * S floats, is kept in a device
+ * array of the library of at most 2^20 floats (4 MiB), one per GPU, held
+ * until the process ends.  Larger B * Hq * S returns ZL_ERR_UNSUPPORTED
+ * before any launch.  The call allocates nothing.  Calls on one GPU share
+ * that array: calls that overlap on one GPU (different streams, or threads
+ * without ordering) race.  dq, dk, dv are bit-identical to those of
+ * zl_kernel_attention with a caller delta buffer. */
+zl_status zl_kernel_attention_bwd_noalloc(int B, int S, int Hq, int Hkv, int hd, const void* q,
+                                          const void* k, const void* v, int64_t ld_qkv,
+                                          const int32_t* seq_lens, const void* o, const float* lse,
+                                          const void* dout, void* dq, void* dk, void* dv, int dtype,
+                                          void* stream);
+
 /* Per-kernel timing of the chunk's own launches.  zl_profile_begin creates
  * `capacity` pairs of HIP events (host resources, no device memory) and,
  * until zl_profile_end, records one pair on the launch stream around each

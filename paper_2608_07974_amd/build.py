@@ -16,7 +16,7 @@ OUT_DIR = os.path.join(HERE, "_lib")
 LIB = os.path.join(OUT_DIR, "libzl.so")
 BUILD = os.path.join(ROOT, "_build")
 SOURCES = ["gemm.hip", "attention.hip", "attention_mfma.hip", "rowops.hip",
-           "objective.hip", "optim.hip", "zl.cpp", "runtime.cpp"]
+           "objective.hip", "optim.hip", "zl.cpp", "runtime.cpp", "noalloc.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -27,6 +27,7 @@ EXPORTED = [
     "zl_pipeline_entry_bytes", "zl_pipeline_create", "zl_pipeline_submit", "zl_pipeline_read_output",
     "zl_pipeline_sync", "zl_pipeline_progress", "zl_pipeline_checkpoint", "zl_pipeline_destroy",
     "zl_chunk_save", "zl_chunk_load", "zl_checkpoint_read_info",
+    "zl_kernel_attention_bwd_noalloc",
 ]
 
 
@@ -118,6 +119,8 @@ def load(path=None):
                            vp],
         "zl_kernel_attention": [c, c, c, c, c, vp, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, vp,
                                 c, c, vp],
+        "zl_kernel_attention_bwd_noalloc": [c, c, c, c, c, vp, vp, vp, i64, vp, vp, vp, vp, vp,
+                                            vp, vp, c, vp],
         "zl_profile_begin": [vp, c],
         "zl_profile_end": [vp, P(zl_profile_entry), P(c)],
         "zl_device_info": [c, P(c), P(c), ctypes.c_char_p, c],
@@ -265,6 +268,13 @@ def zl_kernel_attention(B, S, Hq, Hkv, hd, q, k, v, ld_qkv, seq_lens, o, lse, do
     _check(load().zl_kernel_attention(B, S, Hq, Hkv, hd, q, k, v, ld_qkv, seq_lens, o, lse, dout,
                                       dq, dk, dv, delta, dtype, int(backward), stream),
            "zl_kernel_attention")
+
+
+def zl_kernel_attention_bwd_noalloc(B, S, Hq, Hkv, hd, q, k, v, ld_qkv, seq_lens, o, lse, dout,
+                                    dq, dk, dv, dtype, stream=0):
+    _check(load().zl_kernel_attention_bwd_noalloc(B, S, Hq, Hkv, hd, q, k, v, ld_qkv, seq_lens, o,
+                                                  lse, dout, dq, dk, dv, dtype, stream),
+           "zl_kernel_attention_bwd_noalloc")
 
 
 def zl_profile_begin(h, capacity=4096):
