@@ -144,6 +144,38 @@ def copy_calibration(nbytes=1 << 30, reps=3):
                       "copy_gbs": round(2 * nbytes / (med / 1e3) / 1e9, 1)}))
 
 
+def gemm_compare(shape, reps=5):
+    """One bf16 GEMM C[M, N] = A[M, K] B[N, K]^T (both operands K-major, the
+    layout of the chunk's forward linears and head) with libzl's kernel and
+    with torch.matmul (hipBLASLt), `reps` times each, event-timed: the
+    reference for profiling the two kernels side by side."""
+    import torch
+    from paper_2608_07974_amd import zl
+    M, N, K = (int(x) for x in shape.split(","))
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev).manual_seed(0)
+    A = torch.randn(M, K, device=dev, generator=g).bfloat16()
+    B = torch.randn(N, K, device=dev, generator=g).bfloat16()
+    C = torch.empty(M, N, device=dev)
+    s = torch.cuda.current_stream().cuda_stream
+    runs = {"libzl": lambda: zl.zl_kernel_gemm(M, N, K, A.data_ptr(), K, True, B.data_ptr(), K,
+                                               True, C.data_ptr(), N, zl.ZL_BF16, s),
+            "torch.matmul": lambda: torch.matmul(A, B.t())}
+    out = {"gemm": [M, N, K]}
+    for name, f in runs.items():
+        f()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            f()
+        b.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / reps
+        out[name] = {"ms": round(ms, 4), "tflops": round(2.0 * M * N * K / ms / 1e9, 1)}
+    print(json.dumps(out))
+
+
 def pipeline_bench(args):
     """K chunks of `--config` chained as a stage pipeline on one GPU (one
     stream per stage, early forwarding, update window `--window`) against
@@ -249,12 +281,17 @@ def main():
     ap.add_argument("--profile-json", default=None, help="write the per-kernel profile here")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (counter calibration) and exit")
+    ap.add_argument("--gemm-compare", default=None,
+                    help="M,N,K: time one K-major bf16 GEMM with libzl and with torch.matmul")
     ap.add_argument("--pipeline", type=int, default=0,
                     help="K > 0: time K chunks as a stage pipeline instead (one JSON line)")
     ap.add_argument("--window", type=int, default=1, help="update window (with --pipeline)")
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.gemm_compare:
+        gemm_compare(args.gemm_compare, reps=args.steps)
         return
     if args.pipeline > 0:
         if args.gpus != 1:
