@@ -1,7 +1,8 @@
 """Summarise rocprofv3 output.
 
-Kernel trace (rocpd SQLite output) as markdown:
-    python -m paper_2608_07974_amd.profile_summary RESULTS_DB [--top N]
+Kernel trace (rocpd SQLite output, or the kernel_stats.csv of
+--output-format csv) as markdown:
+    python -m paper_2608_07974_amd.profile_summary RESULTS_DB|KERNEL_STATS_CSV [--top N]
 prints per kernel: calls, total and average duration (from the trace's
 top_kernels view), and the share of the traced GPU time.
 
@@ -36,6 +37,18 @@ def summarise(db_path, top=20):
     for name, calls, total, avg, pct in rows[:top]:
         short = name.split("(")[0].replace("void ", "")
         out.append(f"| `{short}` | {calls} | {total / 1e3:.2f} | {avg:.1f} | {pct:.2f} |")
+    return "\n".join(out)
+
+
+def summarise_stats_csv(path, top=20):
+    """The same table from the kernel_stats.csv that --stats writes with
+    --output-format csv."""
+    rows = sorted(_csv_rows(path), key=lambda r: -float(r["TotalDurationNs"]))
+    out = ["| kernel | calls | total ms | avg us | share % |", "|---|---:|---:|---:|---:|"]
+    for r in rows[:top]:
+        short = r["Name"].split("(")[0].replace("void ", "")
+        out.append(f"| `{short}` | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.2f} | "
+                   f"{float(r['AverageNs']) / 1e3:.1f} | {float(r['Percentage']):.2f} |")
     return "\n".join(out)
 
 
@@ -188,6 +201,8 @@ if __name__ == "__main__":
         with open(a.traffic_record, "w") as f:
             json.dump({"kernels": [rec]}, f, indent=1)
         print(json.dumps(rec, indent=1))
+    elif a.db and a.db.endswith(".csv"):
+        print(summarise_stats_csv(a.db, a.top))
     elif a.pmc:
         for c, (n, mean) in sorted(pmc_means(a.pmc, a.kernel).items()):
             print(f"{c}: dispatches {n}, mean per dispatch {mean:.6g}")
