@@ -134,6 +134,25 @@ __device__ inline void dma16(uint32_t lds_byte, uint32_t voff, i32x4_t rsrc) {
                : "memory");
 }
 __device__ inline void dma_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// 4 bytes per lane: lane i's dword lands at M0 + 4 i
+__device__ inline void dma4(uint32_t lds_byte, uint32_t voff, i32x4_t rsrc) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+               :
+               : "s"(lds_byte), "v"(voff), "s"(rsrc)
+               : "memory");
+}
+// A resource of `bytes` bytes: offsets at or past it read as zero.
+__device__ inline i32x4_t buffer_rsrc_n(const void* base, uint32_t bytes) {
+  i32x4_t r = buffer_rsrc(base);
+  r[2] = (int32_t)bytes;
+  return r;
+}
+// s_waitcnt vmcnt(N), other counters unconstrained (gfx9 encoding)
+template <int N>
+__device__ inline void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
 
 template <int HD, int NT>
 struct TileDma {
@@ -388,18 +407,30 @@ __global__ void __launch_bounds__(256) attn_delta_mfma(AttnDesc a) {
 // ------------------------------------------------------------------- dK dV
 // One workgroup per (128 keys, kv-head): 8 waves of 16 keys walk every
 // (q-head, query tile) pair of the kv group; the pair's Q and dO tiles are
-// copied direct-to-LDS once for all waves.  16 keys per wave keeps the K/V
-// fragments and the fp32 dK/dV accumulators within two waves per SIMD.
+// copied direct-to-LDS once for all waves, KV_NST - 1 pairs ahead of use, with
+// the pair's 64 softmax statistics (lse, delta).  16 keys per wave keeps
+// the K/V fragments and the fp32 dK/dV accumulators within two waves per
+// SIMD.
 constexpr int KV_WAVES = 8;
 constexpr int KV_NT = KV_WAVES * 64;
+#ifndef KV_NST
+#define KV_NST 2
+#endif
+#ifndef DKV_CA
+#define DKV_CA 3
+#endif
+template <int HD>
+constexpr size_t dkv_lds_bytes() {  // KV_NST x (Q | dO tiles, lse | delta of 64 queries)
+  return (size_t)KV_NST * (2 * BT * HD * 2 + 2 * BT * 4);
+}
 
 template <int HD>
 __global__ void __launch_bounds__(KV_NT) attn_dkv_mfma(AttnDesc a) {
   constexpr uint32_t TB = BT * HD * 2;     // one Q or dO tile
-  constexpr uint32_t STAGE = 2 * TB;       // Q | dO
-  constexpr uint32_t STAT0 = 2 * STAGE;    // [stage][lse2 64 | delta 64] floats
+  constexpr uint32_t STAGE = 2 * TB + 2 * BT * 4;  // Q | dO | lse 64 | delta 64
+  constexpr int NST = KV_NST;
+  static_assert(NST >= 2 && NST <= 4 && NST * STAGE <= 160 * 1024, "pipeline depth");
   extern __shared__ __align__(16) unsigned char smem[];
-  float* stat = reinterpret_cast<float*>(smem + STAT0);
   const CausalOrder co = causal_order();
   const int kblk = co.x;                   // early keys see the most queries: first
   const int kvh = co.y, b = co.z;
@@ -440,43 +471,56 @@ __global__ void __launch_bounds__(KV_NT) attn_dkv_mfma(AttnDesc a) {
   dd_.init(lane, a.lddo);
   const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>(smem);
   const int64_t so_b = (int64_t)b * a.Hq * a.S;
-  float st_l = 0.f, st_d = 0.f;  // statistics of query (tile row lane), wave 0
-  auto issue = [&](int pr) {
+  // Copies of pair pr into stage pr % NST: the Q and dO tiles (every wave
+  // its share) and, by wave 0, the pair's lse and delta rows (one dword per
+  // lane; queries past S read as zero)
+  constexpr int PER = 2 * TileDma<HD, KV_NT>::ITEMS;  // tile copies per wave and pair
+  auto issue = [&](int pr, int stage) {
     const int h = kvh * grp + pr / ntq;
     const int q0 = k0 + (pr % ntq) * BT;
-    const uint32_t dst = lds0 + (pr & 1) * STAGE;
+    const uint32_t dst = lds0 + (uint32_t)stage * STAGE;
     dq_.issue(dst, wave, q0, a.S, buffer_rsrc(Q + rowb * a.ldq + (int64_t)h * HD));
     dd_.issue(dst + TB, wave, q0, a.S, buffer_rsrc(DO + rowb * a.lddo + (int64_t)h * HD));
     if (wave == 0) {
-      const int q = q0 + lane;
       const int64_t so = so_b + (int64_t)h * a.S;
-      const float lse = q < a.S ? a.lse[so + q] : -INFINITY;
-      st_l = lse == -INFINITY ? INFINITY : lse * LOG2E;  // p = 0 for such queries
-      st_d = q < a.S ? a.delta[so + q] : 0.f;
+      const uint32_t bytes = (uint32_t)a.S * 4u;
+      const uint32_t vo = (uint32_t)(q0 + lane) * 4u;
+      dma4(dst + 2 * TB, vo, buffer_rsrc_n(a.lse + so, bytes));
+      dma4(dst + 2 * TB + BT * 4, vo, buffer_rsrc_n(a.delta + so, bytes));
     }
   };
-  auto commit = [&](int pr) {
+  // this wave's copies of pair pr have landed once at most `ahead` later
+  // pairs' copies are still outstanding
+  auto wait_pair = [&](int ahead) {
     if (wave == 0) {
-      float* sp = stat + (pr & 1) * 2 * BT;
-      sp[lane] = st_l;
-      sp[BT + lane] = st_d;
+      if (ahead >= 2) wait_vm<2 * (PER + 2)>();
+      else if (ahead == 1) wait_vm<PER + 2>();
+      else wait_vm<0>();
+    } else {
+      if (ahead >= 2) wait_vm<2 * PER>();
+      else if (ahead == 1) wait_vm<PER>();
+      else wait_vm<0>();
     }
   };
-  if (npair > 0) {
-    issue(0);
-    commit(0);
-  }
+  static_assert(2 * (PER + 2) < 64, "vmcnt range");
+  for (int p = 0; p < NST - 1 && p < npair; ++p) issue(p, p);
+  int rd = 0, wr = NST - 1;  // stage read by pair pr, stage written for pair pr + NST - 1
+#pragma unroll 1
   for (int pr = 0; pr < npair; ++pr) {
-    dma_wait();
-    __syncthreads();  // tiles of pair pr everywhere; the other stage is free
-    if (pr + 1 < npair) issue(pr + 1);
+    wait_pair(min(NST - 2, npair - 1 - pr));
+    __syncthreads();  // pair pr's copies everywhere; stage wr (read by pair pr - 1) is free
+    if (pr + NST - 1 < npair) issue(pr + NST - 1, wr);
     const int q0 = k0 + (pr % ntq) * BT;
-    const bf16_t* qt = reinterpret_cast<const bf16_t*>(smem + (pr & 1) * STAGE);
+    const unsigned char* sb = smem + rd * STAGE;
+    rd = rd + 1 == NST ? 0 : rd + 1;
+    wr = wr + 1 == NST ? 0 : wr + 1;
+    const bf16_t* qt = reinterpret_cast<const bf16_t*>(sb);
     const bf16_t* dt = qt + BT * HD;
-    const float* l2s = stat + (pr & 1) * 2 * BT;
-    const float* dls = l2s + BT;
+    const float* lss = reinterpret_cast<const float*>(sb + 2 * TB);  // lse (natural log)
+    const float* dls = lss + BT;
     // some key of the wave lies after some query of the tile, or keys or
-    // queries run past their ends
+    // queries run past their ends (every query before S sees key 0, so its
+    // lse is finite; queries past S read lse = 0 and are masked)
     const bool masked = kw0 + 15 > q0 || q0 + BT > a.S || kw0 + 16 > klim;
     // Fragment reads run one step ahead of the MFMAs that use them: the Q /
     // dO row fragments of the next 16-query block, and the transposed dO / Q
@@ -508,36 +552,46 @@ __global__ void __launch_bounds__(KV_NT) attn_dkv_mfma(AttnDesc a) {
           sc = mfma16(fq[cur][kk], kf[kk], sc);
           dp = mfma16(fd[cur][kk], vf[kk], dp);
         }
+        // the mask as one uniform branch over the block's four scores
+        // (most pairs skip it), not a select per score
+        float x[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) x[r] = sc[r] * cs - lss[qb * 16 + 4 * g + r] * LOG2E;
+        if (masked) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int q = q0 + qb * 16 + 4 * g + r;
+            x[r] = (kj <= q && q < a.S && kj < klim) ? x[r] : -INFINITY;
+          }
+        }
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int ql = qb * 16 + 4 * g + r;
-          float x = sc[r] * cs - l2s[ql];
-          if (masked) {
-            const int q = q0 + ql;
-            x = (kj <= q && q < a.S && kj < klim) ? x : -INFINITY;
-          }
-          const float p = __builtin_amdgcn_exp2f(x);
+          const float p = __builtin_amdgcn_exp2f(x[r]);
           pk[qq * 4 + r] = (__bf16)p;
-          dsk[qq * 4 + r] = (__bf16)(p * (dp[r] - dls[ql]));
+          dsk[qq * 4 + r] = (__bf16)(p * (dp[r] - dls[qb * 16 + 4 * g + r]));
         }
       }
       // dV += P^T dO, dK += dS^T Q over this half's 32 queries
-      bf16x8_t dcol[2], qcol[2];
-      dcol[0] = frag_col<HD>(dt, 32 * half, g, 0, c);
-      qcol[0] = frag_col<HD>(qt, 32 * half, g, 0, c);
+      // (transposed dO / Q column fragments: a ring of CA reads in flight)
+      constexpr int NCOL = HD / 16, CA = DKV_CA;
+      bf16x8_t dcol[CA], qcol[CA];
 #pragma unroll
-      for (int db = 0; db < HD / 16; ++db) {
-        const int cur = db & 1;
-        if (db + 1 < HD / 16) {
-          dcol[cur ^ 1] = frag_col<HD>(dt, 32 * half, g, 16 * (db + 1), c);
-          qcol[cur ^ 1] = frag_col<HD>(qt, 32 * half, g, 16 * (db + 1), c);
-        }
+      for (int i = 0; i < CA; ++i) {
+        dcol[i] = frag_col<HD>(dt, 32 * half, g, 16 * i, c);
+        qcol[i] = frag_col<HD>(qt, 32 * half, g, 16 * i, c);
+      }
+#pragma unroll
+      for (int db = 0; db < NCOL; ++db) {
+        const int cur = db % CA;
         __builtin_amdgcn_sched_barrier(0);
         dv[db] = mfma16(pk, dcol[cur], dv[db]);
         dk[db] = mfma16(dsk, qcol[cur], dk[db]);
+        if (db + CA < NCOL) {
+          dcol[cur] = frag_col<HD>(dt, 32 * half, g, 16 * (db + CA), c);
+          qcol[cur] = frag_col<HD>(qt, 32 * half, g, 16 * (db + CA), c);
+        }
       }
     }
-    if (pr + 1 < npair) commit(pr + 1);
   }
   dma_wait();
   bf16_t* DK = reinterpret_cast<bf16_t*>(a.dk);
@@ -662,16 +716,27 @@ __global__ void __launch_bounds__(FW_NT) attn_dq_mfma(AttnDesc a) {
           dpt[j] = mfma16(va[cur], df[j][kk], dpt[j]);
         }
       }
+      // the mask as one uniform branch over the block's eight scores (most
+      // tiles skip it), not a select per score
+      float x[2][4];
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) x[j][r] = st[j][r] * cs - l2[j];
+      if (masked) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int key = k0 + blk * 16 + 4 * g + r;
+            x[j][r] = (key <= qi[j] && key < kend) ? x[j][r] : -INFINITY;
+          }
+      }
 #pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          float x = st[j][r] * cs - l2[j];
-          if (masked) {
-            const int key = k0 + blk * 16 + 4 * g + r;
-            x = (key <= qi[j] && key < kend) ? x : -INFINITY;
-          }
-          const float p = __builtin_amdgcn_exp2f(x);
+          const float p = __builtin_amdgcn_exp2f(x[j][r]);
           dsk[j][blk >> 1][(blk & 1) * 4 + r] = (__bf16)(p * (dpt[j][r] - dl[j]));
         }
     }
@@ -752,8 +817,7 @@ static hipError_t dq_hpw(const AttnDesc& a, hipStream_t s) {
 
 template <int HD>
 static hipError_t bwd(const AttnDesc& a, hipStream_t s) {
-  // 2 stages x (Q + dO) tiles + 2 stages x (lse, delta) of 64 queries
-  const size_t lds_kv = (size_t)4 * BT * HD * sizeof(bf16_t) + 4 * BT * sizeof(float);
+  const size_t lds_kv = dkv_lds_bytes<HD>();
   static bool once = false;
   if (!once) {
     hipError_t e = set_lds(attn_dkv_mfma<HD>, lds_kv);

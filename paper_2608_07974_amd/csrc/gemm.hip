@@ -1,7 +1,7 @@
 // GEMM kernels for every linear of the chunk map (Eq. (1)) and the frozen
 // readout head (Eq. (2)), forward, data-gradient and weight-gradient forms.
 //
-// bf16: MFMA 32x32x16 (fp32 accumulate) on LDS double-buffered tiles with
+// bf16: MFMA 16x16x32 or 32x32x16 (fp32 accumulate) on LDS tiles with
 // 16-byte XOR-swizzled rows and an XCD-aware tile order so tiles sharing
 // operand panels run on one L2.  The main path copies tiles global -> LDS
 // with the buffer unit's direct-to-LDS loads and reads MN-major operands
@@ -22,6 +22,28 @@ namespace zl {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// The two bf16 MFMA shapes (fp32 accumulate).  MF x MF output block, KS-deep
+// k slice; every lane supplies 8 bf16 of A and of B.  Output register r of
+// lane l holds row row(l, r), column l % MF.
+template <int MF> struct Mma;
+template <> struct Mma<32> {  // v_mfma_f32_32x32x16_bf16: A row l & 31, k 8 (l >> 5) .. +7
+  using acc_t = f32x16_t;
+  static constexpr int KS = 16, NR = 16;
+  __device__ static inline acc_t run(bf16x8_t a, bf16x8_t b, acc_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+  __device__ static constexpr int row(int l, int r) { return 8 * (r >> 2) + 4 * (l >> 5) + (r & 3); }
+};
+template <> struct Mma<16> {  // v_mfma_f32_16x16x32_bf16: A row l & 15, k 8 (l >> 4) .. +7
+  using acc_t = f32x4_t;
+  static constexpr int KS = 32, NR = 4;
+  __device__ static inline acc_t run(bf16x8_t a, bf16x8_t b, acc_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+  __device__ static constexpr int row(int l, int r) { return 4 * (l >> 4) + r; }
+};
 
 // ---------------------------------------------------------------- epilogue
 __device__ inline float silu_f(float g) { return g / (1.f + __expf(-g)); }
@@ -287,12 +309,13 @@ __device__ inline void tile_coords(int b, int nbm, int nbn, int& tm, int& tn) {
 // accumulators are written with compile-time indices (so they stay in
 // registers), then read back row-contiguously, which coalesces the global
 // stores of the epilogue.  Callers end their main loop with a barrier.
-template <int BM, int BN, int WM, int WN>
-__device__ __forceinline__ void store_tile(const f32x16_t (&acc)[BM / WM / 32][BN / WN / 32],
+template <int BM, int BN, int WM, int WN, int MF = 32>
+__device__ __forceinline__ void store_tile(const typename Mma<MF>::acc_t (&acc)[BM / WM / MF][BN / WN / MF],
                                   unsigned char* smem, const GemmDesc& g, const EpiArgs& e,
                                   int m0, int n0, int wave, int lane) {
+  using acc_t = typename Mma<MF>::acc_t;
   constexpr int TM = BM / WM, TN = BN / WN;
-  constexpr int FM = TM / 32, FN = TN / 32;
+  constexpr int FM = TM / 32, FN = TN / MF;
   const int wm = wave / WN, wn = wave % WN;
   constexpr int LDW = TN + 4;
   static_assert(WM * WN * 32 * LDW * 4 <= 160 * 1024, "epilogue tile exceeds LDS");
@@ -301,12 +324,16 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[BM / WM / 32][B
   // One 32-row block per call; the calls are spelled out (not a loop) so
   // that every acc index stays a compile-time constant however large the
   // epilogue grows (a rolled loop would move acc to scratch memory).
-  auto chunk = [&](const f32x16_t (&ai)[FN], const int i) __attribute__((always_inline)) {
+  // a0: the 32 rows' accumulators (MF 32), or those of their first 16 rows
+  // with a1 those of the second 16 (MF 16)
+  auto chunk = [&](const acc_t (&a0)[FN], const acc_t (&a1)[FN], const int i) __attribute__((always_inline)) {
 #pragma unroll
-    for (int j = 0; j < FN; ++j)
+    for (int h = 0; h < 32 / MF; ++h)
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        ep[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * LDW + j * 32 + (lane & 31)] = ai[j][r];
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int r = 0; r < Mma<MF>::NR; ++r)
+          ep[(h * MF + Mma<MF>::row(lane, r)) * LDW + j * MF + (lane & (MF - 1))] = (h ? a1 : a0)[j][r];
     __syncthreads();
     const int mb = m0 + wm * TM + i * 32, nb = n0 + wn * TN;
     // EW consecutive columns per lane: a row of TN columns takes TN / EW lanes
@@ -508,10 +535,11 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[BM / WM / 32][B
     __syncthreads();
   };
   static_assert(FM >= 1 && FM <= 4, "32-row blocks per wave tile");
-  chunk(acc[0], 0);
-  if constexpr (FM > 1) chunk(acc[1], 1);
-  if constexpr (FM > 2) chunk(acc[2], 2);
-  if constexpr (FM > 3) chunk(acc[3], 3);
+  constexpr int S = 32 / MF;  // accumulator row blocks per 32-row block
+  chunk(acc[0], acc[S - 1], 0);
+  if constexpr (FM > 1) chunk(acc[S], acc[2 * S - 1], 1);
+  if constexpr (FM > 2) chunk(acc[2 * S], acc[3 * S - 1], 2);
+  if constexpr (FM > 3) chunk(acc[3 * S], acc[4 * S - 1], 3);
 }
 
 // ------------------------------------------------------------ MFMA kernel
@@ -728,7 +756,7 @@ gemm_mfma_kernel(GemmDesc g, EpiArgs e) {
 // resource's record count reads as zero), so no staging registers, no LDS
 // store instructions and no transposes.  LDS layouts:
 //   K-major operand  [row][64 k],  16-B chunk c of row r at c ^ ((r >> 1) & 7)
-//   MN-major operand [k][R],       16-B chunk c of row k at c ^ xs(k & 3)
+//   MN-major operand [k][R],       16-B chunk c of row k at c ^ xsk<MF>(k)
 // and the DMA lane -> global mapping applies the inverse swizzle.  MN-major
 // fragments are read with the LDS transpose read (ds_read_b64_tr_b16).
 typedef int32_t i32x4_t __attribute__((ext_vector_type(4)));
@@ -750,6 +778,12 @@ __device__ inline i32x4_t buffer_rsrc(const void* base) {
 // values differ in bits 2-3 (distinct 64-byte bank groups for a half-wave
 // transpose read) and in bits 1-2 (distinct 32-byte groups for 16 lanes).
 __device__ inline int xs(int b) { return (0xCA60 >> (4 * b)) & 15; }
+// The swizzle of LDS row k of an MN-major tile read as MF x MF fragments.
+// A half-wave of 16x16 transpose reads covers k rows k0 .. k0 + 3 and
+// k0 + 8 .. k0 + 11 (32 bytes each); folding bit 3 of k into the swizzle
+// puts those 8 rows in 8 distinct 32-byte groups.
+template <int MF>
+__device__ inline int xsk(int k) { return MF == 16 ? xs(k & 3) ^ (k & 8) : xs(k & 3); }
 
 extern "C" __device__ i32x4_t llvm_amdgcn_raw_buffer_load_v4i32(i32x4_t rsrc, uint32_t voffset,
                                                                  uint32_t soffset, int aux)
@@ -773,7 +807,7 @@ template <int BK>
 __device__ inline int kswz(int row) { return (row / (128 / BK)) % (BK / 8); }
 
 // One operand's BK-deep k tile, R rows of M (or N), copied by NT threads.
-template <int R, int BK, int NT, bool KMAJ>
+template <int R, int BK, int NT, bool KMAJ, int MF = 32>
 struct DmaTile {
   static constexpr int ITEMS = R * BK / 8 / NT;  // 16-B chunks per thread
   static_assert(ITEMS >= 1 && ITEMS * NT == R * BK / 8, "tile chunks must divide over the threads");
@@ -792,7 +826,7 @@ struct DmaTile {
         off[j] = row < rvalid ? (uint32_t)(row * ld) * 2u + (uint32_t)ch * 16u : DMA_OOB;
       } else {
         constexpr int CPR = R / 8;
-        const int k = c / CPR, ch = (c % CPR) ^ xs(k & 3);
+        const int k = c / CPR, ch = (c % CPR) ^ xsk<MF>(k);
         kr[j] = k;
         off[j] = ch * 8 < rvalid ? (uint32_t)(k * ld) * 2u + (uint32_t)ch * 16u : DMA_OOB;
       }
@@ -833,22 +867,24 @@ struct DmaTile {
   }
 };
 
-// Per-lane LDS fragment addressing of one operand for the 32x32x16 MFMA:
-// lane l supplies row (l & 31) and k 8 (l >> 5) .. +7 of the 16-deep slice.
-template <int R, int BK, int F, bool KMAJ>
+// Per-lane LDS fragment addressing of one operand for the MF x MF MFMA
+// (Mma<MF>): lane l supplies row l % MF and k 8 (l / MF) .. +7 of the
+// KS-deep slice.  F fragments of MF rows each.
+template <int R, int BK, int F, bool KMAJ, int MF = 32>
 struct FragTile {
-  static constexpr int NS = BK / 16;
+  static constexpr int KS = Mma<MF>::KS;
+  static constexpr int NS = BK / KS;
   static constexpr int NO = KMAJ ? NS : F;
   int off[NO];  // element offsets: per slice (K-major) or per fragment (MN-major)
 
   __device__ inline void init(int wrow, int lane) {
     if (KMAJ) {
-      // fragment rows step by 32, which keeps kswz (period 128/BK rows x
-      // BK/8 chunks <= 32 rows) unchanged: fragment i adds i * 32 * BK
-      const int l = lane & 31, h = lane >> 5, sw = kswz<BK>(l);
+      // fragment rows step by MF, which keeps kswz (period 128/BK rows x
+      // BK/8 chunks = 16 rows) unchanged: fragment i adds i * MF * BK
+      const int l = lane & (MF - 1), h = lane / MF, sw = kswz<BK>(l);
 #pragma unroll
-      for (int q = 0; q < NS; ++q) off[q] = (wrow + l) * BK + (((2 * q + h) ^ sw) * 8);
-    } else {
+      for (int q = 0; q < NS; ++q) off[q] = (wrow + l) * BK + ((((KS / 8) * q + h) ^ sw) * 8);
+    } else if (MF == 32) {
       // transpose read: lane r of 16-lane group G addresses k row
       // 8 (G >> 1) + (r >> 2) (+ 16 q + 4 t) and the 4 elements at
       // m = wrow + 32 i + 16 (G & 1) + 4 (r & 3); it receives column
@@ -858,13 +894,24 @@ struct FragTile {
       const int P = (wrow >> 3) ^ (2 * (G & 1) + ((r >> 1) & 1)) ^ xs(r >> 2);
 #pragma unroll
       for (int i = 0; i < F; ++i) off[i] = kl * R + ((P ^ (4 * i)) << 3) + 4 * (r & 1);
+    } else {
+      // transpose read: lane r of 16-lane group G addresses k row
+      // 8 G + (r >> 2) (+ 32 q + 4 t) and the 4 elements at
+      // m = wrow + 16 i + 4 (r & 3); it receives column m = ... + r of
+      // those 4 k rows.  wrow is a multiple of 64, so the chunk index
+      // (wrow >> 3) + 2 i + ((r >> 1) & 1) equals its XOR form.
+      const int G = lane >> 4, r = lane & 15;
+      const int kl = 8 * G + (r >> 2);
+      const int P = (wrow >> 3) ^ ((r >> 1) & 1) ^ xsk<16>(kl);
+#pragma unroll
+      for (int i = 0; i < F; ++i) off[i] = kl * R + ((P ^ (2 * i)) << 3) + 4 * (r & 1);
     }
   }
   __device__ inline bf16x8_t read(const bf16_t* tile, int q, int i) const {
     if (KMAJ) {
-      return *reinterpret_cast<const bf16x8_t*>(tile + off[q] + i * 32 * BK);
+      return *reinterpret_cast<const bf16x8_t*>(tile + off[q] + i * MF * BK);
     } else {
-      const bf16_t* p = tile + off[i] + 16 * q * R;
+      const bf16_t* p = tile + off[i] + KS * q * R;
       const s16x4_t x = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
           (__attribute__((address_space(3))) s16x4_t*)(p));
       const s16x4_t y = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
@@ -885,21 +932,28 @@ __device__ inline void wait_vmcnt() {
 // NST-stage pipeline: the tile NST - 1 steps ahead is in flight while the
 // current one is multiplied; one barrier per BK-deep tile.  bl is the
 // block's index among the tiles of its problem.
-template <int BM, int BN, int WM, int WN, int BK, int NST, int DS, bool AK, bool BKM, bool RA, bool RB>
+template <int BM, int BN, int WM, int WN, int BK, int NST, int DS, bool AK, bool BKM, bool RA, bool RB, int MF>
 __device__ __forceinline__ void gemm_dma_body(const GemmDesc& g, const EpiArgs& e, const int bl,
                                               unsigned char* smem) {
   constexpr int NT = WM * WN * 64;
   constexpr int TM = BM / WM, TN = BN / WN;
-  constexpr int FM = TM / 32, FN = TN / 32;
-  constexpr int NS = BK / 16;
+  using M = Mma<MF>;
+  using acc_t = typename M::acc_t;
+  constexpr int FM = TM / MF, FN = TN / MF;
+  constexpr int NS = BK / M::KS;
+  // fragments of the next slice: double-buffered (MF 32), or refilled in
+  // place right after their last use in the current slice (MF 16, whose
+  // twice as many fragments would not fit twice beside the accumulators)
+  constexpr int FB = MF == 32 ? 2 : 1;
   constexpr uint32_t ABYTES = BM * BK * 2, STAGE = (BM + BN) * BK * 2;
-  using TA = DmaTile<BM, BK, NT, AK>;
-  using TB = DmaTile<BN, BK, NT, BKM>;
+  using TA = DmaTile<BM, BK, NT, AK, MF>;
+  using TB = DmaTile<BN, BK, NT, BKM, MF>;
   constexpr int PER_TILE = TA::ITEMS + TB::ITEMS;  // DMA instructions per wave per tile
   static_assert(NST >= 2 && (NST - 2) * PER_TILE < 64, "pipeline depth");
   static_assert(!(RA || RB) || NST == 2, "register staging uses two stages");
-  static_assert(DS >= 1 && DS < NS, "the tile copy is spread over slices before the last");
-  static_assert(NS % 2 == 0, "slice parity must repeat per tile");
+  static_assert(GEMM_IL == 2 || (DS >= 1 && DS < NS), "the tile copy is spread over slices before the last");
+  static_assert(MF == 16 || NS % 2 == 0, "slice parity must repeat per tile");
+  static_assert(MF == 32 || GEMM_IL, "16x16 fragments use the interleaved schedule");
 
   const int nbm = (g.M + BM - 1) / BM, nbn = (g.N + BN - 1) / BN;
   int tm, tn;
@@ -920,18 +974,18 @@ __device__ __forceinline__ void gemm_dma_body(const GemmDesc& g, const EpiArgs& 
   TB db;
   da.init(wave, lane, g.lda, min(g.M - m0, BM));
   db.init(wave, lane, g.ldb, min(g.N - n0, BN));
-  FragTile<BM, BK, FM, AK> fa;
-  FragTile<BN, BK, FN, BKM> fb;
+  FragTile<BM, BK, FM, AK, MF> fa;
+  FragTile<BN, BK, FN, BKM, MF> fb;
   fa.init(wm * TM, lane);
   fb.init(wn * TN, lane);
 
-  f32x16_t acc[FM][FN];
+  acc_t acc[FM][FN];
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
     for (int j = 0; j < FN; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+      for (int r = 0; r < M::NR; ++r) acc[i][j][r] = 0.f;
 
   const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>(smem);
   const int nk = (klen + BK - 1) / BK;
@@ -952,7 +1006,7 @@ __device__ __forceinline__ void gemm_dma_body(const GemmDesc& g, const EpiArgs& 
   // before the MFMAs of tile kt's last slice, whose fragments are already
   // in registers, so slice 0 of tile kt+1 is read while they run and the
   // barrier also certifies that every wave is done reading tile kt.
-  bf16x8_t af[2][FM], bfr[2][FN];
+  bf16x8_t af[FB][FM], bfr[FB][FN];
 #pragma unroll
   for (int i = 0; i < FM; ++i) af[0][i] = fa.read(reinterpret_cast<const bf16_t*>(smem), 0, i);
 #pragma unroll
@@ -976,7 +1030,7 @@ __device__ __forceinline__ void gemm_dma_body(const GemmDesc& g, const EpiArgs& 
     static_assert(!RA && !RB, "interleaved schedule uses direct-to-LDS copies");
 #pragma unroll
     for (int q = 0; q < NS; ++q) {
-      const int cb = q & 1, nb = cb ^ 1;
+      const int cb = FB == 2 ? q & 1 : 0, nb = FB == 2 ? cb ^ 1 : 0;
       const bf16_t* src = q + 1 < NS ? as : an;
       const int qs = q + 1 < NS ? q + 1 : 0;
       if (q + 1 == NS) {
@@ -997,13 +1051,20 @@ __device__ __forceinline__ void gemm_dma_body(const GemmDesc& g, const EpiArgs& 
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int t = 0; t < NMF; ++t) {
-        acc[t / FN][t % FN] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            af[cb][t / FN], bfr[cb][t % FN], acc[t / FN][t % FN], 0, 0, 0);
+        acc[t / FN][t % FN] = M::run(af[cb][t / FN], bfr[cb][t % FN], acc[t / FN][t % FN]);
+        if constexpr (FB == 2) {
 #pragma unroll
-        for (int r = 0; r < NRD; ++r) {
-          if (r * NMF / NRD != t) continue;
-          if (r < FM) af[nb][r] = fa.read(src, qs, r);
-          else bfr[nb][r - FM] = fb.read(src + BM * BK, qs, r - FM);
+          for (int r = 0; r < NRD; ++r) {
+            if (r * NMF / NRD != t) continue;
+            if (r < FM) af[nb][r] = fa.read(src, qs, r);
+            else bfr[nb][r - FM] = fb.read(src + BM * BK, qs, r - FM);
+          }
+        } else {
+          // rows i of A end at t = i FN + FN - 1; B columns are used
+          // until the last row, the row the MFMAs run in order of
+          const int ti = t / FN, tj = t % FN;
+          if (ti + 1 == FM) bfr[0][tj] = fb.read(src + BM * BK, qs, tj);
+          if (tj + 1 == FN) af[0][ti] = fa.read(src, qs, ti);
         }
 #pragma unroll
         for (int u = 0; u < TOT; ++u) {
@@ -1051,7 +1112,7 @@ __device__ __forceinline__ void gemm_dma_body(const GemmDesc& g, const EpiArgs& 
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cb][i], bfr[cb][j], acc[i][j], 0, 0, 0);
+          acc[i][j] = M::run(af[cb][i], bfr[cb][j], acc[i][j]);
       __builtin_amdgcn_sched_barrier(0);
     }
 #endif
@@ -1086,26 +1147,26 @@ __device__ __forceinline__ void gemm_dma_body(const GemmDesc& g, const EpiArgs& 
         for (int i = 0; i < FM; ++i)
 #pragma unroll
           for (int j = 0; j < FN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[0][i], bfr[0][j], acc[i][j], 0, 0, 0);
+            acc[i][j] = M::run(af[0][i], bfr[0][j], acc[i][j]);
       }
       __syncthreads();
     }
   }
-  store_tile<BM, BN, WM, WN>(acc, smem, g, e, m0, n0, wave, lane);
+  store_tile<BM, BN, WM, WN, MF>(acc, smem, g, e, m0, n0, wave, lane);
 }
 
 // One launch, one or two problems of the same layout: blocks below nb1 take
 // (g, e), the rest (g2, e2) (two independent weight gradients share a launch
 // so the last wave of one is filled by the other).  The problem is uniform
 // per block; each branch inlines the body with its own descriptors.
-template <int BM, int BN, int WM, int WN, int BK, int NST, int DS, bool AK, bool BKM, bool RA, bool RB>
+template <int BM, int BN, int WM, int WN, int BK, int NST, int DS, bool AK, bool BKM, bool RA, bool RB, int MF>
 __global__ void __launch_bounds__(WM * WN * 64)
 gemm_dma_kernel(GemmDesc g, EpiArgs e, GemmDesc g2, EpiArgs e2, int nb1) {
   extern __shared__ __align__(16) unsigned char smem[];
   if ((int)blockIdx.x < nb1)
-    gemm_dma_body<BM, BN, WM, WN, BK, NST, DS, AK, BKM, RA, RB>(g, e, blockIdx.x, smem);
+    gemm_dma_body<BM, BN, WM, WN, BK, NST, DS, AK, BKM, RA, RB, MF>(g, e, blockIdx.x, smem);
   else
-    gemm_dma_body<BM, BN, WM, WN, BK, NST, DS, AK, BKM, RA, RB>(g2, e2, blockIdx.x - nb1, smem);
+    gemm_dma_body<BM, BN, WM, WN, BK, NST, DS, AK, BKM, RA, RB, MF>(g2, e2, blockIdx.x - nb1, smem);
 }
 
 // ------------------------------------------------------------ SIMT (fp32)
@@ -1203,9 +1264,22 @@ static const char* layout_tag(bool ak, bool bk) {
 // k-tile depth and stages per operand layout: both K-major (forward) BK 64
 // with two stages; otherwise (an MN-major operand: data and weight
 // gradients) BK 32 with three stages, measured faster in the 8B update
+// MFMA shape per layout: 16x16x32 where an operand is K-major (6-8 %
+// faster than 32x32x16 on the forward shapes, 2-3 % on the data-gradient
+// ones), 32x32x16 when both are MN-major (weight gradients: 0.5 % faster)
+#ifndef GEMM_MF
+#define GEMM_MF 16
+#endif
+#ifndef GEMM_MF_MIX
+#define GEMM_MF_MIX 16
+#endif
+#ifndef GEMM_MF_MN
+#define GEMM_MF_MN 32
+#endif
 template <bool AK, bool BKM> struct KTile {
   static constexpr int BK = AK && BKM ? GEMM_BK : GEMM_BK_MN;
   static constexpr int NST = AK && BKM ? GEMM_NST : GEMM_NST_MN;
+  static constexpr int MF = AK && BKM ? GEMM_MF : (AK || BKM ? GEMM_MF_MIX : GEMM_MF_MN);
 };
 #ifndef GEMM_DS
 #define GEMM_DS 1
@@ -1246,7 +1320,7 @@ static bool splitk_kind_ok(EpiKind k) {
 template <int BM, int BN, int WM, int WN, int BK, int NST, bool AK, bool BKM>
 static hipError_t run_dma(const GemmDesc& g, const EpiArgs& e, hipStream_t s, int nz = 1,
                           const GemmDesc* g2 = nullptr, const EpiArgs* e2 = nullptr) {
-  auto kern = gemm_dma_kernel<BM, BN, WM, WN, BK, NST, GEMM_DS, AK, BKM, GEMM_RA, GEMM_RB>;
+  auto kern = gemm_dma_kernel<BM, BN, WM, WN, BK, NST, GEMM_DS, AK, BKM, GEMM_RA, GEMM_RB, KTile<AK, BKM>::MF>;
   const size_t lds_main = (size_t)NST * (BM + BN) * BK * sizeof(bf16_t);
   const size_t lds_epi = (size_t)WM * WN * 32 * (BN / WN + 4) * sizeof(float);
   const size_t lds = lds_main > lds_epi ? lds_main : lds_epi;
