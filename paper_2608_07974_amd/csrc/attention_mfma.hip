@@ -405,14 +405,17 @@ __global__ void __launch_bounds__(256) attn_delta_mfma(AttnDesc a) {
 }
 
 // ------------------------------------------------------------------- dK dV
-// One workgroup per (128 keys, kv-head): 8 waves of 16 keys walk every
+// One workgroup per (KV_KB keys, kv-head): KV_WAVES waves (8) of 16 keys walk every
 // (q-head, query tile) pair of the kv group; the pair's Q and dO tiles are
 // copied direct-to-LDS once for all waves, KV_NST - 1 pairs ahead of use, with
 // the pair's 64 softmax statistics (lse, delta).  16 keys per wave keeps
 // the K/V fragments and the fp32 dK/dV accumulators within two waves per
 // SIMD.
-constexpr int KV_WAVES = 8;
+#ifndef KV_WAVES
+#define KV_WAVES 8
+#endif
 constexpr int KV_NT = KV_WAVES * 64;
+constexpr int KV_KB = KV_WAVES * 16;  // keys per workgroup
 #ifndef KV_NST
 #define KV_NST 2
 #endif
@@ -425,7 +428,7 @@ constexpr size_t dkv_lds_bytes() {  // KV_NST x (Q | dO tiles, lse | delta of 64
 }
 
 template <int HD>
-__global__ void __launch_bounds__(KV_NT) attn_dkv_mfma(AttnDesc a) {
+__global__ void __launch_bounds__(KV_NT, 2) attn_dkv_mfma(AttnDesc a) {
   constexpr uint32_t TB = BT * HD * 2;     // one Q or dO tile
   constexpr uint32_t STAGE = 2 * TB + 2 * BT * 4;  // Q | dO | lse 64 | delta 64
   constexpr int NST = KV_NST;
@@ -438,7 +441,7 @@ __global__ void __launch_bounds__(KV_NT) attn_dkv_mfma(AttnDesc a) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int c = lane & 15, g = lane >> 4;
   const int L = a.seq_lens[b];
-  const int k0 = kblk * BW;
+  const int k0 = kblk * KV_KB;
   const int kw0 = k0 + wave * 16;
   const int klim = min(a.S, L);
   const int kj = kw0 + c;
@@ -831,7 +834,7 @@ static hipError_t bwd(const AttnDesc& a, hipStream_t s) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  dim3 gk((a.S + BW - 1) / BW, a.Hkv, a.B);
+  dim3 gk((a.S + KV_KB - 1) / KV_KB, a.Hkv, a.B);
   hipLaunchKernelGGL(attn_dkv_mfma<HD>, gk, dim3(KV_NT), lds_kv, s, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -11,6 +11,7 @@
 #include <stdio.h>
 
 #include <cstring>
+#include <type_traits>
 
 #include "common.h"
 
@@ -44,6 +45,17 @@ template <> struct Mma<16> {  // v_mfma_f32_16x16x32_bf16: A row l & 15, k 8 (l 
   }
   __device__ static constexpr int row(int l, int r) { return 4 * (l >> 4) + r; }
 };
+
+// f(std::integral_constant<int, i>) for i = B .. E-1: indices that are
+// compile-time constants by construction, whatever the unroller decides
+// (a register array indexed at run time would live in scratch memory).
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
 
 // ---------------------------------------------------------------- epilogue
 __device__ inline float silu_f(float g) { return g / (1.f + __expf(-g)); }
@@ -133,17 +145,31 @@ __device__ __forceinline__ void ldv_f32(const float* p, float (&v)[EW]) {
     v[k] = f.x; v[k + 1] = f.y; v[k + 2] = f.z; v[k + 3] = f.w;
   }
 }
+__device__ __forceinline__ void unpack_bf16x8(const uint4 u, float (&v)[EW]) {
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    v[2 * k] = bf16_to_f32((bf16_t)(w[k] & 0xffff));
+    v[2 * k + 1] = bf16_to_f32((bf16_t)(w[k] >> 16));
+  }
+}
 __device__ __forceinline__ void ldv_act(const void* p, int dt, size_t i, float (&v)[EW]) {
   if (dt == BF16) {
-    const uint4 u = *reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(p) + i);
-    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      v[2 * k] = bf16_to_f32((bf16_t)(w[k] & 0xffff));
-      v[2 * k + 1] = bf16_to_f32((bf16_t)(w[k] >> 16));
-    }
+    unpack_bf16x8(*reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(p) + i), v);
   } else {
     ldv_f32(static_cast<const float*>(p) + i, v);
+  }
+}
+// dL/dg and dL/du of SwiGLU a = silu(g) u from da, and dL/dh of GELU
+__device__ __forceinline__ void swiglu_bwd8(const float (&da)[EW], const float (&g)[EW],
+                                            const float (&u)[EW], float (&dg)[EW], float (&du)[EW]) {
+#pragma unroll
+  for (int i = 0; i < EW; ++i) {
+    const float sg = __builtin_amdgcn_rcpf(1.f + __expf(-g[i]));  // hardware reciprocal (1 ulp)
+    const float silu = g[i] * sg;
+    const float dsilu = sg * (1.f + g[i] * (1.f - sg));
+    dg[i] = da[i] * u[i] * dsilu;
+    du[i] = da[i] * silu;
   }
 }
 __device__ __forceinline__ void stv_act(void* p, int dt, size_t i, const float (&v)[EW]) {
@@ -233,14 +259,7 @@ __device__ __forceinline__ void epilogue_v(const EpiArgs& e, int M, int N, int m
       float g[EW], u[EW], w[EW];
       ldv_act(e.aux, e.out_dtype, mo * e.ldaux + n, g);
       ldv_act(e.aux, e.out_dtype, mo * e.ldaux + n + e.ff, u);
-#pragma unroll
-      for (int i = 0; i < EW; ++i) {
-        const float sg = __builtin_amdgcn_rcpf(1.f + __expf(-g[i]));  // hardware reciprocal (1 ulp)
-        const float silu = g[i] * sg;
-        const float dsilu = sg * (1.f + g[i] * (1.f - sg));
-        v[i] = a[i] * u[i] * dsilu;
-        w[i] = a[i] * silu;
-      }
+      swiglu_bwd8(a, g, u, v, w);
       stv_act(e.out, e.out_dtype, mo * e.ldo + n, v);
       stv_act(e.out, e.out_dtype, mo * e.ldo + n + e.ff, w);
       break;
@@ -392,31 +411,71 @@ __device__ __forceinline__ void store_tile(const typename Mma<MF>::acc_t (&acc)[
       // the hd / EW lanes of one head's columns in a row sum dO (as stored)
       // times O, giving the attention backward's delta of (row, head)
       const int lph = e.hd / EW;
-      for (int t = lane; t < 32 * QPR; t += 64) {
-        const int row = t / QPR, col = (t % QPR) * EW;
-        const int m = mb + row, n = nb + col;
-        float v[EW];
-#pragma unroll
-        for (int k = 0; k < EW; k += 4) {
-          const float4 x = *reinterpret_cast<const float4*>(&ep[row * LDW + col + k]);
-          v[k] = x.x; v[k + 1] = x.y; v[k + 2] = x.z; v[k + 3] = x.w;
-        }
-        epilogue_v(e, g.M, g.N, m, n, v, vec);
+      auto head_sum = [&](const int m, const int n, const float (&v)[EW], const float (&o)[EW])
+          __attribute__((always_inline)) {
         float ds = 0.f;
-        if (m < g.M && n < g.N) {
-          float o[EW];
-          ldv_act(e.aux, e.out_dtype, (size_t)m * e.ldaux + n, o);
 #pragma unroll
-          for (int k = 0; k < EW; ++k) {
-            const float d = e.out_dtype == BF16 ? bf16_to_f32(f32_to_bf16(e.scale * v[k]))
-                                                : e.scale * v[k];
-            ds += d * o[k];
-          }
+        for (int k = 0; k < EW; ++k) {
+          const float d = e.out_dtype == BF16 ? bf16_to_f32(f32_to_bf16(e.scale * v[k]))
+                                              : e.scale * v[k];
+          ds += d * o[k];
         }
         for (int off = 1; off < lph; off <<= 1) ds += __shfl_xor(ds, off, 64);
         if ((lane & (lph - 1)) == 0 && m < g.M && n < g.N) {
           const int b = m / e.seq, sq = m - b * e.seq, h = n / e.hd;
           e.delta[((int64_t)b * e.nheads + h) * e.seq + sq] = ds;
+        }
+      };
+      if (vec && e.out_dtype == BF16 && mb + 32 <= g.M && nb + TN <= g.N) {
+        // interior rows, bf16: O of all of this lane's column groups is
+        // loaded before any dO is stored (the compiler must assume the
+        // stores may alias the loads, so loads placed between them would
+        // each wait a memory round trip)
+        constexpr int IT = 32 * QPR / 64;
+        static_assert(IT * 64 == 32 * QPR, "column groups must divide over the lanes");
+        uint4 oa[IT];
+        static_for<0, IT>([&](auto ic) __attribute__((always_inline)) {
+          constexpr int it = decltype(ic)::value;
+          const int t = lane + 64 * it, m = mb + t / QPR, n = nb + (t % QPR) * EW;
+          oa[it] = *reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(e.aux) +
+                                                   (size_t)m * e.ldaux + n);
+        });
+        static_for<0, IT>([&](auto ic) __attribute__((always_inline)) {
+          constexpr int it = decltype(ic)::value;
+          const int t = lane + 64 * it, row = t / QPR, col = (t % QPR) * EW;
+          const int m = mb + row, n = nb + col;
+          float v[EW], o[EW];
+#pragma unroll
+          for (int k = 0; k < EW; k += 4) {
+            const float4 x = *reinterpret_cast<const float4*>(&ep[row * LDW + col + k]);
+            v[k] = x.x; v[k + 1] = x.y; v[k + 2] = x.z; v[k + 3] = x.w;
+          }
+          float w[EW], bi[EW];  // dO as the plain store of epilogue_v writes it
+#pragma unroll
+          for (int k = 0; k < EW; ++k) bi[k] = 0.f;
+          if (e.bias) ldv_f32(e.bias + n, bi);
+#pragma unroll
+          for (int k = 0; k < EW; ++k) w[k] = e.scale * v[k] + bi[k];
+          stv_act(e.out, BF16, (size_t)m * e.ldo + n, w);
+          unpack_bf16x8(oa[it], o);
+          head_sum(m, n, v, o);
+        });
+      } else {
+        for (int t = lane; t < 32 * QPR; t += 64) {
+          const int row = t / QPR, col = (t % QPR) * EW;
+          const int m = mb + row, n = nb + col;
+          float v[EW], o[EW];
+#pragma unroll
+          for (int k = 0; k < EW; k += 4) {
+            const float4 x = *reinterpret_cast<const float4*>(&ep[row * LDW + col + k]);
+            v[k] = x.x; v[k + 1] = x.y; v[k + 2] = x.z; v[k + 3] = x.w;
+          }
+          epilogue_v(e, g.M, g.N, m, n, v, vec);
+          if (m < g.M && n < g.N) ldv_act(e.aux, e.out_dtype, (size_t)m * e.ldaux + n, o);
+          else
+#pragma unroll
+            for (int k = 0; k < EW; ++k) o[k] = 0.f;
+          head_sum(m, n, v, o);
         }
       }
     } else if (e.kind == EPI_LOGITS) {
@@ -520,6 +579,46 @@ __device__ __forceinline__ void store_tile(const typename Mma<MF>::acc_t (&acc)[
           block_stats(m, n, v, v, mv);
         }
       }
+    } else if (vec && e.out_dtype == BF16 && (e.kind == EPI_SWIGLU_BWD || e.kind == EPI_GELU_BWD) &&
+               mb + 32 <= g.M && nb + TN <= g.N) {
+      // Interior rows, bf16: the activation inputs of all of this lane's
+      // column groups are loaded before any result is stored (the compiler
+      // must assume the stores may alias the loads, so loads placed between
+      // them would each wait a memory round trip).
+      constexpr int IT = 32 * QPR / 64;
+      static_assert(IT * 64 == 32 * QPR, "column groups must divide over the lanes");
+      const bool two = e.kind == EPI_SWIGLU_BWD;
+      uint4 xa[IT], xb[IT];
+      static_for<0, IT>([&](auto ic) __attribute__((always_inline)) {
+        constexpr int it = decltype(ic)::value;
+        const int t = lane + 64 * it, m = mb + t / QPR, n = nb + (t % QPR) * EW;
+        const bf16_t* ap = static_cast<const bf16_t*>(e.aux) + (size_t)m * e.ldaux + n;
+        xa[it] = *reinterpret_cast<const uint4*>(ap);
+        xb[it] = two ? *reinterpret_cast<const uint4*>(ap + e.ff) : make_uint4(0, 0, 0, 0);
+      });
+      static_for<0, IT>([&](auto ic) __attribute__((always_inline)) {
+        constexpr int it = decltype(ic)::value;
+        const int t = lane + 64 * it, row = t / QPR, col = (t % QPR) * EW;
+        const size_t mo = (size_t)(mb + row);
+        const int n = nb + col;
+        float v[EW], x[EW], r[EW];
+#pragma unroll
+        for (int k = 0; k < EW; k += 4) {
+          const float4 f = *reinterpret_cast<const float4*>(&ep[row * LDW + col + k]);
+          v[k] = f.x; v[k + 1] = f.y; v[k + 2] = f.z; v[k + 3] = f.w;
+        }
+        unpack_bf16x8(xa[it], x);
+        if (two) {
+          float u[EW], w[EW];
+          unpack_bf16x8(xb[it], u);
+          swiglu_bwd8(v, x, u, r, w);
+          stv_act(e.out, BF16, mo * e.ldo + n + e.ff, w);
+        } else {
+#pragma unroll
+          for (int k = 0; k < EW; ++k) r[k] = v[k] * gelu_grad_f(x[k]);
+        }
+        stv_act(e.out, BF16, mo * e.ldo + n, r);
+      });
     } else {
       for (int t = lane; t < 32 * QPR; t += 64) {
         const int row = t / QPR, col = (t % QPR) * EW;
