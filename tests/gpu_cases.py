@@ -135,6 +135,9 @@ BF16_CASES = {
     # and every label is its row's most likely token (p_y mostly 0.5-0.95)
     "1b_confident_logits": dict(shape=_cfg("1b", n_layers=1, batch=1, seq=512), head_scale=5.0,
                                 argmax_labels=True),
+    # a token count off every tile and 32-row epilogue block (200 rows): the
+    # epilogues' partial-block paths in bf16
+    "1b_ragged": dict(shape=_cfg("1b", n_layers=1, batch=1, seq=200)),
 }
 
 

@@ -251,6 +251,13 @@ def test_llama8b_bf16_two_layers_alpha1_sgd():
     _named("8b_two_layers_sgd")
 
 
+def test_llama1b_bf16_ragged_tokens():
+    """200 tokens: the last row tile and 32-row epilogue block of every GEMM
+    are partial (residual, RoPE, SwiGLU backward, delta and logit
+    epilogues)."""
+    _named("1b_ragged")
+
+
 def test_llama1b_bf16_confident_logits():
     """Logits up to about 30 with the label its row's most likely token:
     dL/dz = p - 1 at the label is a small difference of large terms, and the
