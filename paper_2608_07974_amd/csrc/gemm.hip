@@ -1099,12 +1099,14 @@ __device__ __forceinline__ void gemm_dma_body(const GemmDesc& g, const EpiArgs& 
   }
   wait_vmcnt<(PRO - 1) * PER_TILE>();
   __syncthreads();
-  // Fragments are double-buffered in registers: the LDS reads of the next
-  // k16 slice are issued before the MFMAs of the current one (scheduling
-  // fences keep that order).  The barrier that publishes tile kt+1 sits
-  // before the MFMAs of tile kt's last slice, whose fragments are already
-  // in registers, so slice 0 of tile kt+1 is read while they run and the
-  // barrier also certifies that every wave is done reading tile kt.
+  // The fragments of the next KS-deep slice are read while the current
+  // slice's MFMAs run (scheduling fences keep that order): into a second
+  // register buffer (MF 32), or into each fragment's own registers right
+  // after its last MFMA of the slice (MF 16).  The barrier that publishes
+  // tile kt+1 sits before the MFMAs of tile kt's last slice, whose
+  // fragments are already in registers, so slice 0 of tile kt+1 is read
+  // while they run and the barrier also certifies that every wave is done
+  // reading tile kt.
   bf16x8_t af[FB][FM], bfr[FB][FN];
 #pragma unroll
   for (int i = 0; i < FM; ++i) af[0][i] = fa.read(reinterpret_cast<const bf16_t*>(smem), 0, i);
