@@ -153,6 +153,14 @@ __device__ inline void wait_vm() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
+// This wave's copies of the oldest outstanding tile have landed once at
+// most `ahead` later tiles' copies (PER instructions each) are in flight.
+template <int PER>
+__device__ inline void wait_tiles(int ahead) {
+  if (ahead >= 2) wait_vm<2 * PER>();
+  else if (ahead == 1) wait_vm<PER>();
+  else wait_vm<0>();
+}
 
 template <int HD, int NT>
 struct TileDma {
@@ -205,6 +213,10 @@ __device__ inline CausalOrder causal_order() {
 // only on tiles that cross the diagonal or the end of the keys.
 constexpr int FW_WAVES = 8;
 constexpr int FW_NT = FW_WAVES * 64;
+#ifndef FW_NST
+#define FW_NST 2  // K/V tile stages of the forward and dQ kernels (3: slower)
+#endif
+static_assert(FW_NST >= 2 && FW_NST <= 4, "K/V pipeline depth");
 constexpr float RESCALE_TAU = 8.f;
 
 template <int HD, int HPW>
@@ -254,22 +266,25 @@ __global__ void __launch_bounds__(FW_NT) attn_fwd_mfma(AttnDesc a) {
   TileDma<HD, FW_NT> dk, dv;
   dk.init(lane, a.ldk);
   dv.init(lane, a.ldv);
-  const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>(smem);  // [2][K | V]
-  if (nt > 0) {
-    dk.issue(lds0, wave, 0, kend, rk);
-    dv.issue(lds0 + TB, wave, 0, kend, rv);
+  const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>(smem);  // [FW_NST][K | V]
+  // K/V tile t goes to stage t % FW_NST, FW_NST - 1 tiles ahead of its use
+  for (int p = 0; p < FW_NST - 1 && p < nt; ++p) {
+    dk.issue(lds0 + p * 2 * TB, wave, p * BT, kend, rk);
+    dv.issue(lds0 + p * 2 * TB + TB, wave, p * BT, kend, rv);
   }
+  int rd = 0, wr = FW_NST - 1;
   for (int t = 0; t < nt; ++t) {
     const int k0 = t * BT;
-    dma_wait();
-    __syncthreads();  // tile t everywhere; the other stage is no longer read
-    if (t + 1 < nt) {
-      const uint32_t nxt = lds0 + ((t + 1) & 1) * 2 * TB;
-      dk.issue(nxt, wave, k0 + BT, kend, rk);
-      dv.issue(nxt + TB, wave, k0 + BT, kend, rv);
+    wait_tiles<2 * TileDma<HD, FW_NT>::ITEMS>(min(FW_NST - 2, nt - 1 - t));
+    __syncthreads();  // tile t everywhere; stage wr (tile t - 1) is no longer read
+    if (t + FW_NST - 1 < nt) {
+      dk.issue(lds0 + wr * 2 * TB, wave, (t + FW_NST - 1) * BT, kend, rk);
+      dv.issue(lds0 + wr * 2 * TB + TB, wave, (t + FW_NST - 1) * BT, kend, rv);
     }
+    const bf16_t* kt = reinterpret_cast<const bf16_t*>(smem + rd * 2 * TB);
+    rd = rd + 1 == FW_NST ? 0 : rd + 1;
+    wr = wr + 1 == FW_NST ? 0 : wr + 1;
     if (k0 >= kend_w) continue;  // past every key this wave's queries see
-    const bf16_t* kt = reinterpret_cast<const bf16_t*>(smem + (t & 1) * 2 * TB);
     const bf16_t* vt = kt + BT * HD;
     // S^T: 8 independent accumulators per k-step; the K fragments of the
     // k-step two ahead are read while the current step's MFMAs run
@@ -672,22 +687,25 @@ __global__ void __launch_bounds__(FW_NT) attn_dq_mfma(AttnDesc a) {
   TileDma<HD, FW_NT> dkm, dvm;
   dkm.init(lane, a.ldk);
   dvm.init(lane, a.ldv);
-  const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>(smem);  // [2][K | V]
-  if (nt > 0) {
-    dkm.issue(lds0, wave, 0, kend, rk);
-    dvm.issue(lds0 + TB, wave, 0, kend, rv);
+  const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>(smem);  // [FW_NST][K | V]
+  // K/V tile t goes to stage t % FW_NST, FW_NST - 1 tiles ahead of its use
+  for (int p = 0; p < FW_NST - 1 && p < nt; ++p) {
+    dkm.issue(lds0 + p * 2 * TB, wave, p * BT, kend, rk);
+    dvm.issue(lds0 + p * 2 * TB + TB, wave, p * BT, kend, rv);
   }
+  int rd = 0, wr = FW_NST - 1;
   for (int t = 0; t < nt; ++t) {
     const int k0 = t * BT;
-    dma_wait();
-    __syncthreads();
-    if (t + 1 < nt) {
-      const uint32_t nxt = lds0 + ((t + 1) & 1) * 2 * TB;
-      dkm.issue(nxt, wave, k0 + BT, kend, rk);
-      dvm.issue(nxt + TB, wave, k0 + BT, kend, rv);
+    wait_tiles<2 * TileDma<HD, FW_NT>::ITEMS>(min(FW_NST - 2, nt - 1 - t));
+    __syncthreads();  // tile t everywhere; stage wr (tile t - 1) is no longer read
+    if (t + FW_NST - 1 < nt) {
+      dkm.issue(lds0 + wr * 2 * TB, wave, (t + FW_NST - 1) * BT, kend, rk);
+      dvm.issue(lds0 + wr * 2 * TB + TB, wave, (t + FW_NST - 1) * BT, kend, rv);
     }
+    const bf16_t* kt = reinterpret_cast<const bf16_t*>(smem + rd * 2 * TB);
+    rd = rd + 1 == FW_NST ? 0 : rd + 1;
+    wr = wr + 1 == FW_NST ? 0 : wr + 1;
     if (k0 >= kend_w) continue;
-    const bf16_t* kt = reinterpret_cast<const bf16_t*>(smem + (t & 1) * 2 * TB);
     const bf16_t* vt = kt + BT * HD;
     const bool masked = k0 + BT - 1 > qw0 || k0 + BT > kend;
     bf16x8_t dsk[2][2];
@@ -782,7 +800,7 @@ static hipError_t set_lds(Kern kern, size_t bytes) {
 
 template <int HD, int HPW>
 static hipError_t fwd_hpw(const AttnDesc& a, hipStream_t s) {
-  const size_t lds = (size_t)4 * BT * HD * sizeof(bf16_t);  // 2 stages x (K + V)
+  const size_t lds = (size_t)FW_NST * 2 * BT * HD * sizeof(bf16_t);  // stages x (K + V)
   static bool once = false;
   if (!once) {
     hipError_t e = set_lds(attn_fwd_mfma<HD, HPW>, lds);
@@ -805,7 +823,7 @@ static hipError_t fwd(const AttnDesc& a, hipStream_t s) {
 
 template <int HD, int HPW>
 static hipError_t dq_hpw(const AttnDesc& a, hipStream_t s) {
-  const size_t lds = (size_t)4 * BT * HD * sizeof(bf16_t);  // 2 stages x (K + V)
+  const size_t lds = (size_t)FW_NST * 2 * BT * HD * sizeof(bf16_t);  // stages x (K + V)
   static bool once = false;
   if (!once) {
     hipError_t e = set_lds(attn_dq_mfma<HD, HPW>, lds);
