@@ -164,12 +164,12 @@ __device__ inline void wait_tiles(int ahead) {
   else wait_vm<0>();
 }
 
-template <int HD, int NT>
+template <int HD, int NT, int ROWS = BT>
 struct TileDma {
   static constexpr int CH = HD / 8;              // 16-byte chunks per row
   static constexpr int RPI = 64 / CH;            // rows per copy instruction
-  static constexpr int ITEMS = BT * CH / NT;     // chunks per thread
-  static_assert(ITEMS >= 1 && ITEMS * NT == BT * CH, "tile chunks must divide over the threads");
+  static constexpr int ITEMS = ROWS * CH / NT;   // chunks per thread
+  static_assert(ITEMS >= 1 && ITEMS * NT == ROWS * CH, "tile chunks must divide over the threads");
   int rl, cl;       // lane's row within an instruction's rows, and its chunk
   uint32_t ldb;     // bytes per matrix row
   __device__ inline void init(int lane, int64_t ld) {
@@ -177,7 +177,7 @@ struct TileDma {
     cl = lane % CH;
     ldb = (uint32_t)ld * 2u;
   }
-  // rows r0 .. r0+BT-1 of the matrix (rows >= rvalid read as zero)
+  // rows r0 .. r0+ROWS-1 of the matrix (rows >= rvalid read as zero)
   __device__ inline void issue(uint32_t lds_byte, int wave, int r0, int rvalid, i32x4_t rsrc) const {
 #pragma unroll
     for (int j = 0; j < ITEMS; ++j) {
@@ -425,7 +425,7 @@ __global__ void __launch_bounds__(256) attn_delta_mfma(AttnDesc a) {
 // One workgroup per (KV_KB keys, kv-head): KV_WAVES waves (8) of 16 keys walk every
 // (q-head, query tile) pair of the kv group; the pair's Q and dO tiles are
 // copied direct-to-LDS once for all waves, KV_NST - 1 pairs ahead of use, with
-// the pair's 64 softmax statistics (lse, delta).  16 keys per wave keeps
+// the pair's softmax statistics (lse, delta of its KV_BQ queries).  16 keys per wave keeps
 // the K/V fragments and the fp32 dK/dV accumulators within two waves per
 // SIMD.
 #ifndef KV_WAVES
@@ -439,15 +439,20 @@ constexpr int KV_KB = KV_WAVES * 16;  // keys per workgroup
 #ifndef DKV_CA
 #define DKV_CA 3
 #endif
+#ifndef KV_BQ
+#define KV_BQ 128  // queries per (q-head, query tile) pair (64: 2 % slower)
+#endif
+static_assert(KV_BQ % 64 == 0, "query tiles of whole 64-row copies");
 template <int HD>
-constexpr size_t dkv_lds_bytes() {  // KV_NST x (Q | dO tiles, lse | delta of 64 queries)
-  return (size_t)KV_NST * (2 * BT * HD * 2 + 2 * BT * 4);
+constexpr size_t dkv_lds_bytes() {  // KV_NST x (Q | dO tiles, lse | delta of KV_BQ queries)
+  return (size_t)KV_NST * (2 * KV_BQ * HD * 2 + 2 * KV_BQ * 4);
 }
 
 template <int HD>
 __global__ void __launch_bounds__(KV_NT, 2) attn_dkv_mfma(AttnDesc a) {
-  constexpr uint32_t TB = BT * HD * 2;     // one Q or dO tile
-  constexpr uint32_t STAGE = 2 * TB + 2 * BT * 4;  // Q | dO | lse 64 | delta 64
+  constexpr int BQ = KV_BQ;
+  constexpr uint32_t TB = BQ * HD * 2;     // one Q or dO tile
+  constexpr uint32_t STAGE = 2 * TB + 2 * BQ * 4;  // Q | dO | lse | delta
   constexpr int NST = KV_NST;
   static_assert(NST >= 2 && NST <= 4 && NST * STAGE <= 160 * 1024, "pipeline depth");
   extern __shared__ __align__(16) unsigned char smem[];
@@ -483,10 +488,10 @@ __global__ void __launch_bounds__(KV_NT, 2) attn_dkv_mfma(AttnDesc a) {
   }
   const float cs = a.scale * LOG2E;
   // (q-head, query tile) pairs; a key block's query tiles start at k0
-  const int ntq = k0 < klim ? (a.S - k0 + BT - 1) / BT : 0;
+  const int ntq = k0 < klim ? (a.S - k0 + BQ - 1) / BQ : 0;
   const int npair = grp * ntq;
 
-  TileDma<HD, KV_NT> dq_, dd_;
+  TileDma<HD, KV_NT, BQ> dq_, dd_;
   dq_.init(lane, a.ldq);
   dd_.init(lane, a.lddo);
   const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>(smem);
@@ -494,27 +499,31 @@ __global__ void __launch_bounds__(KV_NT, 2) attn_dkv_mfma(AttnDesc a) {
   // Copies of pair pr into stage pr % NST: the Q and dO tiles (every wave
   // its share) and, by wave 0, the pair's lse and delta rows (one dword per
   // lane; queries past S read as zero)
-  constexpr int PER = 2 * TileDma<HD, KV_NT>::ITEMS;  // tile copies per wave and pair
+  constexpr int PER = 2 * TileDma<HD, KV_NT, BQ>::ITEMS;  // tile copies per wave and pair
+  constexpr int PST = 2 * (BQ / 64);                      // wave 0's statistics copies
   auto issue = [&](int pr, int stage) {
     const int h = kvh * grp + pr / ntq;
-    const int q0 = k0 + (pr % ntq) * BT;
+    const int q0 = k0 + (pr % ntq) * BQ;
     const uint32_t dst = lds0 + (uint32_t)stage * STAGE;
     dq_.issue(dst, wave, q0, a.S, buffer_rsrc(Q + rowb * a.ldq + (int64_t)h * HD));
     dd_.issue(dst + TB, wave, q0, a.S, buffer_rsrc(DO + rowb * a.lddo + (int64_t)h * HD));
     if (wave == 0) {
       const int64_t so = so_b + (int64_t)h * a.S;
       const uint32_t bytes = (uint32_t)a.S * 4u;
-      const uint32_t vo = (uint32_t)(q0 + lane) * 4u;
-      dma4(dst + 2 * TB, vo, buffer_rsrc_n(a.lse + so, bytes));
-      dma4(dst + 2 * TB + BT * 4, vo, buffer_rsrc_n(a.delta + so, bytes));
+#pragma unroll
+      for (int i = 0; i < BQ / 64; ++i) {
+        const uint32_t vo = (uint32_t)(q0 + 64 * i + lane) * 4u;
+        dma4(dst + 2 * TB + 256 * i, vo, buffer_rsrc_n(a.lse + so, bytes));
+        dma4(dst + 2 * TB + BQ * 4 + 256 * i, vo, buffer_rsrc_n(a.delta + so, bytes));
+      }
     }
   };
   // this wave's copies of pair pr have landed once at most `ahead` later
   // pairs' copies are still outstanding
   auto wait_pair = [&](int ahead) {
     if (wave == 0) {
-      if (ahead >= 2) wait_vm<2 * (PER + 2)>();
-      else if (ahead == 1) wait_vm<PER + 2>();
+      if (ahead >= 2) wait_vm<2 * (PER + PST)>();
+      else if (ahead == 1) wait_vm<PER + PST>();
       else wait_vm<0>();
     } else {
       if (ahead >= 2) wait_vm<2 * PER>();
@@ -522,7 +531,7 @@ __global__ void __launch_bounds__(KV_NT, 2) attn_dkv_mfma(AttnDesc a) {
       else wait_vm<0>();
     }
   };
-  static_assert(2 * (PER + 2) < 64, "vmcnt range");
+  static_assert(2 * (PER + PST) < 64, "vmcnt range");
   for (int p = 0; p < NST - 1 && p < npair; ++p) issue(p, p);
   int rd = 0, wr = NST - 1;  // stage read by pair pr, stage written for pair pr + NST - 1
 #pragma unroll 1
@@ -530,21 +539,22 @@ __global__ void __launch_bounds__(KV_NT, 2) attn_dkv_mfma(AttnDesc a) {
     wait_pair(min(NST - 2, npair - 1 - pr));
     __syncthreads();  // pair pr's copies everywhere; stage wr (read by pair pr - 1) is free
     if (pr + NST - 1 < npair) issue(pr + NST - 1, wr);
-    const int q0 = k0 + (pr % ntq) * BT;
+    const int q0 = k0 + (pr % ntq) * BQ;
     const unsigned char* sb = smem + rd * STAGE;
     rd = rd + 1 == NST ? 0 : rd + 1;
     wr = wr + 1 == NST ? 0 : wr + 1;
     const bf16_t* qt = reinterpret_cast<const bf16_t*>(sb);
-    const bf16_t* dt = qt + BT * HD;
+    const bf16_t* dt = qt + BQ * HD;
     const float* lss = reinterpret_cast<const float*>(sb + 2 * TB);  // lse (natural log)
-    const float* dls = lss + BT;
+    const float* dls = lss + BQ;
     // some key of the wave lies after some query of the tile, or keys or
     // queries run past their ends (every query before S sees key 0, so its
     // lse is finite; queries past S read lse = 0 and are masked)
-    const bool masked = kw0 + 15 > q0 || q0 + BT > a.S || kw0 + 16 > klim;
-    // Fragment reads run one step ahead of the MFMAs that use them: the Q /
-    // dO row fragments of the next 16-query block, and the transposed dO / Q
-    // column fragments of the next 16-wide dV / dK block (double-buffered).
+    const bool masked = kw0 + 15 > q0 || q0 + BQ > a.S || kw0 + 16 > klim;
+    // Fragment reads run ahead of the MFMAs that use them: the Q / dO row
+    // fragments of the next 16-query block (double-buffered), and the
+    // transposed dO / Q column fragments of the dV / dK update (a ring of
+    // DKV_CA reads in flight).
     bf16x8_t fq[2][HD / 32], fd[2][HD / 32];
 #pragma unroll
     for (int kk = 0; kk < HD / 32; ++kk) {
@@ -552,12 +562,12 @@ __global__ void __launch_bounds__(KV_NT, 2) attn_dkv_mfma(AttnDesc a) {
       fd[0][kk] = frag_row<HD>(dt, c, g + 4 * kk);
     }
 #pragma unroll
-    for (int half = 0; half < 2; ++half) {
+    for (int half = 0; half < BQ / 32; ++half) {
       bf16x8_t pk, dsk;
 #pragma unroll
       for (int qq = 0; qq < 2; ++qq) {
         const int qb = 2 * half + qq, cur = qb & 1;
-        if (qb + 1 < 4) {
+        if (qb + 1 < BQ / 16) {
 #pragma unroll
           for (int kk = 0; kk < HD / 32; ++kk) {
             fq[cur ^ 1][kk] = frag_row<HD>(qt, (qb + 1) * 16 + c, g + 4 * kk);
