@@ -216,6 +216,7 @@ def _attn_inputs(B, S, Hq, Hkv, hd, lens, seed):
     (2, 37, 4, 2, 16, [37, 20]),
     (1, 130, 8, 2, 64, [130]),
     (2, 200, 4, 4, 128, [200, 77]),
+    (1, 300, 4, 1, 128, [300]),
     (1, 5, 2, 1, 64, [0]),
     (3, 64, 2, 2, 32, [1, 64, 63]),
 ])
