@@ -900,10 +900,12 @@ __device__ inline void dma16(uint32_t lds_byte, uint32_t voff, i32x4_t rsrc) {
 __device__ inline void dma_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // K-major LDS rows of BK elements: 16-B chunk c of row r sits at
-// c ^ ((r / (128 / BK)) % (BK / 8)), so the 16 lanes of one LDS cycle (16
-// consecutive rows, one chunk each) hit 16 distinct 16-byte bank groups.
+// c ^ ((r / 2) % (BK / 8)) for BK <= 64 (c ^ (r % 16) for BK 128).  A
+// fragment read (16 consecutive rows, one chunk each, per 16 lanes) then
+// takes 4 LDS cycles with no bank conflict, measured on gfx950 at BK 64 and
+// 32; at BK 32 (64-byte rows) the earlier c ^ ((r / 4) % 4) took 8.
 template <int BK>
-__device__ inline int kswz(int row) { return (row / (128 / BK)) % (BK / 8); }
+__device__ inline int kswz(int row) { return (row / (BK <= 64 ? 2 : 128 / BK)) % (BK / 8); }
 
 // One operand's BK-deep k tile, R rows of M (or N), copied by NT threads.
 template <int R, int BK, int NT, bool KMAJ, int MF = 32>
@@ -978,8 +980,8 @@ struct FragTile {
 
   __device__ inline void init(int wrow, int lane) {
     if (KMAJ) {
-      // fragment rows step by MF, which keeps kswz (period 128/BK rows x
-      // BK/8 chunks = 16 rows) unchanged: fragment i adds i * MF * BK
+      // fragment rows step by MF, which keeps kswz (period 2 x BK/8 rows,
+      // at most 16) unchanged: fragment i adds i * MF * BK
       const int l = lane & (MF - 1), h = lane / MF, sw = kswz<BK>(l);
 #pragma unroll
       for (int q = 0; q < NS; ++q) off[q] = (wrow + l) * BK + ((((KS / 8) * q + h) ^ sw) * 8);
