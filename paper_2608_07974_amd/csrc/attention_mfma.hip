@@ -43,18 +43,19 @@ __device__ inline f32x4_t mfma16(bf16x8_t a, bf16x8_t b, f32x4_t c) {
 }
 
 // XOR permutation of a row's 16-byte chunks in LDS.  Two read shapes use a
-// tile: row fragments (16 bytes per lane, rows 16m + c) and transposed
-// column fragments (ds_read_b64_tr_b16, 8 rows per half-wave, two adjacent
-// chunks per row).  Measured on gfx950 with 256-byte rows (head size 128),
-// `row & 15` serves row reads in 4 LDS cycles and transpose reads in 4 (2-way
-// conflict); permutations that put a half-wave's 8 rows in distinct 32-byte
-// groups serve transpose reads in 2 but row reads in 8, and the attention
-// kernels issue two transpose reads per row read or fewer, so `row & 15`
-// stays.  With 128-byte rows (head size 64), `row & 7` leaves both shapes
-// free of bank conflicts, where `(row >> 1) & 7` conflicted on both.
+// tile: row fragments (16 bytes per lane, rows 16m + c, chunk 4kk + g for
+// lane 16g + c) and transposed column fragments (ds_read_b64_tr_b16, 8 rows
+// per half-wave, two adjacent chunks per row).  Measured on gfx950: a 16-byte
+// read serves in one cycle the 16 lanes that share lane bit 5 and the parity
+// of lane bits 2-4, and a transpose read a half-wave.  Both are then free of
+// bank conflicts when, at 256-byte rows (head size 128), the permutation
+// shifted left by one keeps a half-wave's 8 rows in distinct 32-byte groups
+// and x -> swz(x) ^ (bit 2 ^ bit 3 of x) stays one-to-one on 16 rows:
+// `(row & 7) << 1`.  `row & 15` cost the transpose reads a 2-way conflict.
+// At 128-byte rows (head size 64), `row & 7` meets both.
 template <int HD>
 __device__ inline int swz(int row) {
-  return HD == 128 ? (row & 15) : (row & 7);
+  return HD == 128 ? ((row & 7) << 1) : (row & 7);
 }
 
 __device__ inline bf16x8_t zero8() {
